@@ -1,0 +1,15 @@
+"""CPU oracle for FP64 matrix multiplication through Ozaki scheme II on base-13 E2M1 limbs.
+
+TEST INFRASTRUCTURE ONLY. Nothing in the product path may import, call or
+execute this package: only ``tests/``, ``__graft_entry__.smoke()`` and the
+``cpu_baseline`` leg of ``bench.py`` use it. It shares no code, tables or
+constants with the HIP library; every constant here is re-derived from the
+paper's definitions.
+
+Parity status: every function is pinned by ``tests/test_oracle_*.py`` against
+values the paper prints, closed forms, invariants and brute force on tiny
+inputs. No function is "parity unpinned".
+"""
+
+from .ozaki2_fp4 import *  # noqa: F401,F403
+from .ozaki2_fp4 import __all__  # noqa: F401

@@ -1,0 +1,132 @@
+"""Plant plausible mistakes in the oracle (CPU only) and check that the pins
+catch each one: a dropped term, a wrong weight, a sign slip, a transposed
+operand, a wrong rounding mode."""
+
+import numpy as np
+import pytest
+
+import oracle as o
+from oracle import ozaki2_fp4 as mod
+
+
+def _tiny_mismatch():
+    """True when the residue route disagrees with the exact definition on a
+    few tiny matrices (the brute-force pin), or raises an internal check."""
+    rng = np.random.default_rng(1)
+    for _ in range(4):
+        m, n, k = 3, 4, 5
+        A = (rng.random((m, k)) - 0.5) * np.exp2(rng.integers(-30, 30, size=(m, k)))
+        B = (rng.random((k, n)) - 0.5) * np.exp2(rng.integers(-30, 30, size=(k, n)))
+        try:
+            got = o.dgemm(A, B, 14)["C"]
+        except (AssertionError, ValueError):
+            return True
+        if not np.array_equal(got, o.dgemm_definition(A, B, 14)):
+            return True
+    return False
+
+
+def _round_trip_fails():
+    try:
+        for m in o.select_moduli(20):
+            for r in range(m):
+                c0, c1 = o.two_limb_split(r, m)
+                d0 = int(2 * o.e2m1_decode(o.e2m1_code(c0)))
+                d1 = int(2 * o.e2m1_decode(o.e2m1_code(c1)))
+                if (d0 + 13 * d1 - r) % m or abs(d0) > 8 or abs(d1) > 8:
+                    return True
+    except (ValueError, KeyError):
+        return True
+    return False
+
+
+def test_unmutated_oracle_passes():
+    assert not _tiny_mismatch()
+    assert not _round_trip_fails()
+
+
+def test_wrong_composition_weight_is_caught(monkeypatch):
+    orig = mod.residue_products
+
+    def bad(Ai, Bi, m):
+        out = orig(Ai, Bi, m)
+        out["r"] = np.mod(out["G0"] + 169 * out["G1"] + 13 * out["G2"], m)   # weights swapped
+        return out
+    monkeypatch.setattr(mod, "residue_products", bad)
+    assert _tiny_mismatch()
+
+
+def test_dropped_cross_term_is_caught(monkeypatch):
+    def bad(Ai, Bi, m):
+        a0, a1 = o.limb_planes(Ai, m)
+        b0, b1 = o.limb_planes(Bi, m)
+        G0 = a0 @ b0
+        G1 = a0 @ b1                       # a1 b0 dropped
+        G2 = a1 @ b1
+        return {"G0": G0, "G1": G1, "G2": G2, "r": np.mod(G0 + 13 * G1 + 169 * G2, m)}
+    monkeypatch.setattr(mod, "residue_products", bad)
+    assert _tiny_mismatch()
+
+
+def test_transposed_operand_is_caught(monkeypatch):
+    def bad(Ai, Bi, m):
+        a0, a1 = o.limb_planes(Ai, m)
+        b0, b1 = o.limb_planes(Bi, m)
+        G0 = a0 @ b0
+        G1 = a0 @ b1 + (b0.T @ a1.T).T[:, ::-1]     # wrong operand orientation
+        G2 = a1 @ b1
+        return {"G0": G0, "G1": G1, "G2": G2, "r": np.mod(G0 + 13 * G1 + 169 * G2, m)}
+    monkeypatch.setattr(mod, "residue_products", bad)
+    assert _tiny_mismatch()
+
+
+def test_missing_symmetric_map_is_caught(monkeypatch):
+    def bad(res, moduli):
+        P = o.moduli_product(moduli)
+        w = o.crt_weights(moduli)
+        S = sum(np.asarray(r, dtype=np.int64).astype(object) * wi for r, wi in zip(res, w))
+        return np.vectorize(lambda v: v % P, otypes=[object])(S)      # no x - P
+    monkeypatch.setattr(mod, "crt_reconstruct", bad)
+    assert _tiny_mismatch()
+
+
+def test_greedy_without_replacement_is_caught(monkeypatch):
+    monkeypatch.setattr(mod, "greedy_digit", lambda x: (x + 6) % 13 - 6)   # emits +-5
+    assert _round_trip_fails()
+
+
+def test_truncating_conversion_is_caught(monkeypatch):
+    def bad(X, shifts, axis):
+        sh = shifts[:, None] if axis == 1 else shifts[None, :]
+        return np.trunc(np.ldexp(X, sh.astype(np.int64))).astype(np.int64)
+    monkeypatch.setattr(mod, "to_integers", bad)
+    # the conversion pin compares against exact half-to-even rounding
+    X = np.array([[2.5, -3.7, 1e-3, 0.3]])
+    s = o.shift_exponents(X, axis=1, c=3)
+    assert not np.array_equal(mod.to_integers(X, s, axis=1), o.to_integers_fraction(X, s, axis=1))
+
+
+def test_off_by_one_exponent_is_caught(monkeypatch):
+    monkeypatch.setattr(mod, "floor_log2", lambda x: int(np.frexp(abs(x))[1]))   # e instead of e-1
+    X = np.array([[3.0, 1.0]])
+    # shift must take the row maximum into [2^(c-1), 2^c)
+    s = o.shift_exponents(X, axis=1, c=10)
+    v = o.to_integers(X, s, axis=1)
+    assert not (2 ** 9 <= np.max(np.abs(v)) <= 2 ** 10)
+
+
+def test_wrong_modulus_order_is_caught(monkeypatch, paper):
+    monkeypatch.setattr(mod, "select_moduli", lambda L: sorted(o.two_limb_moduli())[:L])
+    assert mod.select_moduli(19) != paper["moduli_L19"]
+
+
+@pytest.mark.parametrize("bad_code", [{6: 6, 8: 5}, {1: 2, 2: 1}])
+def test_wrong_e2m1_code_table_is_caught(monkeypatch, bad_code):
+    table = dict(mod._CODE_OF_MAG)
+    table.update(bad_code)
+    monkeypatch.setattr(mod, "_CODE_OF_MAG", table)
+    bad = False
+    for c in o.doubled_set():
+        if int(2 * o.e2m1_decode(o.e2m1_code(c))) != c:
+            bad = True
+    assert bad
