@@ -1,0 +1,264 @@
+"""Benchmark of the Ozaki-II-on-FP4 FP64 matrix product on one MI355X.
+
+A step is one ozfp4_dgemm call on the m = n = k = 16384 workload (entries
+(U(0,1) - 0.5) exp(0.5 N(0,1)), fixed seed, inputs resident in HBM): line
+maxima and shifts, fused conversion + residues + limb encoding of A and of
+B, the fused residue GEMM over all moduli, and the exact CRT
+reconstruction. The printed JSON line carries the emulated-DGEMM rate
+2 m n k / t, the residue GEMM against the FP4 matrix-core peak (stage time
+measured with HIP events on the library's stream over the timed steps), the
+CPU oracle timed on a bounded sample, a per-stage breakdown, native FP64
+matrix product on the same GPU and the INT8-on-FP4 path as context.
+
+Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--moduli L]
+                       [--size N] [--sweep] [--no-cpu-baseline] [--no-native]
+"""
+
+from __future__ import annotations
+
+import argparse
+import json
+import math
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+FP4_PEAK_TFLOPS = 10100.0       # MI355X dense FP4 matrix peak (published)
+FP64_PEAK_TFLOPS = 78.6         # MI355X FP64 matrix peak (published)
+HBM_PEAK_GBS = 8000.0
+METRIC = "emulated DGEMM TFLOPS at N=16384 + % of FP4 MFMA peak, 1xMI355X"
+SEED = 20260806
+
+
+def log(msg: str) -> None:
+    print(f"[bench] {msg}", file=sys.stderr, flush=True)
+
+
+def dev_cm(X, torch):
+    import numpy as np
+    return torch.from_numpy(np.ascontiguousarray(X.T)).to("cuda").t()
+
+
+def time_dgemm(ozfp4, torch, Ad, Bd, C, L, steps, warmup, profile=True):
+    """Median-free protocol of the contract: W untimed calls, then K calls
+    bracketed by synchronisations. Returns (ms per step, mean stage ms)."""
+    for _ in range(warmup):
+        ozfp4.dgemm(Ad, Bd, L, out=C)
+    torch.cuda.synchronize()
+    ozfp4.ozfp4_profile(profile)
+    stage_sum = None
+    t0 = time.perf_counter()
+    for _ in range(steps):
+        ozfp4.dgemm(Ad, Bd, L, out=C)
+        if profile:
+            st = ozfp4.ozfp4_stage_times()
+            stage_sum = st if stage_sum is None else [a + b for a, b in zip(stage_sum, st)]
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    ozfp4.ozfp4_profile(False)
+    stages = [s / steps for s in stage_sum] if stage_sum else None
+    return (t1 - t0) * 1e3 / steps, stages
+
+
+def cpu_baseline(A, B, L, k, budget_s=12.0):
+    """The oracle, as it stands, on a bounded sample of output elements of
+    the same workload (whole rows of A and columns of B at full k)."""
+    import numpy as np
+
+    import oracle
+    try:
+        from threadpoolctl import threadpool_info
+        blas_threads = max([d.get("num_threads", 1) for d in threadpool_info()] or [1])
+    except Exception:  # noqa: BLE001
+        blas_threads = 1
+    side = 4
+    elapsed = 0.0
+    done = 0
+    while True:
+        rows = np.arange(side)
+        cols = np.arange(side)
+        t0 = time.perf_counter()
+        oracle.dgemm(A, B, L, rows=rows, cols=cols)
+        dt = time.perf_counter() - t0
+        elapsed, done = dt, side * side
+        if dt > budget_s / 4 or side >= 64:
+            break
+        side *= 2
+    tflops = 2.0 * k * done / elapsed / 1e12
+    return {"value": tflops, "unit": "TFLOP/s (emulated DGEMM)", "cores": blas_threads,
+            "kind": "oracle",
+            "sample": f"{side}x{side} output block of the {A.shape[0]}x{B.shape[1]}x{k} workload at full k, "
+                      f"{L} moduli, {elapsed:.2f} s"}
+
+
+def accuracy_bits(C_np, A, B, rows, cols):
+    import oracle
+    worst = 0.0
+    for a, i in enumerate(rows):
+        for b, j in enumerate(cols):
+            worst = max(worst, oracle.normalized_error(float(C_np[a, b]), A, B, int(i), int(j)))
+    return (-math.log2(worst) if worst > 0 else float("inf")), worst
+
+
+def main() -> int:
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=12)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--moduli", type=int, default=18)
+    ap.add_argument("--size", type=int, default=16384)
+    ap.add_argument("--sweep", action="store_true", help="sweep 12..20 moduli at the given size")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-native", action="store_true")
+    ap.add_argument("--no-int8", action="store_true")
+    ap.add_argument("--no-accuracy", action="store_true")
+    args = ap.parse_args()
+
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print("bench.py measures one GPU: this method has no multi-GPU path "
+              "(the output tiles and moduli would shard without communication; see DESIGN.md)",
+              file=sys.stderr)
+        return 2
+
+    import numpy as np
+    import torch
+
+    from paper_2608_06812_amd import ozfp4
+    from paper_2608_06812_amd.workloads import dgemm_inputs, int8_inputs
+
+    ozfp4.load()
+    if not torch.cuda.is_available():
+        raise RuntimeError("bench.py needs a GPU")
+    torch.cuda.set_device(0)
+    N = args.size
+    L = args.moduli
+
+    log(f"generating inputs {N}^3")
+    A, B = dgemm_inputs(N, N, N, 0.5, SEED + 2)
+    Ad, Bd = dev_cm(A, torch), dev_cm(B, torch)
+    C = torch.empty_strided((N, N), (1, N), dtype=torch.float64, device="cuda")
+
+    if args.sweep:
+        rng = np.random.default_rng(7)
+        rows = np.sort(rng.choice(N, 4, replace=False))
+        cols = np.sort(rng.choice(N, 4, replace=False))
+        out = []
+        for Ls in range(12, 21):
+            ms, st = time_dgemm(ozfp4, torch, Ad, Bd, C, Ls, max(2, args.steps // 3), 1)
+            Cs = C[torch.as_tensor(rows, device="cuda")][:, torch.as_tensor(cols, device="cuda")].cpu().numpy()
+            bits, worst = accuracy_bits(Cs, A, B, rows, cols)
+            rec = {"n_moduli": Ls, "ms": ms, "tflops": 2.0 * N ** 3 / ms / 1e9,
+                   "gemm_ms": st[3], "error_bits": bits, "fp64_accurate": worst <= 2.0 ** -50}
+            log(json.dumps(rec))
+            out.append(rec)
+        print(json.dumps({"sweep": out, "size": N}))
+        return 0
+
+    log(f"timing ozfp4_dgemm, {L} moduli")
+    ms, stages = time_dgemm(ozfp4, torch, Ad, Bd, C, L, args.steps, args.warmup)
+    value = 2.0 * N ** 3 / ms / 1e9
+    gemm_ms = stages[3]
+    flops_exec = 4 * L * 2.0 * N ** 3
+    flops_req = (4 * L - 1) * 2.0 * N ** 3
+    achieved = flops_exec / gemm_ms / 1e9
+    stage_names = ["scale", "encode_A", "encode_B", "residue_gemm", "crt"]
+
+    # memory-bound stages: algorithmic bytes per call
+    bytes_scale = 8.0 * (N * N + N * N)
+    bytes_enc = 8.0 * N * N + 2 * L * N * N / 2.0   # per operand: read FP64, write 2L planes
+    bytes_crt = L * N * N + 8.0 * N * N
+    hbm = {
+        "scale_GBs": bytes_scale / stages[0] / 1e6,
+        "encode_A_GBs": bytes_enc / stages[1] / 1e6,
+        "encode_B_GBs": bytes_enc / stages[2] / 1e6,
+        "crt_GBs": bytes_crt / stages[4] / 1e6,
+    }
+    # runtime model t = 2 Q N^3 / R + D / beta (Eq. (model)) at the published peaks
+    D = bytes_scale + 2 * bytes_enc + L * N * N + bytes_crt
+    model_ms = (flops_exec / (FP4_PEAK_TFLOPS * 1e12) + D / (HBM_PEAK_GBS * 1e9)) * 1e3
+
+    result = {
+        "metric": METRIC, "value": value, "unit": "TFLOP/s", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": ms,
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": "f64 (FP4 E2M1 MFMA, FP32 accumulate, exact integer CRT)",
+        "data": "synthetic: (U(0,1)-0.5)*exp(0.5*N(0,1)), seed %d" % (SEED + 2),
+        "config": {"workload": f"dgemm m=n=k={N}, phi=0.5", "m": N, "n": N, "k": N,
+                   "n_moduli": L, "parallelism": "single GPU"},
+        "roofline": {"bound": "mfma", "kernel": "k_gemm_res", "achieved": achieved,
+                     "peak": FP4_PEAK_TFLOPS, "unit": "TFLOP/s", "frac": achieved / FP4_PEAK_TFLOPS,
+                     "traffic": None, "flops_per_launch": flops_exec,
+                     "frac_required_basis": flops_req / gemm_ms / 1e9 / FP4_PEAK_TFLOPS,
+                     "avg_launch_ms": gemm_ms},
+        "stages_ms": dict(zip(stage_names, stages)),
+        "hbm_GBs": hbm,
+        "model_ms": model_ms,
+        "compute_stage_tflops": 2.0 * N ** 3 / (gemm_ms + stages[4]) / 1e9,
+    }
+
+    if not args.no_accuracy:
+        rng = np.random.default_rng(11)
+        rows = np.sort(rng.choice(N, 3, replace=False))
+        cols = np.sort(rng.choice(N, 3, replace=False))
+        Cs = C[torch.as_tensor(rows, device="cuda")][:, torch.as_tensor(cols, device="cuda")].cpu().numpy()
+        bits, _ = accuracy_bits(Cs, A, B, rows, cols)
+        result["accuracy_bits_sample"] = bits
+
+    if not args.no_native:
+        log("timing native FP64 torch.matmul")
+        Ar = Ad.contiguous() if False else torch.from_numpy(A).to("cuda")
+        Br = torch.from_numpy(B).to("cuda")
+        for _ in range(2):
+            torch.matmul(Ar, Br)
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        reps = 5
+        for _ in range(reps):
+            torch.matmul(Ar, Br)
+        torch.cuda.synchronize()
+        nms = (time.perf_counter() - t0) * 1e3 / reps
+        result["native_fp64"] = {"ms": nms, "tflops": 2.0 * N ** 3 / nms / 1e9,
+                                 "speedup_of_emulation": nms / ms}
+        del Ar, Br
+
+    if not args.no_int8:
+        log("timing ozfp4_igemm_s8 8192^3")
+        del Ad, Bd, C
+        torch.cuda.empty_cache()
+        A8, B8 = int8_inputs(8192, 8192, 8192, SEED + 40)
+        A8d, B8d = dev_cm(A8, torch), dev_cm(B8, torch)
+        C8 = torch.empty_strided((8192, 8192), (1, 8192), dtype=torch.int32, device="cuda")
+        for _ in range(2):
+            ozfp4.igemm_s8(A8d, B8d, out=C8)
+        torch.cuda.synchronize()
+        ozfp4.ozfp4_profile(True)
+        reps = 5
+        gsum = 0.0
+        t0 = time.perf_counter()
+        for _ in range(reps):
+            ozfp4.igemm_s8(A8d, B8d, out=C8)
+            gsum += ozfp4.ozfp4_stage_times()[2]
+        torch.cuda.synchronize()
+        ims = (time.perf_counter() - t0) * 1e3 / reps
+        ozfp4.ozfp4_profile(False)
+        gms = gsum / reps
+        result["int8"] = {"workload": "igemm_s8 m=n=k=8192", "ms": ims,
+                          "tops": 2.0 * 8192 ** 3 / ims / 1e9,
+                          "gemm_ms": gms, "fp4_tflops_gemm": 9 * 2.0 * 8192 ** 3 / gms / 1e9,
+                          "fp4_frac": 9 * 2.0 * 8192 ** 3 / gms / 1e9 / FP4_PEAK_TFLOPS}
+
+    if not args.no_cpu_baseline:
+        log("timing the CPU oracle on a sample")
+        result["cpu_baseline"] = cpu_baseline(A, B, L, N)
+
+    print(json.dumps(result), flush=True)
+    return 0
+
+
+if __name__ == "__main__":
+    sys.exit(main())

@@ -1,0 +1,189 @@
+/*
+ * ozfp4 -- FP64 matrix multiplication emulated with Ozaki scheme II on the
+ * FP4 (E2M1) matrix cores of AMD Instinct MI355X (gfx950), through base-13
+ * E2M1 limbs; plus a bit-exact INT8 x INT8 -> INT32 matrix product built on
+ * the same limbs.
+ *
+ * Method: Hayashi, Mukunoki, Hoshino, Katagiri, "DGEMM with Ozaki Scheme I/II
+ * on FP4 Tensor Cores: A Base-13 E2M1 Limb Representation".
+ *
+ * Conventions shared by every entry point
+ *   - BLAS "NN", column-major: C (m x n) = A (m x k) * B (k x n); element
+ *     (i, j) of A is A[i + j*lda]. lda >= max(1, m), ldb >= max(1, k),
+ *     ldc >= max(1, m). C is overwritten (no alpha/beta).
+ *   - Matrix pointers are DEVICE pointers on the current HIP device, owned by
+ *     the caller. They may be null only when the matrix has no elements.
+ *   - Work is issued on the stream set by ozfp4_set_stream (default: the null
+ *     stream). Calls that read back a status synchronize that stream and say
+ *     so below.
+ *   - The library owns a per-device workspace (limb planes, residues,
+ *     exponents) that grows on demand and is released by ozfp4_finalize.
+ *     Calls are not thread-safe and calls that overlap on one device race on
+ *     that workspace.
+ *   - Every entry point returns OZFP4_OK (0) or a negative error code; argument
+ *     errors are detected on the host before any GPU work is issued.
+ */
+#ifndef OZFP4_H
+#define OZFP4_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* Error codes. */
+#define OZFP4_OK           0
+#define OZFP4_EINVAL      -1  /* bad size, leading dimension or null pointer      */
+#define OZFP4_EMODULI     -2  /* n_moduli outside [2, 20], or too few moduli for k */
+#define OZFP4_EKBOUND     -3  /* k above the FP32-exactness bound                  */
+#define OZFP4_ENONFINITE  -4  /* NaN or Inf in A or B; C is unspecified            */
+#define OZFP4_ENOMEM      -5  /* device workspace allocation failed                */
+#define OZFP4_EHIP        -6  /* a HIP runtime call failed                         */
+
+#define OZFP4_MIN_MODULI   2
+#define OZFP4_MAX_MODULI  20
+/* With greedy limbs |c| <= 8 every prefix of the three residue accumulators
+ * (the cross term holds two products per k) is a multiple of 1/4 of
+ * magnitude <= 2^22, exact in FP32, for k <= 131072 (Lemma 2, Lemma 3). */
+#define OZFP4_MAX_K       131072
+/* INT8 path: the deepest limb group holds three products per k, so every
+ * prefix stays exact in FP32 for k <= 2^24 / (3 * 64) = 87381. */
+#define OZFP4_MAX_K_S8     87381
+
+/*
+ * ozfp4_dgemm -- C = fl(A B) for FP64 A, B by Ozaki scheme II on FP4 limbs
+ * (Sec. IV-B scaling, Sec. V-A moduli and two-limb residues, Sec. V-B exact
+ * direct CRT, Sec. VI-D fused residue GEMM).
+ *
+ * Computes, for every (i, j),
+ *     C_ij = RN( (sum_k A~_ik B~_kj) * 2^-(s_i + t_j) )
+ * where A~_ik = round_half_even(A_ik 2^s_i) with one shift per row of A and
+ * B~_kj likewise with one shift per column of B (Sec. IV-B). The shifts put
+ * each row (column) maximum into [2^(c-1), 2^c] with capacities c_A, c_B
+ * chosen from k and the moduli: b is the largest integer with
+ * 2 k 2^b < P = prod m_l (Eq. (crt)), c_A = min(53, ceil(b/2)),
+ * c_B = min(53, b - c_A); an all-zero row or column has shift 0. The
+ * integer product is exact; the only roundings are the conversion and one
+ * final round-to-nearest-even (subnormal results and overflow to +-inf
+ * included).
+ *
+ * n_moduli: number L of moduli, 2..20; the moduli are the first L of the
+ *   greedy pairwise-coprime list 169, 115, 113, 112, ..., 53 (Sec. V-A),
+ *   with 47 as the 20th. The paper uses L = 19.
+ * Returns OZFP4_EMODULI when L moduli cannot hold k (b < 2), OZFP4_EKBOUND
+ * for k > OZFP4_MAX_K, OZFP4_ENONFINITE if A or B holds NaN/Inf.
+ * k == 0 writes zeros to C; m == 0 or n == 0 does nothing.
+ * Synchronizes the stream before returning (it reads the non-finite flag).
+ */
+int ozfp4_dgemm(int64_t m, int64_t n, int64_t k,
+                const double* A, int64_t lda,
+                const double* B, int64_t ldb,
+                double* C, int64_t ldc, int n_moduli);
+
+/*
+ * ozfp4_igemm_s8 -- C = A B for INT8 A, B with INT32 C, bit-exact, on FP4
+ * limbs (Sec. III): every int8 splits into three greedy base-13 limbs
+ * (X_3 = 732 >= 128), the nine limb products run as FP4 matrix products
+ * grouped by i + j with FP32 accumulation (exact by the bound above), and
+ * C = sum_g 13^g * 4 * G_g is formed in wrapping int32 arithmetic, i.e. C
+ * equals the integer product reduced modulo 2^32 into [-2^31, 2^31) exactly
+ * like INT32 accumulation.
+ * Returns OZFP4_EKBOUND for k > OZFP4_MAX_K_S8. k == 0 writes zeros.
+ * Asynchronous on the set stream.
+ */
+int ozfp4_igemm_s8(int64_t m, int64_t n, int64_t k,
+                   const int8_t* A, int64_t lda,
+                   const int8_t* B, int64_t ldb,
+                   int32_t* C, int64_t ldc);
+
+/* Stream for subsequent calls (a hipStream_t; NULL = the null stream). */
+int ozfp4_set_stream(void* stream);
+
+/* Releases every device workspace and table of the library. */
+int ozfp4_finalize(void);
+
+/* Static message for an error code. */
+const char* ozfp4_strerror(int code);
+
+/* ---- host-only queries (no GPU work; usable without a device) ---------- */
+
+/* Writes the first n_moduli moduli (Sec. V-A greedy order) to the HOST array
+ * out[n_moduli]. */
+int ozfp4_moduli(int n_moduli, int32_t* out);
+
+/* Capacities (c_A, c_B) used for inner dimension k with n_moduli moduli
+ * (see ozfp4_dgemm). HOST pointers. */
+int ozfp4_capacity(int64_t k, int n_moduli, int32_t* c_a, int32_t* c_b);
+
+/* Canonical two-limb split of every residue r in [0, m_l) of modulus l
+ * (index in the greedy list): HOST array out[m_l] of bytes, E2M1 code of
+ * c0 in the low nibble and of c1 in the high nibble, where
+ * c0 + 13 c1 = r (mod m_l). The split takes the representative r' of r in
+ * (-m/2, m/2], splits it greedily (smallest-magnitude digit mod 13, +-5
+ * replaced by -+8, Lemma 2) and, when that fails (m = 115, r' = +-57),
+ * moves r' by one m toward the other sign first (Sec. V-A example
+ * -58 = 13(-4) - 6). E2M1 codes: magnitudes 0, .5, 1, 1.5, 2, 3, 4, 6 are
+ * codes 0..7, sign bit 0x8; a limb c is stored as the value c/2. */
+int ozfp4_two_limb_table(int modulus_index, uint8_t* out, int32_t* m_out);
+
+/* Layout of the packed FP4 limb planes (the debug hook below returns them):
+ * lines (rows of A, columns of B) are padded to rows_pad, k to k_pad, and
+ * one plane holds rows_pad * k_pad / 2 bytes. */
+int ozfp4_plane_layout(int64_t lines, int64_t k, int64_t* rows_pad,
+                       int64_t* k_pad, int64_t* bytes_per_plane);
+
+/* ---- parity hooks: the same kernels as ozfp4_dgemm, stopped early ------ */
+
+/*
+ * ozfp4_scales -- the shifts s (m, per row of A) and t (n, per column of B)
+ * of ozfp4_dgemm for this k and n_moduli (Sec. IV-B). s and t are DEVICE
+ * int32 arrays. Synchronizes (non-finite check).
+ */
+int ozfp4_scales(int64_t m, int64_t n, int64_t k,
+                 const double* A, int64_t lda, const double* B, int64_t ldb,
+                 int n_moduli, int32_t* s, int32_t* t);
+
+/*
+ * ozfp4_limb_planes -- the packed E2M1 limb planes of ozfp4_dgemm
+ * (Sec. V-A two-limb residues, Sec. VI-B fused encoder), DEVICE buffers of
+ * 2 * n_moduli * bytes_per_plane bytes each (ozfp4_plane_layout with the
+ * line count m for A and n for B).
+ * Plane p = 2 l + h holds limb h (0: c0, 1: c1) of modulus l. Inside a plane
+ * the bytes are grouped in 1024-byte fragments of 32 lines x 64 k:
+ * fragment (rb, kb) starts at ((rb * (k_pad / 64)) + kb) * 1024; byte
+ * lane * 16 + j of a fragment, lane in [0, 64), j in [0, 16), holds line
+ * rb * 32 + lane % 32 and k = kb * 64 + (lane / 32) * 32 + 2 j (low nibble)
+ * and 2 j + 1 (high nibble). Padding lines and k hold code 0.
+ * Synchronizes.
+ */
+int ozfp4_limb_planes(int64_t m, int64_t n, int64_t k,
+                      const double* A, int64_t lda, const double* B, int64_t ldb,
+                      int n_moduli, uint8_t* planes_a, uint8_t* planes_b);
+
+/*
+ * ozfp4_residues -- the residue matrices r_l = (A~ B~) mod m_l in [0, m_l)
+ * that the fused residue GEMM writes (Sec. V-A, Sec. VI-D): DEVICE bytes,
+ * R[l * ldr * n + i + j * ldr] for l < n_moduli, ldr >= m. Synchronizes.
+ */
+int ozfp4_residues(int64_t m, int64_t n, int64_t k,
+                   const double* A, int64_t lda, const double* B, int64_t ldb,
+                   int n_moduli, uint8_t* R, int64_t ldr);
+
+/* ---- stage timing ------------------------------------------------------ */
+
+/* Enable (1) or disable (0) HIP-event timing of the stages of the next
+ * ozfp4_dgemm / ozfp4_igemm_s8 calls, recorded on the library's stream. */
+int ozfp4_profile(int enable);
+
+/* Milliseconds of each stage of the last profiled call, written to the HOST
+ * array ms[max]; returns the stage count (>= 0) or an error. dgemm stages:
+ * 0 scale, 1 encode A, 2 encode B, 3 residue GEMM, 4 CRT. igemm_s8 stages:
+ * 0 encode A, 1 encode B, 2 GEMM. Synchronizes. */
+int ozfp4_stage_times(double* ms, int max, int* n_stages);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* OZFP4_H */

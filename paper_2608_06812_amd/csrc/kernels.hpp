@@ -1,0 +1,675 @@
+// gfx950 kernels of the Ozaki-II-on-FP4 path. Included by ozfp4.hip only.
+//
+// Data layout (HBM):
+//   * limb planes: per operand, plane p holds one limb of one modulus for
+//     every (line, k); it is a sequence of 1 KiB fragments of 32 lines x 64 k
+//     in the exact register order of the A/B operand of
+//     v_mfma_scale_f32_32x32x64_f8f6f4 in FP4 mode (lane = line % 32 +
+//     32 * (k / 32 % 2), 16 bytes per lane, two E2M1 codes per byte, low
+//     nibble first). A wave therefore moves a fragment with one 16-byte
+//     load per lane, coalesced in HBM and conflict-free in LDS. Fragments
+//     of one 32-line block are contiguous along k.
+//   * residues: one byte per (modulus, i, j), column-major per modulus with
+//     the padded row count as leading dimension.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "tables.hpp"
+
+namespace ozfp4 {
+
+typedef int v4i __attribute__((ext_vector_type(4)));
+typedef int v8i __attribute__((ext_vector_type(8)));
+typedef float v16f __attribute__((ext_vector_type(16)));
+
+constexpr int kFragLines = 32;   // lines per fragment
+constexpr int kFragK = 64;       // k per fragment
+constexpr int kFragBytes = 1024;
+constexpr int kTile = 128;       // GEMM block tile (lines of A and of B)
+constexpr int kStageK = 128;     // k per pipeline stage (two fragments)
+
+constexpr uint64_t kAbsMask = 0x7fffffffffffffffull;
+constexpr uint64_t kNonFinite = 0x7ff0000000000000ull;
+
+// ------------------------------------------------------------ Sec. IV-B
+// floor(log2 |x|) from the bit pattern of the line maximum |x| (finite,
+// nonzero), subnormals included; shift c - 1 - e, or 0 for a zero line.
+__device__ __forceinline__ int line_shift(uint64_t amax_bits, int cap) {
+  if (amax_bits == 0) return 0;
+  int ex = (int)(amax_bits >> 52);
+  int e;
+  if (ex == 0) {
+    uint64_t mant = amax_bits & 0x000fffffffffffffull;
+    e = (63 - __clzll((long long)mant)) - 1074;
+  } else {
+    e = ex - 1023;
+  }
+  return cap - 1 - e;
+}
+
+__global__ void k_fill_u64(uint64_t* __restrict__ p, int64_t n, uint64_t v) {
+  int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i < n) p[i] = v;
+}
+
+__global__ void k_fill_f64_matrix(double* __restrict__ C, int64_t m, int64_t n, int64_t ldc) {
+  int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (t < m * n) C[(t % m) + (t / m) * ldc] = 0.0;
+}
+
+__global__ void k_fill_i32_matrix(int32_t* __restrict__ C, int64_t m, int64_t n, int64_t ldc) {
+  int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (t < m * n) C[(t % m) + (t / m) * ldc] = 0;
+}
+
+// Row maxima of |X| for lines that are adjacent in memory (X[line + kk*ld]):
+// one thread per line over a chunk of kk, then a 64-bit atomic max of the
+// bit patterns (for non-negative doubles the integer order of the patterns
+// is the numeric order; NaN/Inf patterns sort above every finite value).
+constexpr int kAmaxChunk = 256;
+__global__ __launch_bounds__(256) void k_amax_adjacent_lines(
+    const double* __restrict__ X, int64_t ld, int64_t lines, int64_t k,
+    unsigned long long* __restrict__ amax, int* __restrict__ flag) {
+  int64_t line = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (line >= lines) return;
+  int64_t k0 = (int64_t)blockIdx.y * kAmaxChunk;
+  int64_t k1 = min(k, k0 + kAmaxChunk);
+  const uint64_t* p = reinterpret_cast<const uint64_t*>(X) + line;
+  uint64_t mx = 0;
+  int64_t kk = k0;
+  for (; kk + 4 <= k1; kk += 4) {
+    uint64_t a = p[kk * ld] & kAbsMask, b = p[(kk + 1) * ld] & kAbsMask;
+    uint64_t c = p[(kk + 2) * ld] & kAbsMask, d = p[(kk + 3) * ld] & kAbsMask;
+    mx = max(mx, max(max(a, b), max(c, d)));
+  }
+  for (; kk < k1; ++kk) mx = max(mx, p[kk * ld] & kAbsMask);
+  if (mx >= kNonFinite) *flag = 1;
+  if (mx) atomicMax(&amax[line], (unsigned long long)mx);
+}
+
+// Maxima of |X| for lines contiguous in memory (X[kk + line*ld]): one wave
+// per (line, chunk of 4096 k), a wave-wide max, one atomic per wave.
+constexpr int kAmaxContigChunk = 4096;
+__global__ __launch_bounds__(256) void k_amax_contig_lines(
+    const double* __restrict__ X, int64_t ld, int64_t lines, int64_t k,
+    unsigned long long* __restrict__ amax, int* __restrict__ flag) {
+  int64_t line = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+  int lane = threadIdx.x & 63;
+  if (line >= lines) return;
+  int64_t k0 = (int64_t)blockIdx.y * kAmaxContigChunk;
+  int64_t k1 = min(k, k0 + kAmaxContigChunk);
+  const uint64_t* p = reinterpret_cast<const uint64_t*>(X) + line * ld;
+  uint64_t mx = 0;
+  int64_t kk = k0 + lane;
+  for (; kk + 192 < k1; kk += 256) {
+    uint64_t a = p[kk] & kAbsMask, b = p[kk + 64] & kAbsMask;
+    uint64_t c = p[kk + 128] & kAbsMask, d = p[kk + 192] & kAbsMask;
+    mx = max(mx, max(max(a, b), max(c, d)));
+  }
+  for (; kk < k1; kk += 64) mx = max(mx, p[kk] & kAbsMask);
+#pragma unroll
+  for (int off = 32; off >= 1; off >>= 1) {
+    uint64_t o = __shfl_xor(mx, off, 64);
+    mx = max(mx, o);
+  }
+  if (lane == 0) {
+    if (mx >= kNonFinite) *flag = 1;
+    if (mx) atomicMax(&amax[line], (unsigned long long)mx);
+  }
+}
+
+__global__ void k_shifts(const uint64_t* __restrict__ amax, int64_t lines, int cap,
+                         int32_t* __restrict__ out) {
+  int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i < lines) out[i] = line_shift(amax[i], cap);
+}
+
+// ------------------------------------------------------------ Sec. V-A / VI-B
+// Fused integer conversion, residues for every modulus, canonical two-limb
+// split and E2M1 packing. One wave per fragment (32 lines x 64 k); lane
+// (line % 32, k half) converts its 32 values once, then for each modulus
+// reduces them, looks the codes up in an LDS table and stores 16 bytes to
+// each of the two planes of that modulus.
+//   x = |round_half_even(X * 2^s)| < 2^53 is exact in FP64; for each m the
+//   estimate q = floor(x * fl(1/m)) is within one of floor(x / m), so
+//   r = x - q m (exact FMA) lies in [-m, 2m) and indexes a table that
+//   already folds the correction and the sign of X.
+constexpr int kEncWaves = 4;
+__global__ __launch_bounds__(256) void k_encode_dgemm(
+    const double* __restrict__ X, int64_t rs, int64_t ks, int64_t lines, int64_t k,
+    const uint64_t* __restrict__ amax, int cap, uint8_t* __restrict__ planes,
+    int64_t plane_bytes, int64_t nfrag, int64_t kblocks, int L,
+    const ModConst* __restrict__ mc, const uint16_t* __restrict__ lut, int lut_entries) {
+  extern __shared__ uint16_t s_lut[];
+  for (int i = threadIdx.x; i < lut_entries; i += 256) s_lut[i] = lut[i];
+  __syncthreads();
+  const int lane = threadIdx.x & 63;
+  const int wave = threadIdx.x >> 6;
+  for (int64_t f = (int64_t)blockIdx.x * kEncWaves + wave; f < nfrag;
+       f += (int64_t)gridDim.x * kEncWaves) {
+    const int64_t rb = f / kblocks, kb = f - rb * kblocks;
+    const int64_t line = rb * kFragLines + (lane & 31);
+    const int64_t kbase = kb * kFragK + (lane >> 5) * 32;
+    const bool live = line < lines;
+    const int s = live ? line_shift(amax[line], cap) : 0;
+    double x[32];
+    uint32_t neg = 0;
+    const double* src = X + line * rs;
+#pragma unroll
+    for (int e = 0; e < 32; ++e) {
+      const int64_t kk = kbase + e;
+      double v = (live && kk < k) ? src[kk * ks] : 0.0;
+      double t = __builtin_rint(__builtin_ldexp(v, s));
+      neg |= (t < 0.0 ? 1u : 0u) << e;
+      double a = __builtin_fabs(t);
+      // finite inputs give a <= 2^53; NaN/Inf (reported by the scale stage)
+      // must not drive the table index out of range
+      x[e] = (a <= 9007199254740992.0) ? a : 0.0;
+    }
+    uint8_t* out = planes + f * kFragBytes + lane * 16;
+    for (int l = 0; l < L; ++l) {
+      const int m = mc->m[l];
+      const double inv = mc->inv[l];
+      const double md = mc->md[l];
+      const uint16_t* T = s_lut + mc->lut_off[l] + m;
+      const int m3 = 3 * m;
+      uint32_t w0[4], w1[4];
+#pragma unroll
+      for (int g = 0; g < 4; ++g) {
+        uint32_t t4[2];
+#pragma unroll
+        for (int h = 0; h < 2; ++h) {
+          uint32_t acc = 0;
+#pragma unroll
+          for (int e4 = 0; e4 < 4; ++e4) {
+            const int e = g * 8 + h * 4 + e4;
+            double q = __builtin_floor(x[e] * inv);
+            int ri = (int)__builtin_fma(-q, md, x[e]);
+            int idx = ri + (((neg >> e) & 1u) ? m3 : 0);
+            uint32_t E = T[idx];
+            acc |= E << (4 * (e4 & 1) + 16 * (e4 >> 1));
+          }
+          t4[h] = acc;
+        }
+        w0[g] = (t4[0] & 0xffu) | ((t4[0] >> 8) & 0xff00u) | ((t4[1] & 0xffu) << 16) |
+                ((t4[1] << 8) & 0xff000000u);
+        w1[g] = ((t4[0] >> 8) & 0xffu) | ((t4[0] >> 16) & 0xff00u) | ((t4[1] & 0xff00u) << 8) |
+                (t4[1] & 0xff000000u);
+      }
+      v4i p0 = {(int)w0[0], (int)w0[1], (int)w0[2], (int)w0[3]};
+      v4i p1 = {(int)w1[0], (int)w1[1], (int)w1[2], (int)w1[3]};
+      *reinterpret_cast<v4i*>(out + (int64_t)(2 * l) * plane_bytes) = p0;
+      *reinterpret_cast<v4i*>(out + (int64_t)(2 * l + 1) * plane_bytes) = p1;
+    }
+  }
+}
+
+// INT8 encoder (Sec. III): three greedy limbs per value from a 256-entry
+// table (codes of c0, c1, c2 in bits 0-3, 4-7, 8-11), three planes.
+__global__ __launch_bounds__(256) void k_encode_s8(
+    const int8_t* __restrict__ X, int64_t rs, int64_t ks, int64_t lines, int64_t k,
+    uint8_t* __restrict__ planes, int64_t plane_bytes, int64_t nfrag, int64_t kblocks,
+    const uint16_t* __restrict__ lut8) {
+  __shared__ uint16_t s_lut[256];
+  s_lut[threadIdx.x] = lut8[threadIdx.x];
+  __syncthreads();
+  const int lane = threadIdx.x & 63;
+  const int wave = threadIdx.x >> 6;
+  for (int64_t f = (int64_t)blockIdx.x * kEncWaves + wave; f < nfrag;
+       f += (int64_t)gridDim.x * kEncWaves) {
+    const int64_t rb = f / kblocks, kb = f - rb * kblocks;
+    const int64_t line = rb * kFragLines + (lane & 31);
+    const int64_t kbase = kb * kFragK + (lane >> 5) * 32;
+    const bool live = line < lines;
+    const int8_t* src = X + line * rs;
+    uint32_t w[3][4];
+#pragma unroll
+    for (int g = 0; g < 4; ++g) {
+      uint32_t a0 = 0, a1 = 0, a2 = 0;
+#pragma unroll
+      for (int e8 = 0; e8 < 8; ++e8) {
+        const int64_t kk = kbase + g * 8 + e8;
+        int v = (live && kk < k) ? (int)src[kk * ks] : 0;
+        uint32_t E = s_lut[v + 128];
+        a0 |= (E & 0xfu) << (4 * e8);
+        a1 |= ((E >> 4) & 0xfu) << (4 * e8);
+        a2 |= ((E >> 8) & 0xfu) << (4 * e8);
+      }
+      w[0][g] = a0;
+      w[1][g] = a1;
+      w[2][g] = a2;
+    }
+    uint8_t* out = planes + f * kFragBytes + lane * 16;
+#pragma unroll
+    for (int p = 0; p < 3; ++p) {
+      v4i v = {(int)w[p][0], (int)w[p][1], (int)w[p][2], (int)w[p][3]};
+      *reinterpret_cast<v4i*>(out + (int64_t)p * plane_bytes) = v;
+    }
+  }
+}
+
+// ------------------------------------------------------------ Sec. VI-D
+// Block tile index -> (modulus, tile row, tile column). Consecutive block
+// ids go to the 8 XCDs round-robin; remap so that each XCD walks a
+// contiguous range of logical tiles, and order tiles in groups of kGroupM
+// tile rows so that the blocks an XCD runs together share A and B panels
+// in its L2.
+constexpr int kGroupM = 4;
+__device__ __forceinline__ void tile_coords(int64_t bid, int64_t nblocks, int64_t tiles_m,
+                                            int64_t tiles_n, int* l, int64_t* tm, int64_t* tn) {
+  const int64_t xcd = bid & 7, local = bid >> 3;
+  const int64_t base = nblocks >> 3, rem = nblocks & 7;
+  const int64_t logical = xcd * base + min(xcd, rem) + local;
+  const int64_t T = tiles_m * tiles_n;
+  *l = (int)(logical / T);
+  const int64_t t = logical - (int64_t)(*l) * T;
+  const int64_t group = t / (kGroupM * tiles_n);
+  const int64_t first = group * kGroupM;
+  const int64_t gm = min(tiles_m - first, (int64_t)kGroupM);
+  const int64_t in = t - group * kGroupM * tiles_n;
+  *tm = first + in % gm;
+  *tn = in / gm;
+}
+
+__device__ __forceinline__ v16f mfma_fp4(v4i a, v4i b, v16f c) {
+  v8i a8 = {a.x, a.y, a.z, a.w, 0, 0, 0, 0};
+  v8i b8 = {b.x, b.y, b.z, b.w, 0, 0, 0, 0};
+  // cbsz = blgp = 4: both operands E2M1; E8M0 scales 127 = 2^0
+  return __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(a8, b8, c, 4, 4, 0, 127, 0, 127);
+}
+
+// Fused limb-product GEMM over a 128 x 128 block tile, k in stages of 128.
+// NP planes per operand; product (i, j) of plane i of A and plane j of B is
+// accumulated into accumulator acc_index(i, j). Four waves, each 64 x 64
+// (2 x 2 MFMA tiles of 32 x 32). LDS holds two stages (double buffer);
+// global -> register -> LDS staging, one stage ahead.
+//   LDS stage layout: [operand][plane][32-line block 0..3][k fragment 0..1]
+//   x 1 KiB.
+template <int NP>
+struct StageLayout {
+  static constexpr int kBytes = 2 * NP * 4 * 2 * kFragBytes;
+  static constexpr int kChunks = kBytes / 16;            // 16-byte pieces
+  static constexpr int kPerThread = kChunks / 256;       // 4 * NP
+  __device__ static constexpr int frag(int op, int p, int rbl, int kbl) {
+    return (((op * NP + p) * 4 + rbl) * 2 + kbl) * kFragBytes;
+  }
+};
+
+// Dgemm variant: planes 2l (c0) and 2l+1 (c1) of modulus l; accumulators
+// acc0 = a0 b0, acc1 = a0 b1 + a1 b0, acc2 = a1 b1; epilogue
+// r = (4 acc0 + 52 acc1 + 676 acc2) mod m, one byte per element.
+__global__ __launch_bounds__(256, 1) void k_gemm_res(
+    const uint8_t* __restrict__ PA, const uint8_t* __restrict__ PB, uint8_t* __restrict__ R,
+    int64_t plane_a, int64_t plane_b, int64_t kblocks, int64_t tiles_m, int64_t tiles_n,
+    int64_t nblocks, int64_t ldr, int64_t rplane, const ModConst* __restrict__ mc) {
+  constexpr int NP = 2;
+  using SL = StageLayout<NP>;
+  __shared__ __attribute__((aligned(16))) uint8_t lds[2 * SL::kBytes];
+
+  int l;
+  int64_t tm, tn;
+  tile_coords(blockIdx.x, nblocks, tiles_m, tiles_n, &l, &tm, &tn);
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int wm = wave >> 1, wn = wave & 1;
+
+  // source of chunk q of this thread in stage s: piece = tid & 63,
+  // kbl = (tid >> 6) & 1, rbl = ((tid >> 7) & 1) + 2 (q & 1),
+  // plane = (q >> 1) % NP, op = (q >> 1) / NP
+  // uniform part of each source (plane, tile, 64-line half) + one
+  // per-thread offset
+  const int64_t toff = (((tid >> 7) & 1) * kblocks + ((tid >> 6) & 1)) * kFragBytes + (tid & 63) * 16;
+  const uint8_t* gbase[SL::kPerThread];
+#pragma unroll
+  for (int q = 0; q < SL::kPerThread; ++q) {
+    const int p = (q >> 1) % NP, op = (q >> 1) / NP;
+    const int64_t rb0 = (op == 0 ? tm : tn) * 4 + 2 * (q & 1);
+    gbase[q] = (op == 0 ? PA + (int64_t)(2 * l + p) * plane_a : PB + (int64_t)(2 * l + p) * plane_b) +
+               rb0 * kblocks * kFragBytes;
+  }
+  const int nst = (int)(kblocks / 2);
+
+  v16f acc[3][2][2];
+#pragma unroll
+  for (int a = 0; a < 3; ++a)
+#pragma unroll
+    for (int i = 0; i < 2; ++i)
+#pragma unroll
+      for (int j = 0; j < 2; ++j)
+#pragma unroll
+        for (int v = 0; v < 16; ++v) acc[a][i][j][v] = 0.0f;
+
+  v4i stage[SL::kPerThread];
+#pragma unroll
+  for (int q = 0; q < SL::kPerThread; ++q) stage[q] = *reinterpret_cast<const v4i*>(gbase[q] + toff);
+#pragma unroll
+  for (int q = 0; q < SL::kPerThread; ++q)
+    *reinterpret_cast<v4i*>(lds + (q * 256 + tid) * 16) = stage[q];
+  __syncthreads();
+
+  for (int s = 0; s < nst; ++s) {
+    const int buf = s & 1;
+    if (s + 1 < nst) {
+#pragma unroll
+      for (int q = 0; q < SL::kPerThread; ++q)
+        stage[q] = *reinterpret_cast<const v4i*>(gbase[q] + toff + (int64_t)(s + 1) * 2 * kFragBytes);
+    }
+    const uint8_t* sb = lds + buf * SL::kBytes;
+#pragma unroll
+    for (int kbl = 0; kbl < 2; ++kbl) {
+      v4i a[NP][2], b[NP][2];
+#pragma unroll
+      for (int p = 0; p < NP; ++p)
+#pragma unroll
+        for (int i = 0; i < 2; ++i) {
+          a[p][i] = *reinterpret_cast<const v4i*>(sb + SL::frag(0, p, 2 * wm + i, kbl) + lane * 16);
+          b[p][i] = *reinterpret_cast<const v4i*>(sb + SL::frag(1, p, 2 * wn + i, kbl) + lane * 16);
+        }
+#pragma unroll
+      for (int i = 0; i < 2; ++i)
+#pragma unroll
+        for (int j = 0; j < 2; ++j) {
+          acc[0][i][j] = mfma_fp4(a[0][i], b[0][j], acc[0][i][j]);
+          acc[1][i][j] = mfma_fp4(a[0][i], b[1][j], acc[1][i][j]);
+          acc[2][i][j] = mfma_fp4(a[1][i], b[1][j], acc[2][i][j]);
+        }
+#pragma unroll
+      for (int i = 0; i < 2; ++i)
+#pragma unroll
+        for (int j = 0; j < 2; ++j) acc[1][i][j] = mfma_fp4(a[1][i], b[0][j], acc[1][i][j]);
+    }
+    if (s + 1 < nst) {
+      uint8_t* db = lds + (buf ^ 1) * SL::kBytes;
+#pragma unroll
+      for (int q = 0; q < SL::kPerThread; ++q)
+        *reinterpret_cast<v4i*>(db + (q * 256 + tid) * 16) = stage[q];
+    }
+    __syncthreads();
+  }
+
+  // epilogue: residue composition mod m (Sec. V-A, Lemma 3)
+  const int m = mc->m[l];
+  const double inv = mc->inv[l], md = mc->md[l];
+  uint8_t* Rl = R + (int64_t)l * rplane;
+#pragma unroll
+  for (int i = 0; i < 2; ++i)
+#pragma unroll
+    for (int j = 0; j < 2; ++j) {
+      const int64_t col = tn * kTile + wn * 64 + j * 32 + (lane & 31);
+#pragma unroll
+      for (int g = 0; g < 4; ++g) {
+        const int64_t row = tm * kTile + wm * 64 + i * 32 + g * 8 + (lane >> 5) * 4;
+        uint32_t word = 0;
+#pragma unroll
+        for (int v4 = 0; v4 < 4; ++v4) {
+          const int v = g * 4 + v4;
+          double d = 4.0 * (double)acc[0][i][j][v] + 52.0 * (double)acc[1][i][j][v] +
+                     676.0 * (double)acc[2][i][j][v];
+          double qd = __builtin_floor(d * inv);
+          int r = (int)__builtin_fma(-qd, md, d);
+          r += (r < 0) ? m : 0;
+          r -= (r >= m) ? m : 0;
+          word |= (uint32_t)r << (8 * v4);
+        }
+        *reinterpret_cast<uint32_t*>(Rl + col * ldr + row) = word;
+      }
+    }
+}
+
+// INT8 variant: three planes per operand, five accumulators G_g (g = i + j),
+// epilogue C = sum_g 13^g * 4 G_g in wrapping int32. Block tile 128 x 64,
+// four waves of 64 x 32 (2 x 1 MFMA tiles) so the five accumulator sets stay
+// in registers. LDS stage: A [plane][32-line block 0..3][k fragment] then
+// B [plane][32-line block 0..1][k fragment], 1 KiB each.
+constexpr int kTileS8N = 64;
+__global__ __launch_bounds__(256, 1) void k_gemm_s8(
+    const uint8_t* __restrict__ PA, const uint8_t* __restrict__ PB, int32_t* __restrict__ C,
+    int64_t plane_a, int64_t plane_b, int64_t kblocks, int64_t tiles_m, int64_t tiles_n,
+    int64_t nblocks, int64_t m, int64_t n, int64_t ldc) {
+  constexpr int NP = 3;
+  constexpr int kABytes = NP * 4 * 2 * kFragBytes;   // 24 KiB
+  constexpr int kBBytes = NP * 2 * 2 * kFragBytes;   // 12 KiB
+  constexpr int kStage = kABytes + kBBytes;
+  constexpr int kPerA = kABytes / 16 / 256;          // 6
+  constexpr int kPerB = kBBytes / 16 / 256;          // 3
+  __shared__ __attribute__((aligned(16))) uint8_t lds[2 * kStage];
+
+  int l;
+  int64_t tm, tn;
+  tile_coords(blockIdx.x, nblocks, tiles_m, tiles_n, &l, &tm, &tn);
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int wm = wave >> 1, wn = wave & 1;
+
+  // A piece q: plane q >> 1, 32-line block ((q & 1) << 1) | ((tid >> 7) & 1);
+  // B piece q: plane q, 32-line block (tid >> 7) & 1; both k fragment
+  // (tid >> 6) & 1 and 16-byte piece tid & 63.
+  const int64_t toffA = (((tid >> 7) & 1) * kblocks + ((tid >> 6) & 1)) * kFragBytes + (tid & 63) * 16;
+  const int64_t toffB = toffA;
+  const uint8_t* gA[kPerA];
+  const uint8_t* gB[kPerB];
+#pragma unroll
+  for (int q = 0; q < kPerA; ++q)
+    gA[q] = PA + (int64_t)(q >> 1) * plane_a + (tm * 4 + 2 * (q & 1)) * kblocks * kFragBytes;
+#pragma unroll
+  for (int q = 0; q < kPerB; ++q) gB[q] = PB + (int64_t)q * plane_b + tn * 2 * kblocks * kFragBytes;
+  const int nst = (int)(kblocks / 2);
+
+  v16f acc[5][2];
+#pragma unroll
+  for (int a = 0; a < 5; ++a)
+#pragma unroll
+    for (int i = 0; i < 2; ++i)
+#pragma unroll
+      for (int v = 0; v < 16; ++v) acc[a][i][v] = 0.0f;
+
+  v4i sa[kPerA], sbv[kPerB];
+#pragma unroll
+  for (int q = 0; q < kPerA; ++q) sa[q] = *reinterpret_cast<const v4i*>(gA[q] + toffA);
+#pragma unroll
+  for (int q = 0; q < kPerB; ++q) sbv[q] = *reinterpret_cast<const v4i*>(gB[q] + toffB);
+#pragma unroll
+  for (int q = 0; q < kPerA; ++q) *reinterpret_cast<v4i*>(lds + (q * 256 + tid) * 16) = sa[q];
+#pragma unroll
+  for (int q = 0; q < kPerB; ++q) *reinterpret_cast<v4i*>(lds + kABytes + (q * 256 + tid) * 16) = sbv[q];
+  __syncthreads();
+
+  for (int s = 0; s < nst; ++s) {
+    const int buf = s & 1;
+    if (s + 1 < nst) {
+      const int64_t adv = (int64_t)(s + 1) * 2 * kFragBytes;
+#pragma unroll
+      for (int q = 0; q < kPerA; ++q) sa[q] = *reinterpret_cast<const v4i*>(gA[q] + toffA + adv);
+#pragma unroll
+      for (int q = 0; q < kPerB; ++q) sbv[q] = *reinterpret_cast<const v4i*>(gB[q] + toffB + adv);
+    }
+    const uint8_t* sb = lds + buf * kStage;
+#pragma unroll
+    for (int kbl = 0; kbl < 2; ++kbl) {
+      v4i a[NP][2], b[NP];
+#pragma unroll
+      for (int p = 0; p < NP; ++p) {
+#pragma unroll
+        for (int i = 0; i < 2; ++i)
+          a[p][i] = *reinterpret_cast<const v4i*>(sb + ((p * 4 + 2 * wm + i) * 2 + kbl) * kFragBytes + lane * 16);
+        b[p] = *reinterpret_cast<const v4i*>(sb + kABytes + ((p * 2 + wn) * 2 + kbl) * kFragBytes + lane * 16);
+      }
+#pragma unroll
+      for (int pa = 0; pa < NP; ++pa)
+#pragma unroll
+        for (int pb = 0; pb < NP; ++pb)
+#pragma unroll
+          for (int i = 0; i < 2; ++i) acc[pa + pb][i] = mfma_fp4(a[pa][i], b[pb], acc[pa + pb][i]);
+    }
+    if (s + 1 < nst) {
+      uint8_t* db = lds + (buf ^ 1) * kStage;
+#pragma unroll
+      for (int q = 0; q < kPerA; ++q) *reinterpret_cast<v4i*>(db + (q * 256 + tid) * 16) = sa[q];
+#pragma unroll
+      for (int q = 0; q < kPerB; ++q) *reinterpret_cast<v4i*>(db + kABytes + (q * 256 + tid) * 16) = sbv[q];
+    }
+    __syncthreads();
+  }
+
+  const int64_t col = tn * kTileS8N + wn * 32 + (lane & 31);
+#pragma unroll
+  for (int i = 0; i < 2; ++i)
+#pragma unroll
+    for (int v = 0; v < 16; ++v) {
+      const int64_t row = tm * kTile + wm * 64 + i * 32 + (v >> 2) * 8 + (lane >> 5) * 4 + (v & 3);
+      uint32_t c = (uint32_t)(int)(4.0f * acc[0][i][v]);
+      c += 13u * (uint32_t)(int)(4.0f * acc[1][i][v]);
+      c += 169u * (uint32_t)(int)(4.0f * acc[2][i][v]);
+      c += 2197u * (uint32_t)(int)(4.0f * acc[3][i][v]);
+      c += 28561u * (uint32_t)(int)(4.0f * acc[4][i][v]);
+      if (row < m && col < n) C[row + col * ldc] = (int32_t)c;
+    }
+}
+
+// ------------------------------------------------------------ Sec. V-B
+// Exact direct CRT and the single final rounding.
+__device__ __forceinline__ uint64_t word3(uint64_t w0, uint64_t w1, uint64_t w2, int i) {
+  return i == 0 ? w0 : (i == 1 ? w1 : (i == 2 ? w2 : 0ull));
+}
+
+// low 64 bits of (w >> sh), sh >= 1
+__device__ __forceinline__ uint64_t shr3(uint64_t w0, uint64_t w1, uint64_t w2, int sh) {
+  if (sh >= 192) return 0;
+  const int ws = sh >> 6, bs = sh & 63;
+  const uint64_t lo = word3(w0, w1, w2, ws), hi = word3(w0, w1, w2, ws + 1);
+  return bs ? ((lo >> bs) | (hi << (64 - bs))) : lo;
+}
+
+__device__ __forceinline__ int bit3(uint64_t w0, uint64_t w1, uint64_t w2, int b) {
+  if (b >= 192) return 0;
+  return (int)((word3(w0, w1, w2, b >> 6) >> (b & 63)) & 1ull);
+}
+
+// any of bits [0, b) set
+__device__ __forceinline__ bool below3(uint64_t w0, uint64_t w1, uint64_t w2, int b) {
+  if (b <= 0) return false;
+  if (b >= 192) return (w0 | w1 | w2) != 0;
+  const int ws = b >> 6, bs = b & 63;
+  uint64_t acc = 0;
+  if (ws > 0) acc |= w0;
+  if (ws > 1) acc |= w1;
+  const uint64_t part = word3(w0, w1, w2, ws);
+  if (bs) acc |= part & ((1ull << bs) - 1);
+  return acc != 0;
+}
+
+// RN_even(M * 2^e2) for the 192-bit magnitude M, with sign
+__device__ __forceinline__ double round_scaled(uint64_t w0, uint64_t w1, uint64_t w2, int e2,
+                                               bool neg) {
+  if ((w0 | w1 | w2) == 0) return 0.0;
+  const int n = w2 ? 192 - __clzll((long long)w2)
+                   : (w1 ? 128 - __clzll((long long)w1) : 64 - __clzll((long long)w0));
+  const int E = n - 1 + e2;
+  double r;
+  if (E > 1023) {
+    r = __builtin_inf();
+  } else {
+    const int qe = max(E - 52, -1074);
+    const int sh = qe - e2;
+    if (sh <= 0) {
+      r = __builtin_ldexp((double)w0, e2);  // M < 2^53: exact
+    } else {
+      uint64_t Rm = shr3(w0, w1, w2, sh);
+      const int rb = bit3(w0, w1, w2, sh - 1);
+      const bool st = below3(w0, w1, w2, sh - 1);
+      if (rb && (st || (Rm & 1ull))) ++Rm;
+      r = __builtin_ldexp((double)Rm, qe);  // Rm <= 2^53: exact or +inf
+    }
+  }
+  return neg ? -r : r;
+}
+
+__device__ __forceinline__ double crt_finish(const double sig[4], double Qe,
+                                             const CrtConst* __restrict__ cc, int e2) {
+  const double q = __builtin_rint(Qe);        // nearest integer to S / P
+  int64_t v[4];
+#pragma unroll
+  for (int c = 0; c < 4; ++c) v[c] = (int64_t)__builtin_fma(-q, cc->Pc[c], sig[c]);  // exact
+  const int64_t MASK = (1ll << 40) - 1;
+  const int64_t d0 = v[0] & MASK;
+  int64_t t = v[1] + (v[0] >> 40);
+  const int64_t d1 = t & MASK;
+  t = v[2] + (t >> 40);
+  const int64_t d2 = t & MASK;
+  const int64_t t3 = v[3] + (t >> 40);
+  uint64_t w0 = (uint64_t)d0 | ((uint64_t)d1 << 40);
+  uint64_t w1 = ((uint64_t)d1 >> 24) | ((uint64_t)d2 << 16) | ((uint64_t)t3 << 56);
+  uint64_t w2 = (uint64_t)(t3 >> 8);
+  bool neg = (int64_t)w2 < 0;
+  if (neg) {  // two's-complement negation of the 192-bit value
+    w0 = ~w0 + 1;
+    const uint64_t c0 = (w0 == 0) ? 1 : 0;
+    w1 = ~w1 + c0;
+    const uint64_t c1 = (c0 && w1 == 0) ? 1 : 0;
+    w2 = ~w2 + c1;
+  }
+  // symmetric range: x -> x -+ P when 2|x| > P (or 2|x| == P and x < 0)
+  const uint64_t x0 = w0 << 1, x1 = (w1 << 1) | (w0 >> 63), x2 = (w2 << 1) | (w1 >> 63);
+  int cmp = (x2 != cc->P[2]) ? (x2 > cc->P[2] ? 1 : -1)
+          : (x1 != cc->P[1]) ? (x1 > cc->P[1] ? 1 : -1)
+          : (x0 != cc->P[0]) ? (x0 > cc->P[0] ? 1 : -1) : 0;
+  if (cmp > 0 || (cmp == 0 && neg)) {
+    const uint64_t n0 = cc->P[0] - w0;
+    const uint64_t b0 = cc->P[0] < w0 ? 1 : 0;
+    const uint64_t n1 = cc->P[1] - w1 - b0;
+    const uint64_t b1 = (cc->P[1] < w1 || (cc->P[1] == w1 && b0)) ? 1 : 0;
+    const uint64_t n2 = cc->P[2] - w2 - b1;
+    w0 = n0; w1 = n1; w2 = n2;
+    neg = !neg;
+  }
+  return round_scaled(w0, w1, w2, e2, neg);
+}
+
+// One thread per 4 consecutive rows of a column: reads one 32-bit word per
+// modulus, accumulates S = sum r_l w_l as four exact FP64 chunk sums
+// (r_l w_l,c < 2^48, at most 20 terms < 2^53) and the quotient estimate
+// sum r_l fl(w_l / P), then reconstructs and rounds each element.
+__global__ __launch_bounds__(256) void k_crt(
+    const uint8_t* __restrict__ R, int64_t ldr, int64_t rplane, int64_t m, int64_t n,
+    const uint64_t* __restrict__ amaxA, const uint64_t* __restrict__ amaxB, int cA, int cB,
+    const CrtConst* __restrict__ cc, double* __restrict__ C, int64_t ldc) {
+  const int64_t rows4 = (m + 3) >> 2;
+  const int64_t t = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (t >= rows4 * n) return;
+  const int64_t j = t / rows4;
+  const int64_t i0 = (t - j * rows4) * 4;
+  const int L = cc->L;
+  double sig[4][4], Q[4];
+#pragma unroll
+  for (int e = 0; e < 4; ++e) {
+    Q[e] = 0.0;
+#pragma unroll
+    for (int c = 0; c < 4; ++c) sig[e][c] = 0.0;
+  }
+  const uint8_t* src = R + j * ldr + i0;
+  for (int l = 0; l < L; ++l) {
+    const uint32_t w = *reinterpret_cast<const uint32_t*>(src + (int64_t)l * rplane);
+    const double W0 = cc->W[l][0], W1 = cc->W[l][1], W2 = cc->W[l][2], W3 = cc->W[l][3];
+    const double F = cc->F[l];
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      const double r = (double)((w >> (8 * e)) & 0xffu);
+      sig[e][0] = __builtin_fma(r, W0, sig[e][0]);
+      sig[e][1] = __builtin_fma(r, W1, sig[e][1]);
+      sig[e][2] = __builtin_fma(r, W2, sig[e][2]);
+      sig[e][3] = __builtin_fma(r, W3, sig[e][3]);
+      Q[e] = __builtin_fma(r, F, Q[e]);
+    }
+  }
+  const int tj = line_shift(amaxB[j], cB);
+#pragma unroll
+  for (int e = 0; e < 4; ++e) {
+    const int64_t i = i0 + e;
+    if (i < m) {
+      const int si = line_shift(amaxA[i], cA);
+      C[i + j * ldc] = crt_finish(sig[e], Q[e], cc, -(si + tj));
+    }
+  }
+}
+
+}  // namespace ozfp4

@@ -1,0 +1,487 @@
+// C ABI of the Ozaki-II-on-FP4 library (declarations and contracts in
+// include/ozfp4.h). Host code: argument checks, per-device tables and
+// workspace, kernel launches on the library stream, stage timing.
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include <algorithm>
+#include <cstring>
+#include <mutex>
+
+#include "kernels.hpp"
+#include "ozfp4.h"
+#include "tables.hpp"
+
+using namespace ozfp4;
+
+namespace {
+
+constexpr int kMaxDevices = 64;
+constexpr int kMaxStages = 8;
+
+struct DeviceState {
+  bool ready = false;
+  ModConst* d_mod = nullptr;
+  CrtConst* d_crt = nullptr;  // kMaxModuli + 1 entries, index L
+  uint16_t* d_lut = nullptr;
+  uint16_t* d_lut8 = nullptr;
+  uint8_t* ws = nullptr;
+  size_t ws_bytes = 0;
+  int* h_flag = nullptr;      // pinned host word for the non-finite flag
+  hipEvent_t ev[kMaxStages + 1] = {};
+};
+
+HostTables g_tables;
+bool g_tables_ok = false;
+std::once_flag g_tables_once;
+DeviceState g_dev[kMaxDevices];
+hipStream_t g_stream = nullptr;
+bool g_profile = false;
+double g_stage_ms[kMaxStages];
+int g_nstages = 0;
+int g_pending_stages = 0;   // events recorded by the last profiled call
+int g_pending_device = -1;
+
+const HostTables* tables() {
+  std::call_once(g_tables_once, [] { g_tables_ok = build_tables(g_tables); });
+  return g_tables_ok ? &g_tables : nullptr;
+}
+
+inline int64_t round_up(int64_t v, int64_t a) { return (v + a - 1) / a * a; }
+
+#define HIP_TRY(expr)                                  \
+  do {                                                 \
+    if ((expr) != hipSuccess) return OZFP4_EHIP;       \
+  } while (0)
+
+int device_state(DeviceState** out) {
+  const HostTables* T = tables();
+  if (!T) return OZFP4_EHIP;
+  int dev = 0;
+  HIP_TRY(hipGetDevice(&dev));
+  if (dev < 0 || dev >= kMaxDevices) return OZFP4_EHIP;
+  DeviceState& d = g_dev[dev];
+  if (!d.ready) {
+    HIP_TRY(hipMalloc(&d.d_mod, sizeof(ModConst)));
+    HIP_TRY(hipMalloc(&d.d_crt, sizeof(CrtConst) * (kMaxModuli + 1)));
+    HIP_TRY(hipMalloc(&d.d_lut, T->lut.size() * sizeof(uint16_t)));
+    HIP_TRY(hipMalloc(&d.d_lut8, sizeof(T->lut8)));
+    HIP_TRY(hipMemcpy(d.d_mod, &T->mod, sizeof(ModConst), hipMemcpyHostToDevice));
+    HIP_TRY(hipMemcpy(d.d_crt, T->crt, sizeof(CrtConst) * (kMaxModuli + 1), hipMemcpyHostToDevice));
+    HIP_TRY(hipMemcpy(d.d_lut, T->lut.data(), T->lut.size() * sizeof(uint16_t), hipMemcpyHostToDevice));
+    HIP_TRY(hipMemcpy(d.d_lut8, T->lut8, sizeof(T->lut8), hipMemcpyHostToDevice));
+    HIP_TRY(hipHostMalloc(reinterpret_cast<void**>(&d.h_flag), sizeof(int), hipHostMallocDefault));
+    for (int i = 0; i <= kMaxStages; ++i) HIP_TRY(hipEventCreate(&d.ev[i]));
+    d.ready = true;
+  }
+  *out = &d;
+  return OZFP4_OK;
+}
+
+int ensure_workspace(DeviceState* d, size_t bytes) {
+  if (bytes <= d->ws_bytes) return OZFP4_OK;
+  if (d->ws) {
+    HIP_TRY(hipStreamSynchronize(g_stream));
+    HIP_TRY(hipFree(d->ws));
+    d->ws = nullptr;
+    d->ws_bytes = 0;
+  }
+  size_t sz = (bytes + (size_t(1) << 20) - 1) & ~((size_t(1) << 20) - 1);
+  if (hipMalloc(&d->ws, sz) != hipSuccess) {
+    (void)hipGetLastError();
+    return OZFP4_ENOMEM;
+  }
+  d->ws_bytes = sz;
+  return OZFP4_OK;
+}
+
+// ---------------------------------------------------------------- plans
+
+struct DgemmPlan {
+  int64_t m, n, k;
+  int L, cA, cB;
+  int64_t m_pad, n_pad, k_pad, kblocks;
+  int64_t plane_a, plane_b;  // bytes per plane
+  // workspace offsets
+  size_t off_amax_a, off_amax_b, off_flag, off_pa, off_pb, off_r, total;
+};
+
+size_t align256(size_t v) { return (v + 255) & ~size_t(255); }
+
+int check_dgemm_args(int64_t m, int64_t n, int64_t k, const void* A, int64_t lda, const void* B,
+                     int64_t ldb, int n_moduli) {
+  if (m < 0 || n < 0 || k < 0) return OZFP4_EINVAL;
+  if (lda < std::max<int64_t>(1, m) || ldb < std::max<int64_t>(1, k)) return OZFP4_EINVAL;
+  if (n_moduli < OZFP4_MIN_MODULI || n_moduli > OZFP4_MAX_MODULI) return OZFP4_EMODULI;
+  if (m > 0 && n > 0 && k > 0) {
+    if (!A || !B) return OZFP4_EINVAL;
+    if (k > OZFP4_MAX_K) return OZFP4_EKBOUND;
+  }
+  return OZFP4_OK;
+}
+
+int make_dgemm_plan(int64_t m, int64_t n, int64_t k, int L, DgemmPlan* p) {
+  const HostTables* T = tables();
+  if (!T) return OZFP4_EHIP;
+  p->m = m; p->n = n; p->k = k; p->L = L;
+  if (!capacity_split(T->P[L], k, &p->cA, &p->cB)) return OZFP4_EMODULI;
+  p->m_pad = round_up(m, kTile);
+  p->n_pad = round_up(n, kTile);
+  p->k_pad = round_up(k, kStageK);
+  p->kblocks = p->k_pad / kFragK;
+  p->plane_a = p->m_pad * p->k_pad / 2;
+  p->plane_b = p->n_pad * p->k_pad / 2;
+  size_t off = 0;
+  p->off_amax_a = off; off = align256(off + sizeof(uint64_t) * p->m_pad);
+  p->off_amax_b = off; off = align256(off + sizeof(uint64_t) * p->n_pad);
+  p->off_flag = off;   off = align256(off + 256);
+  p->off_pa = off;     off = align256(off + (size_t)p->plane_a * 2 * L);
+  p->off_pb = off;     off = align256(off + (size_t)p->plane_b * 2 * L);
+  p->off_r = off;      off = align256(off + (size_t)p->m_pad * p->n_pad * L);
+  p->total = off;
+  return OZFP4_OK;
+}
+
+inline unsigned blocks_for(int64_t n, int per) { return (unsigned)((n + per - 1) / per); }
+
+void record(DeviceState* d, int i) {
+  if (g_profile) (void)hipEventRecord(d->ev[i], g_stream);
+}
+
+int encode_grid(int64_t nfrag) {
+  // enough blocks to fill the chip several times, each wave loops
+  int64_t want = (nfrag + kEncWaves - 1) / kEncWaves;
+  return (int)std::min<int64_t>(want, 256 * 16);
+}
+
+// Stages of the dgemm pipeline, stopping after `last`:
+// 0 scale, 1 encode A, 2 encode B, 3 residue GEMM, 4 CRT.
+int run_dgemm(const DgemmPlan& p, DeviceState* d, const double* A, int64_t lda, const double* B,
+              int64_t ldb, double* C, int64_t ldc, int last, uint8_t* planes_a_out,
+              uint8_t* planes_b_out) {
+  const HostTables* T = tables();
+  uint8_t* ws = d->ws;
+  uint64_t* amax_a = reinterpret_cast<uint64_t*>(ws + p.off_amax_a);
+  uint64_t* amax_b = reinterpret_cast<uint64_t*>(ws + p.off_amax_b);
+  int* flag = reinterpret_cast<int*>(ws + p.off_flag);
+  uint8_t* pa = planes_a_out ? planes_a_out : ws + p.off_pa;
+  uint8_t* pb = planes_b_out ? planes_b_out : ws + p.off_pb;
+  uint8_t* R = ws + p.off_r;
+  const int L = p.L;
+
+  record(d, 0);
+  // stage 0: line maxima (the flag word shares the zero fill)
+  const int64_t nzero = (int64_t)((p.off_flag + 256 - p.off_amax_a) / sizeof(uint64_t));
+  hipLaunchKernelGGL(k_fill_u64, dim3(blocks_for(nzero, 256)), dim3(256), 0, g_stream,
+                     amax_a, nzero, (uint64_t)0);
+  hipLaunchKernelGGL(k_amax_adjacent_lines, dim3(blocks_for(p.m, 256), blocks_for(p.k, kAmaxChunk)),
+                     dim3(256), 0, g_stream, A, lda, p.m, p.k,
+                     reinterpret_cast<unsigned long long*>(amax_a), flag);
+  hipLaunchKernelGGL(k_amax_contig_lines, dim3(blocks_for(p.n, 4), blocks_for(p.k, kAmaxContigChunk)),
+                     dim3(256), 0, g_stream, B, ldb, p.n, p.k,
+                     reinterpret_cast<unsigned long long*>(amax_b), flag);
+  HIP_TRY(hipGetLastError());
+  record(d, 1);
+  if (last < 1) return OZFP4_OK;
+
+  // stage 1, 2: fused conversion + residues + limbs + E2M1 packing
+  const int lut_entries = T->mod.lut_off[L - 1] + 6 * T->mod.m[L - 1];
+  const size_t lut_bytes = sizeof(uint16_t) * (size_t)lut_entries;
+  const int64_t nfa = (p.m_pad / kFragLines) * p.kblocks;
+  const int64_t nfb = (p.n_pad / kFragLines) * p.kblocks;
+  hipLaunchKernelGGL(k_encode_dgemm, dim3(encode_grid(nfa)), dim3(256), lut_bytes, g_stream, A,
+                     (int64_t)1, lda, p.m, p.k, amax_a, p.cA, pa, p.plane_a, nfa, p.kblocks, L,
+                     d->d_mod, d->d_lut, lut_entries);
+  HIP_TRY(hipGetLastError());
+  record(d, 2);
+  hipLaunchKernelGGL(k_encode_dgemm, dim3(encode_grid(nfb)), dim3(256), lut_bytes, g_stream, B,
+                     ldb, (int64_t)1, p.n, p.k, amax_b, p.cB, pb, p.plane_b, nfb, p.kblocks, L,
+                     d->d_mod, d->d_lut, lut_entries);
+  HIP_TRY(hipGetLastError());
+  record(d, 3);
+  if (last < 3) return OZFP4_OK;
+
+  // stage 3: fused residue GEMM for all moduli
+  const int64_t tiles_m = p.m_pad / kTile, tiles_n = p.n_pad / kTile;
+  const int64_t nblocks = tiles_m * tiles_n * L;
+  hipLaunchKernelGGL(k_gemm_res, dim3((unsigned)nblocks), dim3(256), 0, g_stream, pa, pb, R,
+                     p.plane_a, p.plane_b, p.kblocks, tiles_m, tiles_n, nblocks, p.m_pad,
+                     p.m_pad * p.n_pad, d->d_mod);
+  HIP_TRY(hipGetLastError());
+  record(d, 4);
+  if (last < 4) return OZFP4_OK;
+
+  // stage 4: CRT reconstruction and inverse scaling
+  const int64_t nthreads = ((p.m + 3) / 4) * p.n;
+  hipLaunchKernelGGL(k_crt, dim3(blocks_for(nthreads, 256)), dim3(256), 0, g_stream, R, p.m_pad,
+                     p.m_pad * p.n_pad, p.m, p.n, amax_a, amax_b, p.cA, p.cB, d->d_crt + L, C, ldc);
+  HIP_TRY(hipGetLastError());
+  record(d, 5);
+  return OZFP4_OK;
+}
+
+int finish_with_flag(DeviceState* d, const int* dflag, int nstages) {
+  HIP_TRY(hipMemcpyAsync(d->h_flag, dflag, sizeof(int), hipMemcpyDeviceToHost, g_stream));
+  HIP_TRY(hipStreamSynchronize(g_stream));
+  if (g_profile && nstages > 0) {
+    g_pending_stages = 0;
+    for (int i = 0; i < nstages; ++i) {
+      float ms = 0.f;
+      HIP_TRY(hipEventElapsedTime(&ms, d->ev[i], d->ev[i + 1]));
+      g_stage_ms[i] = ms;
+    }
+    g_nstages = nstages;
+  }
+  return *d->h_flag ? OZFP4_ENONFINITE : OZFP4_OK;
+}
+
+int prepare(int64_t m, int64_t n, int64_t k, int L, DgemmPlan* p, DeviceState** d) {
+  int rc = make_dgemm_plan(m, n, k, L, p);
+  if (rc) return rc;
+  rc = device_state(d);
+  if (rc) return rc;
+  return ensure_workspace(*d, p->total);
+}
+
+}  // namespace
+
+extern "C" {
+
+int ozfp4_dgemm(int64_t m, int64_t n, int64_t k, const double* A, int64_t lda, const double* B,
+                int64_t ldb, double* C, int64_t ldc, int n_moduli) {
+  int rc = check_dgemm_args(m, n, k, A, lda, B, ldb, n_moduli);
+  if (rc) return rc;
+  if (ldc < std::max<int64_t>(1, m)) return OZFP4_EINVAL;
+  if (m == 0 || n == 0) return OZFP4_OK;
+  if (!C) return OZFP4_EINVAL;
+  if (k == 0) {
+    DeviceState* d;
+    rc = device_state(&d);
+    if (rc) return rc;
+    hipLaunchKernelGGL(k_fill_f64_matrix, dim3(blocks_for(m * n, 256)), dim3(256), 0, g_stream, C,
+                       m, n, ldc);
+    HIP_TRY(hipGetLastError());
+    return OZFP4_OK;
+  }
+  DgemmPlan p;
+  DeviceState* d;
+  rc = prepare(m, n, k, n_moduli, &p, &d);
+  if (rc) return rc;
+  rc = run_dgemm(p, d, A, lda, B, ldb, C, ldc, 4, nullptr, nullptr);
+  if (rc) return rc;
+  return finish_with_flag(d, reinterpret_cast<int*>(d->ws + p.off_flag), 5);
+}
+
+int ozfp4_igemm_s8(int64_t m, int64_t n, int64_t k, const int8_t* A, int64_t lda, const int8_t* B,
+                   int64_t ldb, int32_t* C, int64_t ldc) {
+  if (m < 0 || n < 0 || k < 0) return OZFP4_EINVAL;
+  if (lda < std::max<int64_t>(1, m) || ldb < std::max<int64_t>(1, k) ||
+      ldc < std::max<int64_t>(1, m))
+    return OZFP4_EINVAL;
+  if (m == 0 || n == 0) return OZFP4_OK;
+  if (!C) return OZFP4_EINVAL;
+  if (k > OZFP4_MAX_K_S8) return OZFP4_EKBOUND;
+  DeviceState* d;
+  int rc = device_state(&d);
+  if (rc) return rc;
+  if (k == 0) {
+    hipLaunchKernelGGL(k_fill_i32_matrix, dim3(blocks_for(m * n, 256)), dim3(256), 0, g_stream, C,
+                       m, n, ldc);
+    HIP_TRY(hipGetLastError());
+    return OZFP4_OK;
+  }
+  if (!A || !B) return OZFP4_EINVAL;
+  const int64_t m_pad = round_up(m, kTile), n_pad = round_up(n, kTile);
+  const int64_t k_pad = round_up(k, kStageK), kblocks = k_pad / kFragK;
+  const int64_t plane_a = m_pad * k_pad / 2, plane_b = n_pad * k_pad / 2;
+  const size_t off_pb = align256((size_t)plane_a * 3);
+  rc = ensure_workspace(d, off_pb + align256((size_t)plane_b * 3));
+  if (rc) return rc;
+  uint8_t* pa = d->ws;
+  uint8_t* pb = d->ws + off_pb;
+  record(d, 0);
+  const int64_t nfa = (m_pad / kFragLines) * kblocks, nfb = (n_pad / kFragLines) * kblocks;
+  hipLaunchKernelGGL(k_encode_s8, dim3(encode_grid(nfa)), dim3(256), 0, g_stream, A, (int64_t)1,
+                     lda, m, k, pa, plane_a, nfa, kblocks, d->d_lut8);
+  record(d, 1);
+  hipLaunchKernelGGL(k_encode_s8, dim3(encode_grid(nfb)), dim3(256), 0, g_stream, B, ldb,
+                     (int64_t)1, n, k, pb, plane_b, nfb, kblocks, d->d_lut8);
+  record(d, 2);
+  const int64_t tiles_m = m_pad / kTile, tiles_n = n_pad / kTileS8N;
+  const int64_t nblocks = tiles_m * tiles_n;
+  hipLaunchKernelGGL(k_gemm_s8, dim3((unsigned)nblocks), dim3(256), 0, g_stream, pa, pb, C,
+                     plane_a, plane_b, kblocks, tiles_m, tiles_n, nblocks, m, n, ldc);
+  record(d, 3);
+  HIP_TRY(hipGetLastError());
+  if (g_profile) {
+    g_pending_stages = 3;
+    HIP_TRY(hipGetDevice(&g_pending_device));
+  }
+  return OZFP4_OK;
+}
+
+int ozfp4_set_stream(void* stream) {
+  g_stream = reinterpret_cast<hipStream_t>(stream);
+  return OZFP4_OK;
+}
+
+int ozfp4_finalize(void) {
+  int cur = 0;
+  if (hipGetDevice(&cur) != hipSuccess) cur = -1;
+  for (int i = 0; i < kMaxDevices; ++i) {
+    DeviceState& d = g_dev[i];
+    if (!d.ready) continue;
+    if (hipSetDevice(i) != hipSuccess) continue;
+    (void)hipDeviceSynchronize();
+    (void)hipFree(d.ws);
+    (void)hipFree(d.d_mod);
+    (void)hipFree(d.d_crt);
+    (void)hipFree(d.d_lut);
+    (void)hipFree(d.d_lut8);
+    (void)hipHostFree(d.h_flag);
+    for (int e = 0; e <= kMaxStages; ++e) (void)hipEventDestroy(d.ev[e]);
+    d = DeviceState();
+  }
+  if (cur >= 0) (void)hipSetDevice(cur);
+  return OZFP4_OK;
+}
+
+const char* ozfp4_strerror(int code) {
+  switch (code) {
+    case OZFP4_OK: return "success";
+    case OZFP4_EINVAL: return "invalid size, leading dimension or null pointer";
+    case OZFP4_EMODULI: return "n_moduli outside [2, 20] or too few moduli for this k";
+    case OZFP4_EKBOUND: return "k above the FP32-exactness bound";
+    case OZFP4_ENONFINITE: return "NaN or Inf in an input matrix";
+    case OZFP4_ENOMEM: return "device workspace allocation failed";
+    case OZFP4_EHIP: return "HIP runtime error";
+    default: return "unknown error code";
+  }
+}
+
+int ozfp4_moduli(int n_moduli, int32_t* out) {
+  if (n_moduli < 1 || n_moduli > OZFP4_MAX_MODULI || !out) return OZFP4_EINVAL;
+  const HostTables* T = tables();
+  if (!T) return OZFP4_EHIP;
+  for (int i = 0; i < n_moduli; ++i) out[i] = T->moduli[i];
+  return OZFP4_OK;
+}
+
+int ozfp4_capacity(int64_t k, int n_moduli, int32_t* c_a, int32_t* c_b) {
+  if (k < 1 || !c_a || !c_b) return OZFP4_EINVAL;
+  if (n_moduli < OZFP4_MIN_MODULI || n_moduli > OZFP4_MAX_MODULI) return OZFP4_EMODULI;
+  const HostTables* T = tables();
+  if (!T) return OZFP4_EHIP;
+  int a, b;
+  if (!capacity_split(T->P[n_moduli], k, &a, &b)) return OZFP4_EMODULI;
+  *c_a = a;
+  *c_b = b;
+  return OZFP4_OK;
+}
+
+int ozfp4_two_limb_table(int modulus_index, uint8_t* out, int32_t* m_out) {
+  if (modulus_index < 0 || modulus_index >= OZFP4_MAX_MODULI || !out || !m_out) return OZFP4_EINVAL;
+  const HostTables* T = tables();
+  if (!T) return OZFP4_EHIP;
+  const int m = T->moduli[modulus_index];
+  const uint16_t* lut = T->lut.data() + T->mod.lut_off[modulus_index];
+  for (int r = 0; r < m; ++r) {
+    const uint16_t e = lut[r + m];  // remainder estimate r, non-negative value
+    out[r] = (uint8_t)((e & 0xf) | ((e >> 8) & 0xf) << 4);
+  }
+  *m_out = m;
+  return OZFP4_OK;
+}
+
+int ozfp4_plane_layout(int64_t lines, int64_t k, int64_t* rows_pad, int64_t* k_pad,
+                       int64_t* bytes_per_plane) {
+  if (lines < 0 || k < 0 || !rows_pad || !k_pad || !bytes_per_plane) return OZFP4_EINVAL;
+  *rows_pad = round_up(lines, kTile);
+  *k_pad = round_up(k, kStageK);
+  *bytes_per_plane = *rows_pad * *k_pad / 2;
+  return OZFP4_OK;
+}
+
+int ozfp4_scales(int64_t m, int64_t n, int64_t k, const double* A, int64_t lda, const double* B,
+                 int64_t ldb, int n_moduli, int32_t* s, int32_t* t) {
+  int rc = check_dgemm_args(m, n, k, A, lda, B, ldb, n_moduli);
+  if (rc) return rc;
+  if (m == 0 || n == 0 || k == 0) return OZFP4_EINVAL;
+  if (!s || !t) return OZFP4_EINVAL;
+  DgemmPlan p;
+  DeviceState* d;
+  rc = prepare(m, n, k, n_moduli, &p, &d);
+  if (rc) return rc;
+  rc = run_dgemm(p, d, A, lda, B, ldb, nullptr, 0, 0, nullptr, nullptr);
+  if (rc) return rc;
+  hipLaunchKernelGGL(k_shifts, dim3(blocks_for(m, 256)), dim3(256), 0, g_stream,
+                     reinterpret_cast<uint64_t*>(d->ws + p.off_amax_a), m, p.cA, s);
+  hipLaunchKernelGGL(k_shifts, dim3(blocks_for(n, 256)), dim3(256), 0, g_stream,
+                     reinterpret_cast<uint64_t*>(d->ws + p.off_amax_b), n, p.cB, t);
+  HIP_TRY(hipGetLastError());
+  return finish_with_flag(d, reinterpret_cast<int*>(d->ws + p.off_flag), 0);
+}
+
+int ozfp4_limb_planes(int64_t m, int64_t n, int64_t k, const double* A, int64_t lda,
+                      const double* B, int64_t ldb, int n_moduli, uint8_t* planes_a,
+                      uint8_t* planes_b) {
+  int rc = check_dgemm_args(m, n, k, A, lda, B, ldb, n_moduli);
+  if (rc) return rc;
+  if (m == 0 || n == 0 || k == 0) return OZFP4_EINVAL;
+  if (!planes_a || !planes_b) return OZFP4_EINVAL;
+  DgemmPlan p;
+  DeviceState* d;
+  rc = prepare(m, n, k, n_moduli, &p, &d);
+  if (rc) return rc;
+  rc = run_dgemm(p, d, A, lda, B, ldb, nullptr, 0, 2, planes_a, planes_b);
+  if (rc) return rc;
+  return finish_with_flag(d, reinterpret_cast<int*>(d->ws + p.off_flag), 0);
+}
+
+int ozfp4_residues(int64_t m, int64_t n, int64_t k, const double* A, int64_t lda, const double* B,
+                   int64_t ldb, int n_moduli, uint8_t* R, int64_t ldr) {
+  int rc = check_dgemm_args(m, n, k, A, lda, B, ldb, n_moduli);
+  if (rc) return rc;
+  if (m == 0 || n == 0 || k == 0) return OZFP4_EINVAL;
+  if (!R || ldr < m) return OZFP4_EINVAL;
+  DgemmPlan p;
+  DeviceState* d;
+  rc = prepare(m, n, k, n_moduli, &p, &d);
+  if (rc) return rc;
+  rc = run_dgemm(p, d, A, lda, B, ldb, nullptr, 0, 3, nullptr, nullptr);
+  if (rc) return rc;
+  for (int l = 0; l < n_moduli; ++l) {
+    HIP_TRY(hipMemcpy2DAsync(R + (size_t)l * ldr * n, (size_t)ldr,
+                             d->ws + p.off_r + (size_t)l * p.m_pad * p.n_pad, (size_t)p.m_pad,
+                             (size_t)m, (size_t)n, hipMemcpyDeviceToDevice, g_stream));
+  }
+  return finish_with_flag(d, reinterpret_cast<int*>(d->ws + p.off_flag), 0);
+}
+
+int ozfp4_profile(int enable) {
+  g_profile = enable != 0;
+  g_nstages = 0;
+  g_pending_stages = 0;
+  return OZFP4_OK;
+}
+
+int ozfp4_stage_times(double* ms, int max, int* n_stages) {
+  if (!ms || !n_stages || max < 0) return OZFP4_EINVAL;
+  if (g_pending_stages > 0) {  // asynchronous call: resolve its events now
+    DeviceState& d = g_dev[g_pending_device];
+    HIP_TRY(hipEventSynchronize(d.ev[g_pending_stages]));
+    for (int i = 0; i < g_pending_stages; ++i) {
+      float t = 0.f;
+      HIP_TRY(hipEventElapsedTime(&t, d.ev[i], d.ev[i + 1]));
+      g_stage_ms[i] = t;
+    }
+    g_nstages = g_pending_stages;
+    g_pending_stages = 0;
+  }
+  const int c = std::min(g_nstages, max);
+  for (int i = 0; i < c; ++i) ms[i] = g_stage_ms[i];
+  *n_stages = g_nstages;
+  return OZFP4_OK;
+}
+
+}  // extern "C"

@@ -1,0 +1,261 @@
+// Host-side constants of the method, derived at library initialisation from
+// the definitions in the paper (nothing is typed in):
+//   * the two-limb moduli and their greedy pairwise-coprime order (Sec. V-A);
+//   * P, the CRT weights w_l = M_l (M_l^{-1} mod m_l) and their 40-bit
+//     chunks (Sec. V-B);
+//   * the capacity split (c_A, c_B) for an inner dimension k (Sec. IV-B with
+//     Eq. (crt));
+//   * the canonical two-limb split of every residue and its E2M1 codes
+//     (Sec. III, Sec. V-A), as lookup tables for the encoder;
+//   * the three greedy limbs of every int8 (Sec. III).
+#pragma once
+
+#include <stdint.h>
+
+#include <algorithm>
+#include <cstring>
+#include <vector>
+
+namespace ozfp4 {
+
+constexpr int kMaxModuli = 20;
+
+// ---- minimal unsigned multiword integer (little-endian 32-bit words) ----
+struct Big {
+  static constexpr int W = 8;  // 256 bits: P < 2^129 for 20 moduli
+  uint32_t w[W];
+  Big() { std::memset(w, 0, sizeof(w)); }
+  explicit Big(uint64_t v) {
+    std::memset(w, 0, sizeof(w));
+    w[0] = (uint32_t)v;
+    w[1] = (uint32_t)(v >> 32);
+  }
+  void mul_small(uint32_t f) {
+    uint64_t carry = 0;
+    for (int i = 0; i < W; ++i) {
+      uint64_t t = (uint64_t)w[i] * f + carry;
+      w[i] = (uint32_t)t;
+      carry = t >> 32;
+    }
+  }
+  // divides in place, returns the remainder
+  uint32_t div_small(uint32_t d) {
+    uint64_t rem = 0;
+    for (int i = W - 1; i >= 0; --i) {
+      uint64_t cur = (rem << 32) | w[i];
+      w[i] = (uint32_t)(cur / d);
+      rem = cur % d;
+    }
+    return (uint32_t)rem;
+  }
+  void sub_one() {
+    for (int i = 0; i < W; ++i) {
+      if (w[i]-- != 0) break;
+    }
+  }
+  int bitlen() const {
+    for (int i = W - 1; i >= 0; --i)
+      if (w[i]) return 32 * i + 32 - __builtin_clz(w[i]);
+    return 0;
+  }
+  // bits [lo, lo + n) as an integer, n <= 52
+  uint64_t bits(int lo, int n) const {
+    uint64_t out = 0;
+    for (int b = 0; b < n; ++b) {
+      int pos = lo + b;
+      if (pos >= 32 * W) break;
+      out |= (uint64_t)((w[pos >> 5] >> (pos & 31)) & 1u) << b;
+    }
+    return out;
+  }
+};
+
+// ---- Sec. III: E2M1 codes of doubled values, greedy digits ----
+inline int e2m1_code_of_limb(int c) {
+  // stored value c/2; magnitudes 0, .5, 1, 1.5, 2, 3, 4, 6 -> codes 0..7
+  int a = c < 0 ? -c : c;
+  int code;
+  switch (a) {
+    case 0: code = 0; break;
+    case 1: code = 1; break;
+    case 2: code = 2; break;
+    case 3: code = 3; break;
+    case 4: code = 4; break;
+    case 6: code = 5; break;
+    case 8: code = 6; break;
+    case 12: code = 7; break;
+    default: return -1;
+  }
+  return (c < 0) ? (code | 8) : code;
+}
+
+// greedy digit: smallest-magnitude representative mod 13, +-5 -> -+8 (Lemma 2)
+inline int greedy13(int x) {
+  int s = ((x + 6) % 13 + 13) % 13 - 6;
+  if (s == 5) return -8;
+  if (s == -5) return 8;
+  return s;
+}
+
+inline bool limb_in_S(int c) { return e2m1_code_of_limb(c) >= 0; }
+
+// ---- Sec. V-A: two-limb moduli and the greedy list ----
+inline std::vector<int> greedy_moduli() {
+  static const int S[] = {-12, -8, -6, -4, -3, -2, -1, 0, 1, 2, 3, 4, 6, 8, 12};
+  std::vector<int> two_limb;
+  for (int m = 400; m >= 2; --m) {
+    std::vector<char> seen(m, 0);
+    int count = 0;
+    for (int a : S)
+      for (int b : S) {
+        int r = ((a + 13 * b) % m + m) % m;
+        if (!seen[r]) { seen[r] = 1; ++count; }
+      }
+    if (count == m) two_limb.push_back(m);
+  }
+  std::vector<int> chosen;
+  for (int m : two_limb) {  // descending
+    bool ok = true;
+    for (int q : chosen) {
+      int a = m, b = q;
+      while (b) { int t = a % b; a = b; b = t; }
+      if (a != 1) { ok = false; break; }
+    }
+    if (ok) chosen.push_back(m);
+    if ((int)chosen.size() == kMaxModuli) break;
+  }
+  return chosen;
+}
+
+// canonical two-limb split of residue r in [0, m): returns false if none
+inline bool two_limb_split(int r, int m, int* c0, int* c1) {
+  int rp = r;
+  if (2 * rp > m) rp -= m;
+  int cands[2] = {rp, rp > 0 ? rp - m : rp + m};
+  for (int cand : cands) {
+    int a = greedy13(cand);
+    int q = (cand - a) / 13;  // exact
+    int b = greedy13(q);
+    if ((((a + 13 * b - r) % m) + m) % m == 0) {
+      *c0 = a;
+      *c1 = b;
+      return true;
+    }
+  }
+  return false;
+}
+
+// ---- device-side constant blocks (plain data, copied once per device) ----
+struct ModConst {
+  int m[kMaxModuli];
+  int lut_off[kMaxModuli];   // start of modulus l in the encoder LUT (entries)
+  double inv[kMaxModuli];    // fl(1 / m)
+  double md[kMaxModuli];     // m as double
+};
+
+struct CrtConst {
+  int L;
+  int pad_;
+  double W[kMaxModuli][4];   // 40-bit chunks of w_l
+  double F[kMaxModuli];      // fl(u_l / m_l) = fl(w_l / P)
+  double Pc[4];              // 40-bit chunks of P
+  uint64_t P[3];             // P as a 192-bit integer
+};
+
+struct HostTables {
+  std::vector<int> moduli;                 // 20, greedy order
+  ModConst mod;
+  CrtConst crt[kMaxModuli + 1];            // index L (2..20)
+  std::vector<uint16_t> lut;               // encoder LUT, all 20 moduli
+  uint16_t lut8[256];                      // int8 -> three limb codes
+  Big P[kMaxModuli + 1];                   // product of the first L moduli
+  bool ok = false;
+};
+
+// Encoder LUT of modulus m: 6m entries, index (ri + m) + neg * 3m for a
+// remainder estimate ri in [-m, 2m) of |x| and the sign of x; entry =
+// code(c0) | code(c1) << 8 for the canonical split of the class of x.
+inline bool build_tables(HostTables& T) {
+  T.moduli = greedy_moduli();
+  if ((int)T.moduli.size() != kMaxModuli) return false;
+  std::memset(&T.mod, 0, sizeof(T.mod));
+  int off = 0;
+  T.lut.clear();
+  for (int l = 0; l < kMaxModuli; ++l) {
+    int m = T.moduli[l];
+    T.mod.m[l] = m;
+    T.mod.lut_off[l] = off;
+    T.mod.inv[l] = 1.0 / (double)m;
+    T.mod.md[l] = (double)m;
+    for (int neg = 0; neg < 2; ++neg)
+      for (int ri = -m; ri < 2 * m; ++ri) {
+        int cls = ((ri % m) + m) % m;
+        if (neg) cls = (m - cls) % m;
+        int c0, c1;
+        if (!two_limb_split(cls, m, &c0, &c1)) return false;
+        int k0 = e2m1_code_of_limb(c0), k1 = e2m1_code_of_limb(c1);
+        if (k0 < 0 || k1 < 0) return false;
+        T.lut.push_back((uint16_t)(k0 | (k1 << 8)));
+      }
+    off += 6 * m;
+  }
+  // int8: three greedy limbs (X_3 = 732 >= 128)
+  for (int v = -128; v < 128; ++v) {
+    int rest = v, codes = 0;
+    for (int i = 0; i < 3; ++i) {
+      int c = greedy13(rest);
+      int code = e2m1_code_of_limb(c);
+      if (code < 0) return false;
+      codes |= code << (4 * i);
+      rest = (rest - c) / 13;
+    }
+    if (rest != 0) return false;
+    T.lut8[v + 128] = (uint16_t)codes;
+  }
+  // CRT constants for every L
+  for (int L = 0; L <= kMaxModuli; ++L) {
+    std::memset(&T.crt[L], 0, sizeof(CrtConst));
+    T.P[L] = Big(1);
+    if (L < 1) continue;
+    for (int l = 0; l < L; ++l) T.P[L].mul_small((uint32_t)T.moduli[l]);
+    CrtConst& c = T.crt[L];
+    c.L = L;
+    for (int q = 0; q < 4; ++q) c.Pc[q] = (double)T.P[L].bits(40 * q, 40);
+    for (int q = 0; q < 3; ++q) c.P[q] = T.P[L].bits(64 * q, 32) | (T.P[L].bits(64 * q + 32, 32) << 32);
+    for (int l = 0; l < L; ++l) {
+      int m = T.moduli[l];
+      Big Mi = T.P[L];
+      Mi.div_small((uint32_t)m);          // exact: M_l = P / m_l
+      Big tmp = Mi;
+      uint32_t Mmod = tmp.div_small((uint32_t)m);
+      int u = -1;
+      for (int x = 1; x < m; ++x)
+        if ((uint64_t)Mmod * x % m == 1) { u = x; break; }
+      if (u < 0) return false;
+      Big w = Mi;
+      w.mul_small((uint32_t)u);           // w_l = M_l u_l < P
+      for (int q = 0; q < 4; ++q) c.W[l][q] = (double)w.bits(40 * q, 40);
+      c.F[l] = (double)u / (double)m;     // = w_l / P, correctly rounded
+    }
+  }
+  T.ok = true;
+  return true;
+}
+
+// Largest b with 2 k 2^b < P (Eq. (crt)) and the split c_A = min(53,
+// ceil(b/2)), c_B = min(53, b - c_A) (Sec. IV-B). Returns false if b < 2.
+inline bool capacity_split(const Big& P, int64_t k, int* cA, int* cB) {
+  if (k < 1) return false;
+  // 2 k 2^b < P  <=>  2^(b+1) <= floor((P - 1) / k)
+  Big q = P;
+  q.sub_one();
+  q.div_small((uint32_t)k);
+  int b = q.bitlen() - 2;
+  if (b < 2) return false;
+  int a = std::min(53, (b + 1) / 2);
+  *cA = a;
+  *cB = std::min(53, b - a);
+  return true;
+}
+
+}  // namespace ozfp4

@@ -1,0 +1,270 @@
+"""Thin ctypes binding of libozfp4.so (C ABI in include/ozfp4.h).
+
+The functions named ``ozfp4_*`` mirror the C entry points one to one (plain
+integers and pointers in, status code out). The torch helpers below them only
+marshal arguments: they check dtypes and layouts, allocate outputs with
+torch, pass device pointers and the current torch stream, and raise on a
+nonzero status. Every arithmetic step runs in the library's HIP kernels;
+there is no CPU fallback, and ``load()`` raises if the library is missing.
+
+Matrices are column-major as in BLAS: a torch tensor X of shape (rows, cols)
+is accepted when X.stride(0) == 1, with leading dimension X.stride(1).
+``colmajor(X)`` makes such a copy of any 2-D tensor.
+"""
+
+from __future__ import annotations
+
+import ctypes
+import os
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libozfp4.so")
+
+OZFP4_OK = 0
+OZFP4_EINVAL = -1
+OZFP4_EMODULI = -2
+OZFP4_EKBOUND = -3
+OZFP4_ENONFINITE = -4
+OZFP4_ENOMEM = -5
+OZFP4_EHIP = -6
+OZFP4_MIN_MODULI = 2
+OZFP4_MAX_MODULI = 20
+OZFP4_MAX_K = 131072
+OZFP4_MAX_K_S8 = 87381
+
+_lib = None
+
+_i64, _int, _p = ctypes.c_int64, ctypes.c_int, ctypes.c_void_p
+_SIGNATURES = {
+    "ozfp4_dgemm": (_int, [_i64, _i64, _i64, _p, _i64, _p, _i64, _p, _i64, _int]),
+    "ozfp4_igemm_s8": (_int, [_i64, _i64, _i64, _p, _i64, _p, _i64, _p, _i64]),
+    "ozfp4_set_stream": (_int, [_p]),
+    "ozfp4_finalize": (_int, []),
+    "ozfp4_strerror": (ctypes.c_char_p, [_int]),
+    "ozfp4_moduli": (_int, [_int, _p]),
+    "ozfp4_capacity": (_int, [_i64, _int, _p, _p]),
+    "ozfp4_two_limb_table": (_int, [_int, _p, _p]),
+    "ozfp4_plane_layout": (_int, [_i64, _i64, _p, _p, _p]),
+    "ozfp4_scales": (_int, [_i64, _i64, _i64, _p, _i64, _p, _i64, _int, _p, _p]),
+    "ozfp4_limb_planes": (_int, [_i64, _i64, _i64, _p, _i64, _p, _i64, _int, _p, _p]),
+    "ozfp4_residues": (_int, [_i64, _i64, _i64, _p, _i64, _p, _i64, _int, _p, _i64]),
+    "ozfp4_profile": (_int, [_int]),
+    "ozfp4_stage_times": (_int, [_p, _int, _p]),
+}
+
+
+class OzFP4Error(RuntimeError):
+    def __init__(self, code: int, where: str):
+        self.code = code
+        super().__init__(f"{where}: {ozfp4_strerror(code)} (code {code})")
+
+
+def load() -> ctypes.CDLL:
+    """Load libozfp4.so from the package directory (raises if it is missing)."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError(f"{LIB_PATH} is not built; run python -m paper_2608_06812_amd.build")
+        lib = ctypes.CDLL(LIB_PATH)
+        for name, (res, args) in _SIGNATURES.items():
+            fn = getattr(lib, name)
+            fn.restype = res
+            fn.argtypes = args
+        _lib = lib
+    return _lib
+
+
+# ---------------------------------------------------------------- raw C ABI
+
+def ozfp4_dgemm(m, n, k, A, lda, B, ldb, C, ldc, n_moduli) -> int:
+    return load().ozfp4_dgemm(m, n, k, A, lda, B, ldb, C, ldc, n_moduli)
+
+
+def ozfp4_igemm_s8(m, n, k, A, lda, B, ldb, C, ldc) -> int:
+    return load().ozfp4_igemm_s8(m, n, k, A, lda, B, ldb, C, ldc)
+
+
+def ozfp4_set_stream(stream) -> int:
+    return load().ozfp4_set_stream(stream)
+
+
+def ozfp4_finalize() -> int:
+    return load().ozfp4_finalize()
+
+
+def ozfp4_strerror(code: int) -> str:
+    return load().ozfp4_strerror(code).decode()
+
+
+def ozfp4_moduli(n_moduli: int) -> list[int]:
+    out = (ctypes.c_int32 * max(1, n_moduli))()
+    _check(load().ozfp4_moduli(n_moduli, out), "ozfp4_moduli")
+    return list(out)[:n_moduli]
+
+
+def ozfp4_capacity(k: int, n_moduli: int) -> tuple[int, int]:
+    a, b = ctypes.c_int32(), ctypes.c_int32()
+    _check(load().ozfp4_capacity(k, n_moduli, ctypes.byref(a), ctypes.byref(b)), "ozfp4_capacity")
+    return a.value, b.value
+
+
+def ozfp4_two_limb_table(modulus_index: int) -> tuple[int, bytes]:
+    out = (ctypes.c_uint8 * 256)()
+    m = ctypes.c_int32()
+    _check(load().ozfp4_two_limb_table(modulus_index, out, ctypes.byref(m)), "ozfp4_two_limb_table")
+    return m.value, bytes(out)[: m.value]
+
+
+def ozfp4_plane_layout(lines: int, k: int) -> tuple[int, int, int]:
+    r, kp, b = ctypes.c_int64(), ctypes.c_int64(), ctypes.c_int64()
+    _check(load().ozfp4_plane_layout(lines, k, ctypes.byref(r), ctypes.byref(kp), ctypes.byref(b)),
+           "ozfp4_plane_layout")
+    return r.value, kp.value, b.value
+
+
+def ozfp4_scales(m, n, k, A, lda, B, ldb, n_moduli, s, t) -> int:
+    return load().ozfp4_scales(m, n, k, A, lda, B, ldb, n_moduli, s, t)
+
+
+def ozfp4_limb_planes(m, n, k, A, lda, B, ldb, n_moduli, planes_a, planes_b) -> int:
+    return load().ozfp4_limb_planes(m, n, k, A, lda, B, ldb, n_moduli, planes_a, planes_b)
+
+
+def ozfp4_residues(m, n, k, A, lda, B, ldb, n_moduli, R, ldr) -> int:
+    return load().ozfp4_residues(m, n, k, A, lda, B, ldb, n_moduli, R, ldr)
+
+
+def ozfp4_profile(enable: bool) -> int:
+    return load().ozfp4_profile(1 if enable else 0)
+
+
+def ozfp4_stage_times() -> list[float]:
+    buf = (ctypes.c_double * 8)()
+    cnt = ctypes.c_int()
+    _check(load().ozfp4_stage_times(buf, 8, ctypes.byref(cnt)), "ozfp4_stage_times")
+    return list(buf)[: cnt.value]
+
+
+def _check(code: int, where: str) -> None:
+    if code != OZFP4_OK:
+        raise OzFP4Error(code, where)
+
+
+# ---------------------------------------------------------------- torch helpers
+
+def colmajor(X):
+    """A column-major copy (stride(0) == 1) of a 2-D torch tensor."""
+    return X.t().contiguous().t()
+
+
+def _cm(X, dtype, name):
+    import torch
+    if not isinstance(X, torch.Tensor) or X.dim() != 2:
+        raise TypeError(f"{name} must be a 2-D torch tensor")
+    if X.dtype != dtype:
+        raise TypeError(f"{name} must be {dtype}")
+    if not X.is_cuda:
+        raise ValueError(f"{name} must be a device tensor")
+    if X.stride(0) != 1 and X.shape[0] > 1:
+        X = colmajor(X)
+    ld = max(1, X.stride(1) if X.shape[1] > 1 else X.shape[0])
+    return X, ld
+
+
+def _use_torch_stream(device):
+    import torch
+    ozfp4_set_stream(torch.cuda.current_stream(device).cuda_stream)
+
+
+def _empty_cm(rows, cols, dtype, device):
+    import torch
+    return torch.empty_strided((rows, cols), (1, max(1, rows)), dtype=dtype, device=device)
+
+
+def dgemm(A, B, n_moduli: int = 19, out=None):
+    """C = fl(A B) for float64 device tensors A (m x k), B (k x n) by Ozaki
+    scheme II on FP4 limbs; returns C (m x n), column-major."""
+    import torch
+    A, lda = _cm(A, torch.float64, "A")
+    B, ldb = _cm(B, torch.float64, "B")
+    m, k = A.shape
+    k2, n = B.shape
+    if k != k2:
+        raise ValueError("inner dimensions differ")
+    C = _empty_cm(m, n, torch.float64, A.device) if out is None else out
+    if C.shape != (m, n) or C.dtype != torch.float64 or (C.stride(0) != 1 and m > 1):
+        raise ValueError("out must be a column-major float64 (m x n) tensor")
+    ldc = max(1, C.stride(1) if n > 1 else m)
+    _use_torch_stream(A.device)
+    _check(ozfp4_dgemm(m, n, k, A.data_ptr(), lda, B.data_ptr(), ldb, C.data_ptr(), ldc, n_moduli),
+           "ozfp4_dgemm")
+    return C
+
+
+def igemm_s8(A, B, out=None):
+    """C = A B for int8 device tensors, int32 result wrapping modulo 2^32;
+    returns C (m x n), column-major."""
+    import torch
+    A, lda = _cm(A, torch.int8, "A")
+    B, ldb = _cm(B, torch.int8, "B")
+    m, k = A.shape
+    k2, n = B.shape
+    if k != k2:
+        raise ValueError("inner dimensions differ")
+    C = _empty_cm(m, n, torch.int32, A.device) if out is None else out
+    if C.shape != (m, n) or C.dtype != torch.int32 or (C.stride(0) != 1 and m > 1):
+        raise ValueError("out must be a column-major int32 (m x n) tensor")
+    ldc = max(1, C.stride(1) if n > 1 else m)
+    _use_torch_stream(A.device)
+    _check(ozfp4_igemm_s8(m, n, k, A.data_ptr(), lda, B.data_ptr(), ldb, C.data_ptr(), ldc),
+           "ozfp4_igemm_s8")
+    return C
+
+
+def scales(A, B, n_moduli: int = 19):
+    """Shifts (s per row of A, t per column of B) as int32 device tensors."""
+    import torch
+    A, lda = _cm(A, torch.float64, "A")
+    B, ldb = _cm(B, torch.float64, "B")
+    m, k = A.shape
+    n = B.shape[1]
+    s = torch.empty(m, dtype=torch.int32, device=A.device)
+    t = torch.empty(n, dtype=torch.int32, device=A.device)
+    _use_torch_stream(A.device)
+    _check(ozfp4_scales(m, n, k, A.data_ptr(), lda, B.data_ptr(), ldb, n_moduli, s.data_ptr(),
+                        t.data_ptr()), "ozfp4_scales")
+    return s, t
+
+
+def limb_planes(A, B, n_moduli: int = 19):
+    """Packed E2M1 limb planes of A and B (uint8 device tensors of shape
+    (2 n_moduli, bytes_per_plane)) in the fragment layout of
+    include/ozfp4.h."""
+    import torch
+    A, lda = _cm(A, torch.float64, "A")
+    B, ldb = _cm(B, torch.float64, "B")
+    m, k = A.shape
+    n = B.shape[1]
+    _, _, bpa = ozfp4_plane_layout(m, k)
+    _, _, bpb = ozfp4_plane_layout(n, k)
+    pa = torch.empty((2 * n_moduli, bpa), dtype=torch.uint8, device=A.device)
+    pb = torch.empty((2 * n_moduli, bpb), dtype=torch.uint8, device=A.device)
+    _use_torch_stream(A.device)
+    _check(ozfp4_limb_planes(m, n, k, A.data_ptr(), lda, B.data_ptr(), ldb, n_moduli, pa.data_ptr(),
+                             pb.data_ptr()), "ozfp4_limb_planes")
+    return pa, pb
+
+
+def residues(A, B, n_moduli: int = 19):
+    """Residue matrices (A~ B~) mod m_l as a uint8 device tensor of shape
+    (n_moduli, n, m): R[l, j, i] = residue of element (i, j)."""
+    import torch
+    A, lda = _cm(A, torch.float64, "A")
+    B, ldb = _cm(B, torch.float64, "B")
+    m, k = A.shape
+    n = B.shape[1]
+    R = torch.empty((n_moduli, n, m), dtype=torch.uint8, device=A.device)
+    _use_torch_stream(A.device)
+    _check(ozfp4_residues(m, n, k, A.data_ptr(), lda, B.data_ptr(), ldb, n_moduli, R.data_ptr(), m),
+           "ozfp4_residues")
+    return R

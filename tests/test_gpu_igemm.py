@@ -1,0 +1,63 @@
+"""GPU parity of the bit-exact INT8 x INT8 -> INT32 product on FP4 limbs
+(Sec. III) against the integer oracle."""
+
+import numpy as np
+import pytest
+
+import oracle as o
+from gpu_util import announce, dev_cm, to_np
+from paper_2608_06812_amd.workloads import int8_inputs
+
+pytestmark = pytest.mark.gpu
+
+SEED = 20260811
+
+
+@pytest.mark.parametrize("m,n,k", [
+    (128, 64, 128), (1, 1, 1), (131, 67, 129), (300, 200, 1000), (64, 65, 4097), (17, 300, 2),
+])
+def test_igemm_s8_bit_exact(gpu_lib, m, n, k):
+    A, B = int8_inputs(m, n, k, SEED)
+    want = o.igemm_s8(A, B)
+    announce(f"igemm_s8 m={m} n={n} k={k}")
+    C = to_np(gpu_lib.igemm_s8(dev_cm(A), dev_cm(B)))
+    assert np.array_equal(C, want)
+
+
+def test_igemm_s8_extremes_at_max_k(gpu_lib):
+    """All -128 (the largest limb products) at k = 87381, the FP32-exactness
+    limit of the grouped accumulators; plus mixed signs."""
+    k = 87381
+    A = np.full((128, k), -128, dtype=np.int8)
+    B = np.full((k, 64), -128, dtype=np.int8)
+    A[1::2, :] = 127
+    B[:, 1::3] = -127
+    A[:, -1] = 1
+    want = o.igemm_s8(A, B)
+    announce(f"igemm_s8 extremes k={k}")
+    C = to_np(gpu_lib.igemm_s8(dev_cm(A), dev_cm(B)))
+    assert np.array_equal(C, want)
+
+
+def test_igemm_s8_k_zero(gpu_lib):
+    import torch
+    announce("igemm_s8 k=0")
+    C = gpu_lib.igemm_s8(dev_cm(np.zeros((4, 0), dtype=np.int8)), dev_cm(np.zeros((0, 3), dtype=np.int8)))
+    assert C.shape == (4, 3) and bool(torch.all(C == 0))
+
+
+@pytest.mark.slow
+def test_igemm_s8_8192_rows_sampled(gpu_lib):
+    """The INT8 configuration (8192^3): 48 whole rows and 48 whole columns
+    of C checked exactly (FP64 BLAS is exact here: |sum| <= 2^27)."""
+    A, B = int8_inputs(8192, 8192, 8192, SEED + 1)
+    announce("igemm_s8 8192^3")
+    Cd = gpu_lib.igemm_s8(dev_cm(A), dev_cm(B))
+    rng = np.random.default_rng(5)
+    rows = np.sort(rng.choice(8192, 48, replace=False))
+    cols = np.sort(rng.choice(8192, 48, replace=False))
+    import torch
+    got_rows = to_np(Cd[torch.as_tensor(rows, device="cuda")])
+    got_cols = to_np(Cd[:, torch.as_tensor(cols, device="cuda")])
+    assert np.array_equal(got_rows, o.igemm_s8(A[rows], B))
+    assert np.array_equal(got_cols, o.igemm_s8(A, B[:, cols]))

@@ -1,0 +1,129 @@
+"""Host-side checks of libozfp4.so that need no GPU: the library loads, it
+exports every entry point include/ozfp4.h declares, its host-only queries
+(moduli, capacities, two-limb tables, plane layout) agree with the oracle's
+independent derivation, and argument errors are reported before any GPU
+work."""
+
+import ctypes
+import os
+import re
+
+import pytest
+
+import oracle as o
+from paper_2608_06812_amd import ozfp4
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "ozfp4.h")
+
+
+def _declared_symbols():
+    text = open(HEADER).read()
+    return sorted(set(re.findall(r"\b(ozfp4_[a-z0-9_]+)\s*\(", text)))
+
+
+@pytest.fixture(scope="module")
+def lib():
+    if not os.path.exists(ozfp4.LIB_PATH):
+        from paper_2608_06812_amd import build
+        build.build()
+    return ozfp4.load()
+
+
+def test_header_declares_the_boundary():
+    names = _declared_symbols()
+    for required in ("ozfp4_dgemm", "ozfp4_igemm_s8", "ozfp4_set_stream", "ozfp4_finalize",
+                     "ozfp4_strerror", "ozfp4_scales", "ozfp4_limb_planes", "ozfp4_residues"):
+        assert required in names
+
+
+def test_library_exports_every_declared_symbol(lib):
+    for name in _declared_symbols():
+        assert hasattr(lib, name), name
+    # and the binding wraps each of them under the same name
+    for name in _declared_symbols():
+        assert callable(getattr(ozfp4, name)), name
+
+
+def test_moduli_match_oracle_and_paper(lib, paper):
+    assert ozfp4.ozfp4_moduli(19) == paper["moduli_L19"]
+    assert ozfp4.ozfp4_moduli(20) == o.select_moduli(20)
+
+
+def test_capacity_matches_oracle(lib):
+    for L in range(2, 21):
+        ms = o.select_moduli(L)
+        for k in (1, 2, 3, 100, 256, 4096, 8192, 16384, 32768, 65536, 131072):
+            try:
+                want = o.capacity_bits(k, ms)
+            except ValueError:
+                with pytest.raises(ozfp4.OzFP4Error) as ei:
+                    ozfp4.ozfp4_capacity(k, L)
+                assert ei.value.code == ozfp4.OZFP4_EMODULI
+                continue
+            assert ozfp4.ozfp4_capacity(k, L) == want, (k, L)
+
+
+def test_two_limb_tables_match_oracle(lib):
+    for idx, m in enumerate(o.select_moduli(20)):
+        got_m, table = ozfp4.ozfp4_two_limb_table(idx)
+        assert got_m == m
+        for r in range(m):
+            c0, c1 = o.two_limb_split(r, m)
+            assert table[r] == (o.e2m1_code(c0) | (o.e2m1_code(c1) << 4)), (m, r)
+
+
+def test_plane_layout(lib):
+    assert ozfp4.ozfp4_plane_layout(1, 1) == (128, 128, 128 * 64)
+    assert ozfp4.ozfp4_plane_layout(256, 256) == (256, 256, 256 * 128)
+    assert ozfp4.ozfp4_plane_layout(300, 129) == (384, 256, 384 * 128)
+
+
+def test_strerror(lib):
+    assert ozfp4.ozfp4_strerror(0) == "success"
+    for code in range(-6, 0):
+        assert ozfp4.ozfp4_strerror(code) != "unknown error code"
+    assert ozfp4.ozfp4_strerror(-99) == "unknown error code"
+
+
+@pytest.mark.parametrize("args,code", [
+    ((-1, 4, 4, 1, 4, 1, 4, 1, 4, 19), ozfp4.OZFP4_EINVAL),          # negative m
+    ((4, 4, 4, 1, 3, 1, 4, 1, 4, 19), ozfp4.OZFP4_EINVAL),           # lda < m
+    ((4, 4, 4, 1, 4, 1, 3, 1, 4, 19), ozfp4.OZFP4_EINVAL),           # ldb < k
+    ((4, 4, 4, 1, 4, 1, 4, 1, 3, 19), ozfp4.OZFP4_EINVAL),           # ldc < m
+    ((4, 4, 4, 0, 4, 1, 4, 1, 4, 19), ozfp4.OZFP4_EINVAL),           # null A
+    ((4, 4, 4, 1, 4, 0, 4, 1, 4, 19), ozfp4.OZFP4_EINVAL),           # null B
+    ((4, 4, 4, 1, 4, 1, 4, 1, 4, 1), ozfp4.OZFP4_EMODULI),           # too few moduli
+    ((4, 4, 4, 1, 4, 1, 4, 1, 4, 21), ozfp4.OZFP4_EMODULI),          # too many moduli
+    ((4, 4, 131073, 1, 4, 1, 131073, 1, 4, 19), ozfp4.OZFP4_EKBOUND),
+    ((4, 4, 65536, 1, 4, 1, 65536, 1, 4, 2), ozfp4.OZFP4_EMODULI),   # P too small for k
+])
+def test_dgemm_argument_errors_on_host(lib, args, code):
+    assert ozfp4.ozfp4_dgemm(*args) == code
+
+
+def test_dgemm_empty_is_noop(lib):
+    assert ozfp4.ozfp4_dgemm(0, 5, 5, 0, 1, 0, 5, 0, 1, 19) == ozfp4.OZFP4_OK
+    assert ozfp4.ozfp4_dgemm(5, 0, 5, 0, 5, 0, 5, 0, 5, 19) == ozfp4.OZFP4_OK
+
+
+@pytest.mark.parametrize("args,code", [
+    ((4, 4, 4, 1, 3, 1, 4, 1, 4), ozfp4.OZFP4_EINVAL),
+    ((4, 4, 4, 1, 4, 1, 4, 0, 4), ozfp4.OZFP4_EINVAL),               # null C
+    ((4, 4, 87382, 1, 4, 1, 87382, 1, 4), ozfp4.OZFP4_EKBOUND),
+])
+def test_igemm_argument_errors_on_host(lib, args, code):
+    assert ozfp4.ozfp4_igemm_s8(*args) == code
+
+
+def test_hook_argument_errors_on_host(lib):
+    assert ozfp4.ozfp4_residues(4, 4, 4, 1, 4, 1, 4, 19, 1, 3) == ozfp4.OZFP4_EINVAL   # ldr < m
+    assert ozfp4.ozfp4_scales(4, 4, 4, 1, 4, 1, 4, 19, 0, 1) == ozfp4.OZFP4_EINVAL     # null s
+    assert ozfp4.ozfp4_limb_planes(4, 4, 4, 1, 4, 1, 4, 19, 1, 0) == ozfp4.OZFP4_EINVAL
+
+
+def test_binding_refuses_missing_library(monkeypatch, tmp_path):
+    monkeypatch.setattr(ozfp4, "_lib", None)
+    monkeypatch.setattr(ozfp4, "LIB_PATH", str(tmp_path / "missing.so"))
+    with pytest.raises(RuntimeError):
+        ozfp4.load()
