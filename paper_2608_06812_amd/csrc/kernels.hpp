@@ -256,7 +256,10 @@ __global__ __launch_bounds__(256) void k_encode_s8(
 // contiguous range of logical tiles, and order tiles in groups of kGroupM
 // tile rows so that the blocks an XCD runs together share A and B panels
 // in its L2.
-constexpr int kGroupM = 4;
+#ifndef OZFP4_GROUP_M
+#define OZFP4_GROUP_M 8
+#endif
+constexpr int kGroupM = OZFP4_GROUP_M;
 __device__ __forceinline__ void tile_coords(int64_t bid, int64_t nblocks, int64_t tiles_m,
                                             int64_t tiles_n, int* l, int64_t* tm, int64_t* tn) {
   const int64_t xcd = bid & 7, local = bid >> 3;
@@ -297,38 +300,115 @@ struct StageLayout {
   }
 };
 
+// LDS DMA: each lane copies 16 bytes from global memory to LDS at
+// lds_base + 16 * lane (global_load_lds_dwordx4); lds_base must be
+// wave-uniform. Completion is tracked by vmcnt like any vector load.
+__device__ __forceinline__ void dma16(const uint8_t* gsrc, uint8_t* lds_base) {
+  __builtin_amdgcn_global_load_lds(gsrc, (__attribute__((address_space(3))) void*)lds_base, 16, 0, 0);
+}
+
+// s_waitcnt vmcnt(N) lgkmcnt(0) (expcnt untouched): this wave's vector
+// loads except the newest N have landed, and its LDS reads are complete.
+template <int N>
+__device__ __forceinline__ void wait_vm_lgkm0() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4));
+}
+
+__device__ __forceinline__ void block_sync() {
+  asm volatile("" ::: "memory");
+  __builtin_amdgcn_s_barrier();
+  asm volatile("" ::: "memory");
+}
+
+// Operand fragments of one k fragment (64 k) held by one wave: [plane][i].
+struct HalfFrags {
+  v4i a[2][2];
+  v4i b[2][2];
+};
+
+__device__ __forceinline__ void read_half(HalfFrags& F, const uint8_t* sb, int kbl, int wm, int wn,
+                                          int lane) {
+  using SL = StageLayout<2>;
+#pragma unroll
+  for (int p = 0; p < 2; ++p)
+#pragma unroll
+    for (int i = 0; i < 2; ++i) {
+      F.a[p][i] = *reinterpret_cast<const v4i*>(sb + SL::frag(0, p, 2 * wm + i, kbl) + lane * 16);
+      F.b[p][i] = *reinterpret_cast<const v4i*>(sb + SL::frag(1, p, 2 * wn + i, kbl) + lane * 16);
+    }
+}
+
+// acc0 += a0 b0, acc1 += a0 b1 + a1 b0, acc2 += a1 b1 over one k fragment
+__device__ __forceinline__ void compute_half(v16f (&acc)[3][2][2], const HalfFrags& F) {
+#pragma unroll
+  for (int i = 0; i < 2; ++i)
+#pragma unroll
+    for (int j = 0; j < 2; ++j) {
+      acc[0][i][j] = mfma_fp4(F.a[0][i], F.b[0][j], acc[0][i][j]);
+      acc[1][i][j] = mfma_fp4(F.a[0][i], F.b[1][j], acc[1][i][j]);
+      acc[2][i][j] = mfma_fp4(F.a[1][i], F.b[1][j], acc[2][i][j]);
+    }
+#pragma unroll
+  for (int i = 0; i < 2; ++i)
+#pragma unroll
+    for (int j = 0; j < 2; ++j) acc[1][i][j] = mfma_fp4(F.a[1][i], F.b[0][j], acc[1][i][j]);
+}
+
+// s_waitcnt vmcnt(8 * stages) lgkmcnt(0) for a runtime stage count
+__device__ __forceinline__ void wait_stages(int stages) {
+  if (stages >= 3) wait_vm_lgkm0<24>();
+  else if (stages == 2) wait_vm_lgkm0<16>();
+  else if (stages == 1) wait_vm_lgkm0<8>();
+  else wait_vm_lgkm0<0>();
+}
+
 // Dgemm variant: planes 2l (c0) and 2l+1 (c1) of modulus l; accumulators
 // acc0 = a0 b0, acc1 = a0 b1 + a1 b0, acc2 = a1 b1; epilogue
 // r = (4 acc0 + 52 acc1 + 676 acc2) mod m, one byte per element.
+// Operand stages stream through a ring of kStages LDS slots by LDS DMA
+// (each wave copies 8 whole fragments, 1 KiB each and contiguous in HBM,
+// per stage). Each wave moves stage s + 1 from LDS into a second register
+// set while its MFMAs consume stage s; a slot is refilled only after every
+// wave has its contents in registers.
+#ifndef OZFP4_STAGES
+#define OZFP4_STAGES 4
+#endif
+constexpr int kStages = OZFP4_STAGES;
+static_assert(kStages >= 2 && kStages <= 4, "ring depth");
 __global__ __launch_bounds__(256, 1) void k_gemm_res(
     const uint8_t* __restrict__ PA, const uint8_t* __restrict__ PB, uint8_t* __restrict__ R,
     int64_t plane_a, int64_t plane_b, int64_t kblocks, int64_t tiles_m, int64_t tiles_n,
     int64_t nblocks, int64_t ldr, int64_t rplane, const ModConst* __restrict__ mc) {
   constexpr int NP = 2;
   using SL = StageLayout<NP>;
-  __shared__ __attribute__((aligned(16))) uint8_t lds[2 * SL::kBytes];
+  static_assert(SL::kBytes == 32 * kFragBytes, "32 fragments per stage");
+  __shared__ __attribute__((aligned(1024))) uint8_t lds[kStages * SL::kBytes];
 
   int l;
   int64_t tm, tn;
   tile_coords(blockIdx.x, nblocks, tiles_m, tiles_n, &l, &tm, &tn);
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int wm = wave >> 1, wn = wave & 1;
 
-  // source of chunk q of this thread in stage s: piece = tid & 63,
-  // kbl = (tid >> 6) & 1, rbl = ((tid >> 7) & 1) + 2 (q & 1),
-  // plane = (q >> 1) % NP, op = (q >> 1) / NP
-  // uniform part of each source (plane, tile, 64-line half) + one
-  // per-thread offset
-  const int64_t toff = (((tid >> 7) & 1) * kblocks + ((tid >> 6) & 1)) * kFragBytes + (tid & 63) * 16;
-  const uint8_t* gbase[SL::kPerThread];
+  // fragment f = wave * 8 + j of a stage: kbl = f & 1, 32-line block
+  // (f >> 1) & 3, plane (f >> 3) & 1, operand f >> 4 (LDS order of SL::frag)
+  const uint8_t* gsrc[8];
 #pragma unroll
-  for (int q = 0; q < SL::kPerThread; ++q) {
-    const int p = (q >> 1) % NP, op = (q >> 1) / NP;
-    const int64_t rb0 = (op == 0 ? tm : tn) * 4 + 2 * (q & 1);
-    gbase[q] = (op == 0 ? PA + (int64_t)(2 * l + p) * plane_a : PB + (int64_t)(2 * l + p) * plane_b) +
-               rb0 * kblocks * kFragBytes;
+  for (int j = 0; j < 8; ++j) {
+    const int f = wave * 8 + j;
+    const int kbl = f & 1, rbl = (f >> 1) & 3, p = (f >> 3) & 1, op = f >> 4;
+    gsrc[j] = (op == 0 ? PA + (int64_t)(2 * l + p) * plane_a + (tm * 4 + rbl) * kblocks * kFragBytes
+                       : PB + (int64_t)(2 * l + p) * plane_b + (tn * 4 + rbl) * kblocks * kFragBytes) +
+              kbl * kFragBytes + lane * 16;
   }
   const int nst = (int)(kblocks / 2);
+  auto issue = [&](int s) {
+    uint8_t* dst = lds + (s % kStages) * SL::kBytes + wave * 8 * kFragBytes;
+#pragma unroll
+    for (int j = 0; j < 8; ++j) dma16(gsrc[j] + (int64_t)s * 2 * kFragBytes, dst + j * kFragBytes);
+  };
 
   v16f acc[3][2][2];
 #pragma unroll
@@ -340,52 +420,39 @@ __global__ __launch_bounds__(256, 1) void k_gemm_res(
 #pragma unroll
         for (int v = 0; v < 16; ++v) acc[a][i][j][v] = 0.0f;
 
-  v4i stage[SL::kPerThread];
+  const int pro = min(kStages, nst);
 #pragma unroll
-  for (int q = 0; q < SL::kPerThread; ++q) stage[q] = *reinterpret_cast<const v4i*>(gbase[q] + toff);
-#pragma unroll
-  for (int q = 0; q < SL::kPerThread; ++q)
-    *reinterpret_cast<v4i*>(lds + (q * 256 + tid) * 16) = stage[q];
-  __syncthreads();
-
-  for (int s = 0; s < nst; ++s) {
-    const int buf = s & 1;
+  for (int s = 0; s < kStages; ++s)
+    if (s < pro) issue(s);
+  wait_stages(pro - 1);
+  block_sync();
+  // k fragment 1 of stage s is read while fragment 0 computes; the next
+  // stage's fragment 0 is read (after the barrier) while fragment 1 computes.
+  // Steady state without branches (the refill is always due), then the tail.
+  HalfFrags F0, F1;
+  read_half(F0, lds, 0, wm, wn, lane);
+  int s = 0;
+  for (; s + kStages < nst; ++s) {
+    read_half(F1, lds + (s % kStages) * SL::kBytes, 1, wm, wn, lane);
+    compute_half(acc, F0);
+    __builtin_amdgcn_sched_barrier(0);
+    wait_vm_lgkm0<8 * (kStages - 2)>();   // stage s + 1 landed; own reads done
+    block_sync();                         // ... for every wave
+    issue(s + kStages);                   // refills the slot of stage s
+    read_half(F0, lds + ((s + 1) % kStages) * SL::kBytes, 0, wm, wn, lane);
+    compute_half(acc, F1);
+    __builtin_amdgcn_sched_barrier(0);
+  }
+  for (; s < nst; ++s) {
+    read_half(F1, lds + (s % kStages) * SL::kBytes, 1, wm, wn, lane);
+    compute_half(acc, F0);
+    __builtin_amdgcn_sched_barrier(0);
     if (s + 1 < nst) {
-#pragma unroll
-      for (int q = 0; q < SL::kPerThread; ++q)
-        stage[q] = *reinterpret_cast<const v4i*>(gbase[q] + toff + (int64_t)(s + 1) * 2 * kFragBytes);
+      wait_stages(min(kStages - 2, nst - 2 - s));
+      block_sync();
+      read_half(F0, lds + ((s + 1) % kStages) * SL::kBytes, 0, wm, wn, lane);
     }
-    const uint8_t* sb = lds + buf * SL::kBytes;
-#pragma unroll
-    for (int kbl = 0; kbl < 2; ++kbl) {
-      v4i a[NP][2], b[NP][2];
-#pragma unroll
-      for (int p = 0; p < NP; ++p)
-#pragma unroll
-        for (int i = 0; i < 2; ++i) {
-          a[p][i] = *reinterpret_cast<const v4i*>(sb + SL::frag(0, p, 2 * wm + i, kbl) + lane * 16);
-          b[p][i] = *reinterpret_cast<const v4i*>(sb + SL::frag(1, p, 2 * wn + i, kbl) + lane * 16);
-        }
-#pragma unroll
-      for (int i = 0; i < 2; ++i)
-#pragma unroll
-        for (int j = 0; j < 2; ++j) {
-          acc[0][i][j] = mfma_fp4(a[0][i], b[0][j], acc[0][i][j]);
-          acc[1][i][j] = mfma_fp4(a[0][i], b[1][j], acc[1][i][j]);
-          acc[2][i][j] = mfma_fp4(a[1][i], b[1][j], acc[2][i][j]);
-        }
-#pragma unroll
-      for (int i = 0; i < 2; ++i)
-#pragma unroll
-        for (int j = 0; j < 2; ++j) acc[1][i][j] = mfma_fp4(a[1][i], b[0][j], acc[1][i][j]);
-    }
-    if (s + 1 < nst) {
-      uint8_t* db = lds + (buf ^ 1) * SL::kBytes;
-#pragma unroll
-      for (int q = 0; q < SL::kPerThread; ++q)
-        *reinterpret_cast<v4i*>(db + (q * 256 + tid) * 16) = stage[q];
-    }
-    __syncthreads();
+    compute_half(acc, F1);
   }
 
   // epilogue: residue composition mod m (Sec. V-A, Lemma 3)
