@@ -116,6 +116,8 @@ def main() -> int:
     ap.add_argument("--no-native", action="store_true")
     ap.add_argument("--no-int8", action="store_true")
     ap.add_argument("--no-accuracy", action="store_true")
+    ap.add_argument("--copy-calibration", action="store_true",
+                    help="also run a plain 1 GiB device copy (reference for HBM byte counters)")
     args = ap.parse_args()
 
     world = int(os.environ.get("WORLD_SIZE", "1"))
@@ -200,6 +202,15 @@ def main() -> int:
         "model_ms": model_ms,
         "compute_stage_tflops": 2.0 * N ** 3 / (gemm_ms + stages[4]) / 1e9,
     }
+
+    if args.copy_calibration:
+        src = torch.empty(1 << 27, dtype=torch.float64, device="cuda").fill_(1.0)
+        dst = torch.empty_like(src)
+        for _ in range(3):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        result["copy_calibration_bytes"] = {"read": src.numel() * 8, "write": dst.numel() * 8}
+        del src, dst
 
     if not args.no_accuracy:
         rng = np.random.default_rng(11)

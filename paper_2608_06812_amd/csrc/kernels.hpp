@@ -27,8 +27,9 @@ typedef float v16f __attribute__((ext_vector_type(16)));
 constexpr int kFragLines = 32;   // lines per fragment
 constexpr int kFragK = 64;       // k per fragment
 constexpr int kFragBytes = 1024;
-constexpr int kTile = 128;       // GEMM block tile (lines of A and of B)
+constexpr int kTile = 256;       // line padding of every operand (multiple of both GEMM block tiles)
 constexpr int kStageK = 128;     // k per pipeline stage (two fragments)
+constexpr int kMinKPad = 384;    // k is padded to at least three stages
 
 constexpr uint64_t kAbsMask = 0x7fffffffffffffffull;
 constexpr uint64_t kNonFinite = 0x7ff0000000000000ull;
@@ -257,7 +258,7 @@ __global__ __launch_bounds__(256) void k_encode_s8(
 // tile rows so that the blocks an XCD runs together share A and B panels
 // in its L2.
 #ifndef OZFP4_GROUP_M
-#define OZFP4_GROUP_M 8
+#define OZFP4_GROUP_M 4
 #endif
 constexpr int kGroupM = OZFP4_GROUP_M;
 __device__ __forceinline__ void tile_coords(int64_t bid, int64_t nblocks, int64_t tiles_m,
@@ -321,69 +322,35 @@ __device__ __forceinline__ void block_sync() {
   asm volatile("" ::: "memory");
 }
 
-// Operand fragments of one k fragment (64 k) held by one wave: [plane][i].
-struct HalfFrags {
-  v4i a[2][2];
-  v4i b[2][2];
-};
-
-__device__ __forceinline__ void read_half(HalfFrags& F, const uint8_t* sb, int kbl, int wm, int wn,
-                                          int lane) {
-  using SL = StageLayout<2>;
-#pragma unroll
-  for (int p = 0; p < 2; ++p)
-#pragma unroll
-    for (int i = 0; i < 2; ++i) {
-      F.a[p][i] = *reinterpret_cast<const v4i*>(sb + SL::frag(0, p, 2 * wm + i, kbl) + lane * 16);
-      F.b[p][i] = *reinterpret_cast<const v4i*>(sb + SL::frag(1, p, 2 * wn + i, kbl) + lane * 16);
-    }
-}
-
-// acc0 += a0 b0, acc1 += a0 b1 + a1 b0, acc2 += a1 b1 over one k fragment
-__device__ __forceinline__ void compute_half(v16f (&acc)[3][2][2], const HalfFrags& F) {
-#pragma unroll
-  for (int i = 0; i < 2; ++i)
-#pragma unroll
-    for (int j = 0; j < 2; ++j) {
-      acc[0][i][j] = mfma_fp4(F.a[0][i], F.b[0][j], acc[0][i][j]);
-      acc[1][i][j] = mfma_fp4(F.a[0][i], F.b[1][j], acc[1][i][j]);
-      acc[2][i][j] = mfma_fp4(F.a[1][i], F.b[1][j], acc[2][i][j]);
-    }
-#pragma unroll
-  for (int i = 0; i < 2; ++i)
-#pragma unroll
-    for (int j = 0; j < 2; ++j) acc[1][i][j] = mfma_fp4(F.a[1][i], F.b[0][j], acc[1][i][j]);
-}
-
-// s_waitcnt vmcnt(8 * stages) lgkmcnt(0) for a runtime stage count
-__device__ __forceinline__ void wait_stages(int stages) {
-  if (stages >= 3) wait_vm_lgkm0<24>();
-  else if (stages == 2) wait_vm_lgkm0<16>();
-  else if (stages == 1) wait_vm_lgkm0<8>();
-  else wait_vm_lgkm0<0>();
-}
-
-// Dgemm variant: planes 2l (c0) and 2l+1 (c1) of modulus l; accumulators
-// acc0 = a0 b0, acc1 = a0 b1 + a1 b0, acc2 = a1 b1; epilogue
+// Dgemm residue GEMM: planes 2l (c0) and 2l+1 (c1) of modulus l;
+// accumulators acc0 = a0 b0, acc1 = a0 b1 + a1 b0, acc2 = a1 b1; epilogue
 // r = (4 acc0 + 52 acc1 + 676 acc2) mod m, one byte per element.
-// Operand stages stream through a ring of kStages LDS slots by LDS DMA
-// (each wave copies 8 whole fragments, 1 KiB each and contiguous in HBM,
-// per stage). Each wave moves stage s + 1 from LDS into a second register
-// set while its MFMAs consume stage s; a slot is refilled only after every
-// wave has its contents in registers.
-#ifndef OZFP4_STAGES
-#define OZFP4_STAGES 4
-#endif
-constexpr int kStages = OZFP4_STAGES;
-static_assert(kStages >= 2 && kStages <= 4, "ring depth");
-__global__ __launch_bounds__(256, 1) void k_gemm_res(
+//
+// Block tile 256 (lines of A) x 128 (lines of B), k in stages of 128. Eight
+// waves, two per SIMD, each 64 x 64 (2 x 2 MFMA tiles of 32 x 32, three
+// accumulator sets = 192 registers, everything within 256 registers so two
+// waves share a SIMD and cover each other's LDS and barrier waits). A stage
+// is 48 fragments (A: 2 planes x 8 line blocks x 2 k fragments, then B:
+// 2 planes x 4 line blocks x 2 k fragments), 48 KiB, copied into a 3-slot
+// LDS ring by LDS DMA (6 whole fragments per wave, each 1 KiB contiguous in
+// HBM), up to three stages ahead of the one being multiplied.
+constexpr int kTileM = 256;        // lines of A per block
+constexpr int kTileN = 128;        // lines of B per block
+constexpr int kRing = 3;           // LDS slots
+constexpr int kWaves = 8;
+constexpr int kStageFrags = 48;
+constexpr int kStageBytes = kStageFrags * kFragBytes;
+constexpr int kDmaPerWave = kStageFrags / kWaves;   // 6
+
+// LDS offset of fragment (plane p, line block rb / cb, k fragment kbl)
+__device__ __forceinline__ constexpr int fragA(int p, int rb, int kbl) { return ((p * 8 + rb) * 2 + kbl) * kFragBytes; }
+__device__ __forceinline__ constexpr int fragB(int p, int cb, int kbl) { return (32 + (p * 4 + cb) * 2 + kbl) * kFragBytes; }
+
+__global__ __launch_bounds__(512, 1) void k_gemm_res(
     const uint8_t* __restrict__ PA, const uint8_t* __restrict__ PB, uint8_t* __restrict__ R,
     int64_t plane_a, int64_t plane_b, int64_t kblocks, int64_t tiles_m, int64_t tiles_n,
     int64_t nblocks, int64_t ldr, int64_t rplane, const ModConst* __restrict__ mc) {
-  constexpr int NP = 2;
-  using SL = StageLayout<NP>;
-  static_assert(SL::kBytes == 32 * kFragBytes, "32 fragments per stage");
-  __shared__ __attribute__((aligned(1024))) uint8_t lds[kStages * SL::kBytes];
+  __shared__ __attribute__((aligned(1024))) uint8_t lds[kRing * kStageBytes];
 
   int l;
   int64_t tm, tn;
@@ -391,23 +358,28 @@ __global__ __launch_bounds__(256, 1) void k_gemm_res(
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int wm = wave >> 1, wn = wave & 1;
+  const int rbw = 2 * wm, cbw = 2 * wn;   // this wave's first A / B line block
 
-  // fragment f = wave * 8 + j of a stage: kbl = f & 1, 32-line block
-  // (f >> 1) & 3, plane (f >> 3) & 1, operand f >> 4 (LDS order of SL::frag)
-  const uint8_t* gsrc[8];
+  // fragment f = wave * 6 + j of a stage (LDS offset f KiB): uniform base
+  const uint8_t* gsrc[kDmaPerWave];
 #pragma unroll
-  for (int j = 0; j < 8; ++j) {
-    const int f = wave * 8 + j;
-    const int kbl = f & 1, rbl = (f >> 1) & 3, p = (f >> 3) & 1, op = f >> 4;
-    gsrc[j] = (op == 0 ? PA + (int64_t)(2 * l + p) * plane_a + (tm * 4 + rbl) * kblocks * kFragBytes
-                       : PB + (int64_t)(2 * l + p) * plane_b + (tn * 4 + rbl) * kblocks * kFragBytes) +
-              kbl * kFragBytes + lane * 16;
+  for (int j = 0; j < kDmaPerWave; ++j) {
+    const int f = wave * kDmaPerWave + j;
+    if (f < 32) {
+      const int kbl = f & 1, rb = (f >> 1) & 7, p = f >> 4;
+      gsrc[j] = PA + (int64_t)(2 * l + p) * plane_a + ((tm * 8 + rb) * kblocks + kbl) * kFragBytes;
+    } else {
+      const int g = f - 32, kbl = g & 1, cb = (g >> 1) & 3, p = g >> 3;
+      gsrc[j] = PB + (int64_t)(2 * l + p) * plane_b + ((tn * 4 + cb) * kblocks + kbl) * kFragBytes;
+    }
   }
+  const int lane16 = lane * 16;
   const int nst = (int)(kblocks / 2);
   auto issue = [&](int s) {
-    uint8_t* dst = lds + (s % kStages) * SL::kBytes + wave * 8 * kFragBytes;
+    uint8_t* dst = lds + (s % kRing) * kStageBytes + wave * kDmaPerWave * kFragBytes;
 #pragma unroll
-    for (int j = 0; j < 8; ++j) dma16(gsrc[j] + (int64_t)s * 2 * kFragBytes, dst + j * kFragBytes);
+    for (int j = 0; j < kDmaPerWave; ++j)
+      dma16(gsrc[j] + (int64_t)s * 2 * kFragBytes + lane16, dst + j * kFragBytes);
   };
 
   v16f acc[3][2][2];
@@ -420,40 +392,79 @@ __global__ __launch_bounds__(256, 1) void k_gemm_res(
 #pragma unroll
         for (int v = 0; v < 16; ++v) acc[a][i][j][v] = 0.0f;
 
-  const int pro = min(kStages, nst);
+  // Per stage: k fragment 0 (read, 16 MFMAs), k fragment 1 (read, 12
+  // MFMAs), then the stage handover: wait until stage s + 1 has landed and
+  // this wave's reads are done, barrier, refill the slot of stage s with
+  // stage s + 3, and only then issue the last 4 MFMAs of stage s, so the
+  // matrix pipe still has queued work while the waves synchronise.
 #pragma unroll
-  for (int s = 0; s < kStages; ++s)
-    if (s < pro) issue(s);
-  wait_stages(pro - 1);
+  for (int s = 0; s < kRing; ++s) issue(s);     // nst >= kRing by padding
+  wait_vm_lgkm0<2 * kDmaPerWave>();
   block_sync();
-  // k fragment 1 of stage s is read while fragment 0 computes; the next
-  // stage's fragment 0 is read (after the barrier) while fragment 1 computes.
-  // Steady state without branches (the refill is always due), then the tail.
-  HalfFrags F0, F1;
-  read_half(F0, lds, 0, wm, wn, lane);
+
+  v4i a[2][2], b[2][2];   // [plane][i] of A, [plane][j] of B
+  auto read_frags = [&](const uint8_t* sb, int kbl) {
+#pragma unroll
+    for (int p = 0; p < 2; ++p)
+#pragma unroll
+      for (int i = 0; i < 2; ++i) {
+        a[p][i] = *reinterpret_cast<const v4i*>(sb + fragA(p, rbw + i, kbl) + lane16);
+        b[p][i] = *reinterpret_cast<const v4i*>(sb + fragB(p, cbw + i, kbl) + lane16);
+      }
+  };
+  // every product except a1 b1 (acc2), which is issued after the handover
+  auto mfma_head = [&]() {
+#pragma unroll
+    for (int i = 0; i < 2; ++i)
+#pragma unroll
+      for (int j = 0; j < 2; ++j) {
+        acc[0][i][j] = mfma_fp4(a[0][i], b[0][j], acc[0][i][j]);
+        acc[1][i][j] = mfma_fp4(a[0][i], b[1][j], acc[1][i][j]);
+      }
+#pragma unroll
+    for (int i = 0; i < 2; ++i)
+#pragma unroll
+      for (int j = 0; j < 2; ++j) acc[1][i][j] = mfma_fp4(a[1][i], b[0][j], acc[1][i][j]);
+  };
+  auto mfma_tail = [&]() {
+#pragma unroll
+    for (int i = 0; i < 2; ++i)
+#pragma unroll
+      for (int j = 0; j < 2; ++j) acc[2][i][j] = mfma_fp4(a[1][i], b[1][j], acc[2][i][j]);
+  };
+  auto stage_body = [&](int s) {   // everything of stage s before the handover
+    const uint8_t* sb = lds + (s % kRing) * kStageBytes;
+    read_frags(sb, 0);
+    mfma_head();
+    mfma_tail();
+    __builtin_amdgcn_sched_barrier(0);
+    read_frags(sb, 1);
+    mfma_head();
+    __builtin_amdgcn_sched_barrier(0);
+  };
+
   int s = 0;
-  for (; s + kStages < nst; ++s) {
-    read_half(F1, lds + (s % kStages) * SL::kBytes, 1, wm, wn, lane);
-    compute_half(acc, F0);
-    __builtin_amdgcn_sched_barrier(0);
-    wait_vm_lgkm0<8 * (kStages - 2)>();   // stage s + 1 landed; own reads done
-    block_sync();                         // ... for every wave
-    issue(s + kStages);                   // refills the slot of stage s
-    read_half(F0, lds + ((s + 1) % kStages) * SL::kBytes, 0, wm, wn, lane);
-    compute_half(acc, F1);
+  for (; s + kRing < nst; ++s) {   // steady state: the refill is always due
+    stage_body(s);
+    wait_vm_lgkm0<kDmaPerWave>();  // stage s + 1 landed; reads of stage s done
+    block_sync();
+    issue(s + kRing);              // refills the slot of stage s
+    mfma_tail();
     __builtin_amdgcn_sched_barrier(0);
   }
-  for (; s < nst; ++s) {
-    read_half(F1, lds + (s % kStages) * SL::kBytes, 1, wm, wn, lane);
-    compute_half(acc, F0);
-    __builtin_amdgcn_sched_barrier(0);
-    if (s + 1 < nst) {
-      wait_stages(min(kStages - 2, nst - 2 - s));
-      block_sync();
-      read_half(F0, lds + ((s + 1) % kStages) * SL::kBytes, 0, wm, wn, lane);
-    }
-    compute_half(acc, F1);
-  }
+  // the last three stages (k is padded to at least three stages)
+  stage_body(s);
+  wait_vm_lgkm0<kDmaPerWave>();
+  block_sync();
+  mfma_tail();
+  __builtin_amdgcn_sched_barrier(0);
+  stage_body(s + 1);
+  wait_vm_lgkm0<0>();
+  block_sync();
+  mfma_tail();
+  __builtin_amdgcn_sched_barrier(0);
+  stage_body(s + 2);
+  mfma_tail();
 
   // epilogue: residue composition mod m (Sec. V-A, Lemma 3)
   const int m = mc->m[l];
@@ -463,10 +474,10 @@ __global__ __launch_bounds__(256, 1) void k_gemm_res(
   for (int i = 0; i < 2; ++i)
 #pragma unroll
     for (int j = 0; j < 2; ++j) {
-      const int64_t col = tn * kTile + wn * 64 + j * 32 + (lane & 31);
+      const int64_t col = tn * kTileN + wn * 64 + j * 32 + (lane & 31);
 #pragma unroll
       for (int g = 0; g < 4; ++g) {
-        const int64_t row = tm * kTile + wm * 64 + i * 32 + g * 8 + (lane >> 5) * 4;
+        const int64_t row = tm * kTileM + wm * 64 + i * 32 + g * 8 + (lane >> 5) * 4;
         uint32_t word = 0;
 #pragma unroll
         for (int v4 = 0; v4 < 4; ++v4) {
@@ -489,6 +500,7 @@ __global__ __launch_bounds__(256, 1) void k_gemm_res(
 // four waves of 64 x 32 (2 x 1 MFMA tiles) so the five accumulator sets stay
 // in registers. LDS stage: A [plane][32-line block 0..3][k fragment] then
 // B [plane][32-line block 0..1][k fragment], 1 KiB each.
+constexpr int kTileS8M = 128;
 constexpr int kTileS8N = 64;
 __global__ __launch_bounds__(256, 1) void k_gemm_s8(
     const uint8_t* __restrict__ PA, const uint8_t* __restrict__ PB, int32_t* __restrict__ C,
@@ -583,7 +595,7 @@ __global__ __launch_bounds__(256, 1) void k_gemm_s8(
   for (int i = 0; i < 2; ++i)
 #pragma unroll
     for (int v = 0; v < 16; ++v) {
-      const int64_t row = tm * kTile + wm * 64 + i * 32 + (v >> 2) * 8 + (lane >> 5) * 4 + (v & 3);
+      const int64_t row = tm * kTileS8M + wm * 64 + i * 32 + (v >> 2) * 8 + (lane >> 5) * 4 + (v & 3);
       uint32_t c = (uint32_t)(int)(4.0f * acc[0][i][v]);
       c += 13u * (uint32_t)(int)(4.0f * acc[1][i][v]);
       c += 169u * (uint32_t)(int)(4.0f * acc[2][i][v]);

@@ -127,7 +127,7 @@ int make_dgemm_plan(int64_t m, int64_t n, int64_t k, int L, DgemmPlan* p) {
   if (!capacity_split(T->P[L], k, &p->cA, &p->cB)) return OZFP4_EMODULI;
   p->m_pad = round_up(m, kTile);
   p->n_pad = round_up(n, kTile);
-  p->k_pad = round_up(k, kStageK);
+  p->k_pad = std::max<int64_t>(kMinKPad, round_up(k, kStageK));
   p->kblocks = p->k_pad / kFragK;
   p->plane_a = p->m_pad * p->k_pad / 2;
   p->plane_b = p->n_pad * p->k_pad / 2;
@@ -202,9 +202,9 @@ int run_dgemm(const DgemmPlan& p, DeviceState* d, const double* A, int64_t lda, 
   if (last < 3) return OZFP4_OK;
 
   // stage 3: fused residue GEMM for all moduli
-  const int64_t tiles_m = p.m_pad / kTile, tiles_n = p.n_pad / kTile;
+  const int64_t tiles_m = p.m_pad / kTileM, tiles_n = p.n_pad / kTileN;
   const int64_t nblocks = tiles_m * tiles_n * L;
-  hipLaunchKernelGGL(k_gemm_res, dim3((unsigned)nblocks), dim3(256), 0, g_stream, pa, pb, R,
+  hipLaunchKernelGGL(k_gemm_res, dim3((unsigned)nblocks), dim3(kWaves * 64), 0, g_stream, pa, pb, R,
                      p.plane_a, p.plane_b, p.kblocks, tiles_m, tiles_n, nblocks, p.m_pad,
                      p.m_pad * p.n_pad, d->d_mod);
   HIP_TRY(hipGetLastError());
@@ -292,7 +292,7 @@ int ozfp4_igemm_s8(int64_t m, int64_t n, int64_t k, const int8_t* A, int64_t lda
   }
   if (!A || !B) return OZFP4_EINVAL;
   const int64_t m_pad = round_up(m, kTile), n_pad = round_up(n, kTile);
-  const int64_t k_pad = round_up(k, kStageK), kblocks = k_pad / kFragK;
+  const int64_t k_pad = std::max<int64_t>(kMinKPad, round_up(k, kStageK)), kblocks = k_pad / kFragK;
   const int64_t plane_a = m_pad * k_pad / 2, plane_b = n_pad * k_pad / 2;
   const size_t off_pb = align256((size_t)plane_a * 3);
   rc = ensure_workspace(d, off_pb + align256((size_t)plane_b * 3));
@@ -307,7 +307,7 @@ int ozfp4_igemm_s8(int64_t m, int64_t n, int64_t k, const int8_t* A, int64_t lda
   hipLaunchKernelGGL(k_encode_s8, dim3(encode_grid(nfb)), dim3(256), 0, g_stream, B, ldb,
                      (int64_t)1, n, k, pb, plane_b, nfb, kblocks, d->d_lut8);
   record(d, 2);
-  const int64_t tiles_m = m_pad / kTile, tiles_n = n_pad / kTileS8N;
+  const int64_t tiles_m = m_pad / kTileS8M, tiles_n = n_pad / kTileS8N;
   const int64_t nblocks = tiles_m * tiles_n;
   hipLaunchKernelGGL(k_gemm_s8, dim3((unsigned)nblocks), dim3(256), 0, g_stream, pa, pb, C,
                      plane_a, plane_b, kblocks, tiles_m, tiles_n, nblocks, m, n, ldc);
@@ -397,7 +397,7 @@ int ozfp4_plane_layout(int64_t lines, int64_t k, int64_t* rows_pad, int64_t* k_p
                        int64_t* bytes_per_plane) {
   if (lines < 0 || k < 0 || !rows_pad || !k_pad || !bytes_per_plane) return OZFP4_EINVAL;
   *rows_pad = round_up(lines, kTile);
-  *k_pad = round_up(k, kStageK);
+  *k_pad = std::max<int64_t>(kMinKPad, round_up(k, kStageK));
   *bytes_per_plane = *rows_pad * *k_pad / 2;
   return OZFP4_OK;
 }

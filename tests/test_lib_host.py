@@ -74,9 +74,11 @@ def test_two_limb_tables_match_oracle(lib):
 
 
 def test_plane_layout(lib):
-    assert ozfp4.ozfp4_plane_layout(1, 1) == (128, 128, 128 * 64)
-    assert ozfp4.ozfp4_plane_layout(256, 256) == (256, 256, 256 * 128)
-    assert ozfp4.ozfp4_plane_layout(300, 129) == (384, 256, 384 * 128)
+    # lines padded to 256, k to a multiple of 128 and at least 384
+    assert ozfp4.ozfp4_plane_layout(1, 1) == (256, 384, 256 * 192)
+    assert ozfp4.ozfp4_plane_layout(256, 256) == (256, 384, 256 * 192)
+    assert ozfp4.ozfp4_plane_layout(300, 129) == (512, 384, 512 * 192)
+    assert ozfp4.ozfp4_plane_layout(300, 1000) == (512, 1024, 512 * 512)
 
 
 def test_strerror(lib):
