@@ -43,7 +43,8 @@ __all__ = [
     "residue_products", "crt_reconstruct", "crt_reconstruct_paper",
     "round_scaled", "dgemm", "dgemm_definition", "int8_limbs", "igemm_s8",
     "igemm_s8_limbs", "fp32_exact_bound", "fp32_accumulate_emulated",
-    "exact_product_entry", "normalized_error", "MAX_K_FP32",
+    "exact_product_entry", "normalized_error", "exact_block", "normalized_errors_block",
+    "MAX_K_FP32",
 ]
 
 
@@ -571,3 +572,80 @@ def normalized_error(C_ij: float, A: np.ndarray, B: np.ndarray, i: int, j: int) 
     if denom == 0:
         return 0.0
     return float(abs(Fraction(C_ij) - exact) / denom)
+
+
+def _fixed_point_lines(X: np.ndarray, axis: int):
+    """Each line of X (rows for axis=1, columns for axis=0) as exact integers
+    N * 2^base: returns (sign, significand M < 2^53, shift >= 0, base) with
+    X = sign * M * 2^(shift + base) elementwise and base shared per line."""
+    X = np.asarray(X, dtype=np.float64)
+    f, e = np.frexp(np.abs(X))                    # |X| = f 2^e, f in [0.5, 1)
+    M = np.ldexp(f, 53).astype(np.int64)          # exact 53-bit significands
+    E = (e - 53).astype(np.int64)
+    E = np.where(M == 0, np.iinfo(np.int64).max, E)
+    base = np.min(E, axis=axis, keepdims=True)
+    base = np.where(base == np.iinfo(np.int64).max, 0, base)
+    shift = np.where(M == 0, 0, E - base)
+    sign = np.where(X < 0, -1, 1).astype(np.int64)
+    return sign, M, shift, np.squeeze(base, axis=axis)
+
+
+def _digits(M: np.ndarray, shift: np.ndarray, q: int) -> np.ndarray:
+    """Bits [18 q, 18 q + 18) of M * 2^shift (M < 2^53, shift >= 0)."""
+    lo = 18 * q - shift
+    Mu = M.astype(np.uint64)
+    right = (Mu >> np.clip(lo, 0, 63).astype(np.uint64)) & np.uint64(0x3FFFF)
+    left = (Mu << np.clip(-lo, 0, 63).astype(np.uint64)) & np.uint64(0x3FFFF)
+    out = np.where(lo >= 0, np.where(lo >= 53, 0, right), np.where(lo <= -18, 0, left))
+    return out.astype(np.int64)
+
+
+def exact_block(A: np.ndarray, B: np.ndarray, rows, cols):
+    """Exact (A B)_ij and sum_k |A_ik||B_kj| for i in rows, j in cols, as
+    Fraction object arrays.
+
+    Each row of A (column of B) is written as integers times a common power
+    of two; the integers are split into 18-bit digits whose products summed
+    over k stay below 2^36 k < 2^53 (k < 2^17), so every digit matmul is
+    exact in FP64 BLAS; the digit products are recombined in Python ints.
+    """
+    A = np.asarray(A, dtype=np.float64)[np.asarray(rows), :]
+    B = np.asarray(B, dtype=np.float64)[:, np.asarray(cols)]
+    k = A.shape[1]
+    if k >= (1 << 17):
+        raise ValueError("k too large for exact digit products")
+    sa, Ma, sha, ba = _fixed_point_lines(A, axis=1)
+    sb, Mb, shb, bb = _fixed_point_lines(B, axis=0)
+    na = int((53 + int(sha.max(initial=0)) + 17) // 18)
+    nb = int((53 + int(shb.max(initial=0)) + 17) // 18)
+    da = [_digits(Ma, sha, q) for q in range(na)]
+    db = [_digits(Mb, shb, q) for q in range(nb)]
+    prod = np.zeros((A.shape[0], B.shape[1]), dtype=object)
+    absum = np.zeros((A.shape[0], B.shape[1]), dtype=object)
+    for p in range(na):
+        for q in range(nb):
+            w = 1 << (18 * (p + q))
+            s_ = np.rint((sa * da[p]).astype(np.float64) @ (sb * db[q]).astype(np.float64))
+            u_ = np.rint(da[p].astype(np.float64) @ db[q].astype(np.float64))
+            prod = prod + s_.astype(np.int64).astype(object) * w
+            absum = absum + u_.astype(np.int64).astype(object) * w
+    out_p = np.empty(prod.shape, dtype=object)
+    out_a = np.empty(prod.shape, dtype=object)
+    two = Fraction(2)
+    for i in range(prod.shape[0]):
+        for j in range(prod.shape[1]):
+            scale = two ** (int(ba[i]) + int(bb[j]))
+            out_p[i, j] = Fraction(int(prod[i, j])) * scale
+            out_a[i, j] = Fraction(int(absum[i, j])) * scale
+    return out_p, out_a
+
+
+def normalized_errors_block(C_block: np.ndarray, A: np.ndarray, B: np.ndarray, rows, cols) -> np.ndarray:
+    """|C_ij - (AB)_ij| / sum_k |A_ik||B_kj| for a block, exactly (Sec. VII-A)."""
+    exact, denom = exact_block(A, B, rows, cols)
+    out = np.zeros(exact.shape, dtype=np.float64)
+    for i in range(exact.shape[0]):
+        for j in range(exact.shape[1]):
+            if denom[i, j] != 0:
+                out[i, j] = float(abs(Fraction(float(C_block[i, j])) - exact[i, j]) / denom[i, j])
+    return out

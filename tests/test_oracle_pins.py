@@ -466,3 +466,39 @@ def test_int8_wraps_like_int32():
     exact = 128 * 128 * 140000
     assert exact >= 2 ** 31
     assert int(o.igemm_s8(A, B)[0, 0]) == exact - 2 ** 32
+
+
+# ---------------------------------------------------------------- exact block products
+
+@pytest.mark.parametrize("seed", range(4))
+def test_exact_block_matches_fraction_sums(seed):
+    """The digit-split exact block product equals plain Fraction sums,
+    including zeros, subnormals and large exponent spreads."""
+    rng = np.random.default_rng(40 + seed)
+    m, n, k = 5, 4, 37
+    A = (rng.random((m, k)) - 0.5) * np.exp2(rng.integers(-60, 60, size=(m, k)))
+    B = (rng.random((k, n)) - 0.5) * np.exp2(rng.integers(-60, 60, size=(k, n)))
+    A[rng.random((m, k)) < 0.2] = 0.0
+    A[0, 0] = 5e-324
+    B[1, 1] = -2.5e-310
+    if seed == 1:
+        A[2, :] = 0.0
+    rows, cols = [0, 2, 4], [1, 3]
+    P, S = o.exact_block(A, B, rows, cols)
+    for a, i in enumerate(rows):
+        for b, j in enumerate(cols):
+            assert P[a, b] == o.exact_product_entry(A, B, i, j)
+            want = sum((abs(Fraction(float(A[i, q]))) * abs(Fraction(float(B[q, j]))) for q in range(k)),
+                       Fraction(0))
+            assert S[a, b] == want
+
+
+def test_normalized_errors_block_matches_single_entry():
+    rng = np.random.default_rng(9)
+    A = rng.standard_normal((3, 50))
+    B = rng.standard_normal((50, 3))
+    C = A @ B
+    got = o.normalized_errors_block(C, A, B, range(3), range(3))
+    for i in range(3):
+        for j in range(3):
+            assert got[i, j] == o.normalized_error(C[i, j], A, B, i, j)
