@@ -253,10 +253,13 @@ __global__ __launch_bounds__(256) void k_encode_s8(
 
 // ------------------------------------------------------------ Sec. VI-D
 // Block tile index -> (modulus, tile row, tile column). Consecutive block
-// ids go to the 8 XCDs round-robin; remap so that each XCD walks a
-// contiguous range of logical tiles, and order tiles in groups of kGroupM
-// tile rows so that the blocks an XCD runs together share A and B panels
-// in its L2.
+// ids go to the 8 XCDs round-robin. When the tile count T of one modulus is
+// a multiple of 8, XCD x takes tiles [x T/8, (x+1) T/8) of every modulus in
+// turn: every XCD then carries the same mix of moduli, the blocks an XCD
+// runs together share the A and B panels of one modulus in its L2, and all
+// XCDs stream the same B panels at about the same time. Otherwise each XCD
+// takes a contiguous range of the flattened (modulus, tile) order. Tiles
+// are ordered in groups of kGroupM tile rows.
 #ifndef OZFP4_GROUP_M
 #define OZFP4_GROUP_M 4
 #endif
@@ -264,11 +267,18 @@ constexpr int kGroupM = OZFP4_GROUP_M;
 __device__ __forceinline__ void tile_coords(int64_t bid, int64_t nblocks, int64_t tiles_m,
                                             int64_t tiles_n, int* l, int64_t* tm, int64_t* tn) {
   const int64_t xcd = bid & 7, local = bid >> 3;
-  const int64_t base = nblocks >> 3, rem = nblocks & 7;
-  const int64_t logical = xcd * base + min(xcd, rem) + local;
   const int64_t T = tiles_m * tiles_n;
-  *l = (int)(logical / T);
-  const int64_t t = logical - (int64_t)(*l) * T;
+  int64_t t;
+  if ((T & 7) == 0) {
+    const int64_t per = T >> 3;
+    *l = (int)(local / per);
+    t = xcd * per + (local - (int64_t)(*l) * per);
+  } else {
+    const int64_t base = nblocks >> 3, rem = nblocks & 7;
+    const int64_t logical = xcd * base + min(xcd, rem) + local;
+    *l = (int)(logical / T);
+    t = logical - (int64_t)(*l) * T;
+  }
   const int64_t group = t / (kGroupM * tiles_n);
   const int64_t first = group * kGroupM;
   const int64_t gm = min(tiles_m - first, (int64_t)kGroupM);
@@ -346,15 +356,13 @@ constexpr int kDmaPerWave = kStageFrags / kWaves;   // 6
 __device__ __forceinline__ constexpr int fragA(int p, int rb, int kbl) { return ((p * 8 + rb) * 2 + kbl) * kFragBytes; }
 __device__ __forceinline__ constexpr int fragB(int p, int cb, int kbl) { return (32 + (p * 4 + cb) * 2 + kbl) * kFragBytes; }
 
-__global__ __launch_bounds__(512, 1) void k_gemm_res(
-    const uint8_t* __restrict__ PA, const uint8_t* __restrict__ PB, uint8_t* __restrict__ R,
-    int64_t plane_a, int64_t plane_b, int64_t kblocks, int64_t tiles_m, int64_t tiles_n,
-    int64_t nblocks, int64_t ldr, int64_t rplane, const ModConst* __restrict__ mc) {
-  __shared__ __attribute__((aligned(1024))) uint8_t lds[kRing * kStageBytes];
-
-  int l;
-  int64_t tm, tn;
-  tile_coords(blockIdx.x, nblocks, tiles_m, tiles_n, &l, &tm, &tn);
+// One block tile of modulus l. kSkipA1B1: m = 169 = 13^2, where 169 a1 b1 is
+// 0 mod m (Sec. V-A), so the a1 b1 products are not issued (acc2 stays 0).
+template <bool kSkipA1B1>
+__device__ __forceinline__ void gemm_res_tile(
+    uint8_t* lds, int l, int64_t tm, int64_t tn, const uint8_t* __restrict__ PA,
+    const uint8_t* __restrict__ PB, uint8_t* __restrict__ R, int64_t plane_a, int64_t plane_b,
+    int64_t kblocks, int64_t ldr, int64_t rplane, const ModConst* __restrict__ mc) {
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int wm = wave >> 1, wn = wave & 1;
@@ -427,10 +435,12 @@ __global__ __launch_bounds__(512, 1) void k_gemm_res(
       for (int j = 0; j < 2; ++j) acc[1][i][j] = mfma_fp4(a[1][i], b[0][j], acc[1][i][j]);
   };
   auto mfma_tail = [&]() {
+    if constexpr (!kSkipA1B1) {
 #pragma unroll
-    for (int i = 0; i < 2; ++i)
+      for (int i = 0; i < 2; ++i)
 #pragma unroll
-      for (int j = 0; j < 2; ++j) acc[2][i][j] = mfma_fp4(a[1][i], b[1][j], acc[2][i][j]);
+        for (int j = 0; j < 2; ++j) acc[2][i][j] = mfma_fp4(a[1][i], b[1][j], acc[2][i][j]);
+    }
   };
   auto stage_body = [&](int s) {   // everything of stage s before the handover
     const uint8_t* sb = lds + (s % kRing) * kStageBytes;
@@ -493,6 +503,20 @@ __global__ __launch_bounds__(512, 1) void k_gemm_res(
         *reinterpret_cast<uint32_t*>(Rl + col * ldr + row) = word;
       }
     }
+}
+
+__global__ __launch_bounds__(512, 1) void k_gemm_res(
+    const uint8_t* __restrict__ PA, const uint8_t* __restrict__ PB, uint8_t* __restrict__ R,
+    int64_t plane_a, int64_t plane_b, int64_t kblocks, int64_t tiles_m, int64_t tiles_n,
+    int64_t nblocks, int64_t ldr, int64_t rplane, const ModConst* __restrict__ mc) {
+  __shared__ __attribute__((aligned(1024))) uint8_t lds[kRing * kStageBytes];
+  int l;
+  int64_t tm, tn;
+  tile_coords(blockIdx.x, nblocks, tiles_m, tiles_n, &l, &tm, &tn);
+  if (mc->m[l] == 169)
+    gemm_res_tile<true>(lds, l, tm, tn, PA, PB, R, plane_a, plane_b, kblocks, ldr, rplane, mc);
+  else
+    gemm_res_tile<false>(lds, l, tm, tn, PA, PB, R, plane_a, plane_b, kblocks, ldr, rplane, mc);
 }
 
 // INT8 variant: three planes per operand, five accumulators G_g (g = i + j),
