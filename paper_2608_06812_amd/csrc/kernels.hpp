@@ -133,11 +133,21 @@ __global__ void k_shifts(const uint64_t* __restrict__ amax, int64_t lines, int c
 // (line % 32, k half) converts its 32 values once, then for each modulus
 // reduces them, looks the codes up in an LDS table and stores 16 bytes to
 // each of the two planes of that modulus.
-//   x = |round_half_even(X * 2^s)| < 2^53 is exact in FP64; for each m the
-//   estimate q = floor(x * fl(1/m)) is within one of floor(x / m), so
-//   r = x - q m (exact FMA) lies in [-m, 2m) and indexes a table that
-//   already folds the correction and the sign of X.
+//   x = round_half_even(X * 2^s), |x| <= 2^53, is exact in FP64 and kept as
+//   2x. For each m, q = floor(2x * fl(1/m) / 2) is within one of
+//   floor(x / m), so 2r = 2x - q 2m (exact FMA) has r in [-m, 2m), and r
+//   indexes a table over [-m, 2m) that maps every estimate to the codes of
+//   the canonical split of its class. Adding 2^52 plus the table's byte
+//   offset to 2r gives a double in [2^52, 2^53) whose low 32 bits are the
+//   LDS byte address of the entry.
 constexpr int kEncWaves = 4;
+typedef __attribute__((address_space(3))) const uint16_t lds_u16;
+
+__device__ __forceinline__ uint32_t lut_lookup(double y) {
+  const uint32_t addr = (uint32_t)__double_as_longlong(y);
+  return *reinterpret_cast<lds_u16*>((size_t)addr);
+}
+
 __global__ __launch_bounds__(256) void k_encode_dgemm(
     const double* __restrict__ X, int64_t rs, int64_t ks, int64_t lines, int64_t k,
     const uint64_t* __restrict__ amax, int cap, uint8_t* __restrict__ planes,
@@ -146,6 +156,8 @@ __global__ __launch_bounds__(256) void k_encode_dgemm(
   extern __shared__ uint16_t s_lut[];
   for (int i = threadIdx.x; i < lut_entries; i += 256) s_lut[i] = lut[i];
   __syncthreads();
+  const uint32_t lds_base =
+      (uint32_t)(size_t)(__attribute__((address_space(3))) uint16_t*)s_lut;
   const int lane = threadIdx.x & 63;
   const int wave = threadIdx.x >> 6;
   for (int64_t f = (int64_t)blockIdx.x * kEncWaves + wave; f < nfrag;
@@ -155,49 +167,50 @@ __global__ __launch_bounds__(256) void k_encode_dgemm(
     const int64_t kbase = kb * kFragK + (lane >> 5) * 32;
     const bool live = line < lines;
     const int s = live ? line_shift(amax[line], cap) : 0;
-    double x[32];
-    uint32_t neg = 0;
-    const double* src = X + line * rs;
+    double x2[32];
+    const double* src = X + (live ? line : 0) * rs + kbase * ks;
+    if (live && kbase + 32 <= k) {
+#pragma unroll
+      for (int e = 0; e < 32; ++e) {
+        x2[e] = *src;
+        src += ks;
+      }
+    } else {
+#pragma unroll
+      for (int e = 0; e < 32; ++e) {
+        x2[e] = (live && kbase + e < k) ? *src : 0.0;
+        src += ks;
+      }
+    }
 #pragma unroll
     for (int e = 0; e < 32; ++e) {
-      const int64_t kk = kbase + e;
-      double v = (live && kk < k) ? src[kk * ks] : 0.0;
-      double t = __builtin_rint(__builtin_ldexp(v, s));
-      neg |= (t < 0.0 ? 1u : 0u) << e;
-      double a = __builtin_fabs(t);
-      // finite inputs give a <= 2^53; NaN/Inf (reported by the scale stage)
-      // must not drive the table index out of range
-      x[e] = (a <= 9007199254740992.0) ? a : 0.0;
+      const double t = __builtin_rint(__builtin_ldexp(x2[e], s));
+      // finite inputs give |t| <= 2^53; NaN/Inf (reported by the scale
+      // stage) must not drive the table address out of range
+      x2[e] = (__builtin_fabs(t) <= 0x1p53) ? 2.0 * t : 0.0;
     }
     uint8_t* out = planes + f * kFragBytes + lane * 16;
     for (int l = 0; l < L; ++l) {
       const int m = mc->m[l];
-      const double inv = mc->inv[l];
-      const double md = mc->md[l];
-      const uint16_t* T = s_lut + mc->lut_off[l] + m;
-      const int m3 = 3 * m;
+      const double inv = 0.5 * mc->inv[l];
+      const double m2 = 2.0 * mc->md[l];
+      const double base = 0x1p52 + (double)(lds_base + 2u * (uint32_t)(mc->lut_off[l] + m));
       uint32_t w0[4], w1[4];
 #pragma unroll
       for (int g = 0; g < 4; ++g) {
-        uint32_t t4[2];
+        uint32_t p[4];
 #pragma unroll
-        for (int h = 0; h < 2; ++h) {
-          uint32_t acc = 0;
-#pragma unroll
-          for (int e4 = 0; e4 < 4; ++e4) {
-            const int e = g * 8 + h * 4 + e4;
-            double q = __builtin_floor(x[e] * inv);
-            int ri = (int)__builtin_fma(-q, md, x[e]);
-            int idx = ri + (((neg >> e) & 1u) ? m3 : 0);
-            uint32_t E = T[idx];
-            acc |= E << (4 * (e4 & 1) + 16 * (e4 >> 1));
-          }
-          t4[h] = acc;
+        for (int h = 0; h < 4; ++h) {
+          const int e = g * 8 + h * 2;
+          const double q0 = __builtin_floor(x2[e] * inv);
+          const double q1 = __builtin_floor(x2[e + 1] * inv);
+          const uint32_t E0 = lut_lookup(__builtin_fma(-q0, m2, x2[e]) + base);
+          const uint32_t E1 = lut_lookup(__builtin_fma(-q1, m2, x2[e + 1]) + base);
+          p[h] = E0 | (E1 << 4);  // byte 0: plane-0 byte, byte 1: plane-1 byte
         }
-        w0[g] = (t4[0] & 0xffu) | ((t4[0] >> 8) & 0xff00u) | ((t4[1] & 0xffu) << 16) |
-                ((t4[1] << 8) & 0xff000000u);
-        w1[g] = ((t4[0] >> 8) & 0xffu) | ((t4[0] >> 16) & 0xff00u) | ((t4[1] & 0xff00u) << 8) |
-                (t4[1] & 0xff000000u);
+        const uint32_t u = p[0] | (p[1] << 16), v = p[2] | (p[3] << 16);
+        w0[g] = __builtin_amdgcn_perm(v, u, 0x06040200u);
+        w1[g] = __builtin_amdgcn_perm(v, u, 0x07050301u);
       }
       v4i p0 = {(int)w0[0], (int)w0[1], (int)w0[2], (int)w0[3]};
       v4i p1 = {(int)w1[0], (int)w1[1], (int)w1[2], (int)w1[3]};
@@ -687,22 +700,28 @@ __device__ __forceinline__ double round_scaled(uint64_t w0, uint64_t w1, uint64_
   return neg ? -r : r;
 }
 
-__device__ __forceinline__ double crt_finish(const double sig[4], double Qe,
-                                             const CrtConst* __restrict__ cc, int e2) {
-  const double q = __builtin_rint(Qe);        // nearest integer to S / P
-  int64_t v[4];
-#pragma unroll
-  for (int c = 0; c < 4; ++c) v[c] = (int64_t)__builtin_fma(-q, cc->Pc[c], sig[c]);  // exact
-  const int64_t MASK = (1ll << 40) - 1;
-  const int64_t d0 = v[0] & MASK;
-  int64_t t = v[1] + (v[0] >> 40);
+// Exact path. x' = S - q P is assembled from the 42-bit chunk differences
+// v_c = sig_c - q P_c (exact integers below 2^53 in magnitude) as a 192-bit
+// two's-complement integer. It is mapped into the symmetric range
+// (-P/2, P/2] and RN(x 2^e2) is taken, including subnormal results and
+// overflow to infinity. s3 = 0 when three chunks are in use (then P_3 = 0).
+__device__ __forceinline__ double crt_exact(double s0, double s1, double s2, double s3, double q,
+                                            const CrtConst* __restrict__ cc, int e2) {
+  const int64_t v0 = (int64_t)__builtin_fma(-q, cc->Pc[0], s0);
+  const int64_t v1 = (int64_t)__builtin_fma(-q, cc->Pc[1], s1);
+  const int64_t v2 = (int64_t)__builtin_fma(-q, cc->Pc[2], s2);
+  const int64_t v3 = (int64_t)__builtin_fma(-q, cc->Pc[3], s3);
+  constexpr int64_t MASK = (1ll << kCrtChunkBits) - 1;
+  const int64_t d0 = v0 & MASK;
+  int64_t t = v1 + (v0 >> 42);
   const int64_t d1 = t & MASK;
-  t = v[2] + (t >> 40);
+  t = v2 + (t >> 42);
   const int64_t d2 = t & MASK;
-  const int64_t t3 = v[3] + (t >> 40);
-  uint64_t w0 = (uint64_t)d0 | ((uint64_t)d1 << 40);
-  uint64_t w1 = ((uint64_t)d1 >> 24) | ((uint64_t)d2 << 16) | ((uint64_t)t3 << 56);
-  uint64_t w2 = (uint64_t)(t3 >> 8);
+  const int64_t t3 = v3 + (t >> 42);
+  // x' = d0 + d1 2^42 + d2 2^84 + t3 2^126
+  uint64_t w0 = (uint64_t)d0 | ((uint64_t)d1 << 42);
+  uint64_t w1 = ((uint64_t)d1 >> 22) | ((uint64_t)d2 << 20) | ((uint64_t)t3 << 62);
+  uint64_t w2 = (uint64_t)(t3 >> 2);
   bool neg = (int64_t)w2 < 0;
   if (neg) {  // two's-complement negation of the 192-bit value
     w0 = ~w0 + 1;
@@ -728,10 +747,54 @@ __device__ __forceinline__ double crt_finish(const double sig[4], double Qe,
   return round_scaled(w0, w1, w2, e2, neg);
 }
 
+// Fast path for three chunks, in FP64 only. Carry normalisation gives
+// x' = t 2^84 + d1 2^42 + d0 with 0 <= d0, d1 < 2^42, every step exact.
+//   |t| <= 2: (t 2^42 + d1) is exact, so one FMA rounds x' once.
+//   |t| >= 3: |x'| >= 2^85. y = d1 2^42 + d0 is rounded to odd at 53 bits
+//     (Fast2Sum gives the sign of the error), a grid of at most 2^31 that is
+//     at least 4 times finer than the grid of x' (>= 2^33); adding t 2^84
+//     and rounding to nearest then equals RN(x') (rounding to odd with two
+//     extra bits, Boldo and Melquiond).
+// RN(x' 2^e2) = RN(x') 2^e2 whenever the result is normal. The path gives up
+// (returns false) when |x'| may lie outside (-P/2, P/2], which the quotient
+// estimate leaves only when S / P is within about 2^-30 of a half-integer,
+// or when the result may be subnormal; crt_exact then decides.
+__device__ __forceinline__ bool crt_fast3(double s0, double s1, double s2, double q,
+                                          const CrtConst* __restrict__ cc, int e2, double* out) {
+  constexpr double kC = 0x1p42, kCi = 0x1p-42;
+  const double v0 = __builtin_fma(-q, cc->Pc[0], s0);
+  double v1 = __builtin_fma(-q, cc->Pc[1], s1);
+  const double v2 = __builtin_fma(-q, cc->Pc[2], s2);
+  const double c0 = __builtin_floor(v0 * kCi);
+  const double d0 = __builtin_fma(-c0, kC, v0);
+  v1 += c0;
+  const double c1 = __builtin_floor(v1 * kCi);
+  const double d1 = __builtin_fma(-c1, kC, v1);
+  const double t = v2 + c1;
+  const double r_small = __builtin_fma(__builtin_fma(t, kC, d1), kC, d0);
+  const double D1 = d1 * kC;
+  const double sy = D1 + d0;
+  const double ey = d0 - (sy - D1);
+  uint64_t bits = (uint64_t)__double_as_longlong(sy);
+  bits = ey > 0.0 ? (bits | 1ull) : ((ey < 0.0 && !(bits & 1ull)) ? bits - 1ull : bits);
+  const double r_large = __builtin_fma(t, 0x1p84, __longlong_as_double((long long)bits));
+  const double r = __builtin_fabs(t) <= 2.0 ? r_small : r_large;
+  if (!(__builtin_fabs(r) < cc->sym_limit)) return false;
+  if (r != 0.0) {
+    int fe;
+    (void)__builtin_frexp(r, &fe);
+    if (fe + e2 <= -1020) return false;
+  }
+  *out = __builtin_ldexp(r, e2);
+  return true;
+}
+
 // One thread per 4 consecutive rows of a column: reads one 32-bit word per
-// modulus, accumulates S = sum r_l w_l as four exact FP64 chunk sums
-// (r_l w_l,c < 2^48, at most 20 terms < 2^53) and the quotient estimate
-// sum r_l fl(w_l / P), then reconstructs and rounds each element.
+// modulus and accumulates the exact chunk sums sig_c = sum_l r_l w_l,c
+// (Sec. V-B). The quotient q = rint(S / P) comes from the chunk sums,
+// then every element is reconstructed and rounded once. NC = number of
+// 42-bit chunks (3 for up to 19 moduli, 4 for 20).
+template <int NC>
 __global__ __launch_bounds__(256) void k_crt(
     const uint8_t* __restrict__ R, int64_t ldr, int64_t rplane, int64_t m, int64_t n,
     const uint64_t* __restrict__ amaxA, const uint64_t* __restrict__ amaxB, int cA, int cB,
@@ -742,26 +805,29 @@ __global__ __launch_bounds__(256) void k_crt(
   const int64_t j = t / rows4;
   const int64_t i0 = (t - j * rows4) * 4;
   const int L = cc->L;
-  double sig[4][4], Q[4];
+  double sig[4][NC];
 #pragma unroll
-  for (int e = 0; e < 4; ++e) {
-    Q[e] = 0.0;
+  for (int e = 0; e < 4; ++e)
 #pragma unroll
-    for (int c = 0; c < 4; ++c) sig[e][c] = 0.0;
-  }
+    for (int c = 0; c < NC; ++c) sig[e][c] = 0.0;
   const uint8_t* src = R + j * ldr + i0;
-  for (int l = 0; l < L; ++l) {
-    const uint32_t w = *reinterpret_cast<const uint32_t*>(src + (int64_t)l * rplane);
-    const double W0 = cc->W[l][0], W1 = cc->W[l][1], W2 = cc->W[l][2], W3 = cc->W[l][3];
-    const double F = cc->F[l];
+  // all loads first, so that the L reads of a thread are in flight together
+  uint32_t words[kMaxModuli];
+#pragma unroll
+  for (int l = 0; l < kMaxModuli; ++l)
+    if (l < L) words[l] = *reinterpret_cast<const uint32_t*>(src + (int64_t)l * rplane);
+#pragma unroll
+  for (int l = 0; l < kMaxModuli; ++l) {
+    if (l >= L) break;
+    const uint32_t w = words[l];
+    double W[NC];
+#pragma unroll
+    for (int c = 0; c < NC; ++c) W[c] = cc->W[l][c];
 #pragma unroll
     for (int e = 0; e < 4; ++e) {
       const double r = (double)((w >> (8 * e)) & 0xffu);
-      sig[e][0] = __builtin_fma(r, W0, sig[e][0]);
-      sig[e][1] = __builtin_fma(r, W1, sig[e][1]);
-      sig[e][2] = __builtin_fma(r, W2, sig[e][2]);
-      sig[e][3] = __builtin_fma(r, W3, sig[e][3]);
-      Q[e] = __builtin_fma(r, F, Q[e]);
+#pragma unroll
+      for (int c = 0; c < NC; ++c) sig[e][c] = __builtin_fma(r, W[c], sig[e][c]);
     }
   }
   const int tj = line_shift(amaxB[j], cB);
@@ -769,8 +835,17 @@ __global__ __launch_bounds__(256) void k_crt(
   for (int e = 0; e < 4; ++e) {
     const int64_t i = i0 + e;
     if (i < m) {
-      const int si = line_shift(amaxA[i], cA);
-      C[i + j * ldc] = crt_finish(sig[e], Q[e], cc, -(si + tj));
+      const int e2 = -(line_shift(amaxA[i], cA) + tj);
+      double Qe = sig[e][NC - 1] * cc->Qc[NC - 1];
+#pragma unroll
+      for (int c = NC - 2; c >= 0; --c) Qe = __builtin_fma(sig[e][c], cc->Qc[c], Qe);
+      const double q = __builtin_rint(Qe);
+      double out;
+      bool done = false;
+      if constexpr (NC == 3) done = crt_fast3(sig[e][0], sig[e][1], sig[e][2], q, cc, e2, &out);
+      if (!done)
+        out = crt_exact(sig[e][0], sig[e][1], sig[e][2], NC == 4 ? sig[e][NC - 1] : 0.0, q, cc, e2);
+      C[i + j * ldc] = out;
     }
   }
 }

@@ -185,7 +185,7 @@ int run_dgemm(const DgemmPlan& p, DeviceState* d, const double* A, int64_t lda, 
   if (last < 1) return OZFP4_OK;
 
   // stage 1, 2: fused conversion + residues + limbs + E2M1 packing
-  const int lut_entries = T->mod.lut_off[L - 1] + 6 * T->mod.m[L - 1];
+  const int lut_entries = T->mod.lut_off[L - 1] + 3 * T->mod.m[L - 1];
   const size_t lut_bytes = sizeof(uint16_t) * (size_t)lut_entries;
   const int64_t nfa = (p.m_pad / kFragLines) * p.kblocks;
   const int64_t nfb = (p.n_pad / kFragLines) * p.kblocks;
@@ -213,8 +213,14 @@ int run_dgemm(const DgemmPlan& p, DeviceState* d, const double* A, int64_t lda, 
 
   // stage 4: CRT reconstruction and inverse scaling
   const int64_t nthreads = ((p.m + 3) / 4) * p.n;
-  hipLaunchKernelGGL(k_crt, dim3(blocks_for(nthreads, 256)), dim3(256), 0, g_stream, R, p.m_pad,
-                     p.m_pad * p.n_pad, p.m, p.n, amax_a, amax_b, p.cA, p.cB, d->d_crt + L, C, ldc);
+  if (crt_chunks(L) == 3)
+    hipLaunchKernelGGL(k_crt<3>, dim3(blocks_for(nthreads, 256)), dim3(256), 0, g_stream, R,
+                       p.m_pad, p.m_pad * p.n_pad, p.m, p.n, amax_a, amax_b, p.cA, p.cB,
+                       d->d_crt + L, C, ldc);
+  else
+    hipLaunchKernelGGL(k_crt<4>, dim3(blocks_for(nthreads, 256)), dim3(256), 0, g_stream, R,
+                       p.m_pad, p.m_pad * p.n_pad, p.m, p.n, amax_a, amax_b, p.cA, p.cB,
+                       d->d_crt + L, C, ldc);
   HIP_TRY(hipGetLastError());
   record(d, 5);
   return OZFP4_OK;

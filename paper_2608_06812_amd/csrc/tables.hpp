@@ -1,7 +1,7 @@
 // Host-side constants of the method, derived at library initialisation from
 // the definitions in the paper (nothing is typed in):
 //   * the two-limb moduli and their greedy pairwise-coprime order (Sec. V-A);
-//   * P, the CRT weights w_l = M_l (M_l^{-1} mod m_l) and their 40-bit
+//   * P, the CRT weights w_l = M_l (M_l^{-1} mod m_l) and their 42-bit
 //     chunks (Sec. V-B);
 //   * the capacity split (c_A, c_B) for an inner dimension k (Sec. IV-B with
 //     Eq. (crt));
@@ -13,6 +13,7 @@
 #include <stdint.h>
 
 #include <algorithm>
+#include <cmath>
 #include <cstring>
 #include <vector>
 
@@ -153,12 +154,21 @@ struct ModConst {
   double md[kMaxModuli];     // m as double
 };
 
+// Chunk width of the exact FP64 CRT sums. With R = sum (m_l - 1) <= 1799
+// for up to 20 moduli, R (2^42 - 1) < 2^53, so every chunk sum
+// sum r_l w_l,c, every q P_c with q <= R, and every carry-normalised chunk
+// is an integer below 2^53 and exact in FP64. Three chunks (126 bits) cover
+// P for up to 19 moduli (P < 2^124), four for 20.
+constexpr int kCrtChunkBits = 42;
+inline int crt_chunks(int L) { return L <= 19 ? 3 : 4; }
+
 struct CrtConst {
   int L;
-  int pad_;
-  double W[kMaxModuli][4];   // 40-bit chunks of w_l
-  double F[kMaxModuli];      // fl(u_l / m_l) = fl(w_l / P)
-  double Pc[4];              // 40-bit chunks of P
+  int nc;                    // chunks in use, crt_chunks(L)
+  double W[kMaxModuli][4];   // 42-bit chunks of w_l
+  double Pc[4];              // 42-bit chunks of P
+  double Qc[4];              // ~ 2^(42 c) / P, weights of the quotient estimate
+  double sym_limit;          // ~ (P / 2)(1 - 2^-30): a rounded |x| below it is inside (-P/2, P/2]
   uint64_t P[3];             // P as a 192-bit integer
 };
 
@@ -172,9 +182,9 @@ struct HostTables {
   bool ok = false;
 };
 
-// Encoder LUT of modulus m: 6m entries, index (ri + m) + neg * 3m for a
-// remainder estimate ri in [-m, 2m) of |x| and the sign of x; entry =
-// code(c0) | code(c1) << 8 for the canonical split of the class of x.
+// Encoder LUT of modulus m: 3m entries, index r + m for a remainder
+// estimate r in [-m, 2m) of a signed integer x; entry = code(c0) |
+// code(c1) << 8 for the canonical split of the class of x mod m.
 inline bool build_tables(HostTables& T) {
   T.moduli = greedy_moduli();
   if ((int)T.moduli.size() != kMaxModuli) return false;
@@ -187,17 +197,15 @@ inline bool build_tables(HostTables& T) {
     T.mod.lut_off[l] = off;
     T.mod.inv[l] = 1.0 / (double)m;
     T.mod.md[l] = (double)m;
-    for (int neg = 0; neg < 2; ++neg)
-      for (int ri = -m; ri < 2 * m; ++ri) {
-        int cls = ((ri % m) + m) % m;
-        if (neg) cls = (m - cls) % m;
-        int c0, c1;
-        if (!two_limb_split(cls, m, &c0, &c1)) return false;
-        int k0 = e2m1_code_of_limb(c0), k1 = e2m1_code_of_limb(c1);
-        if (k0 < 0 || k1 < 0) return false;
-        T.lut.push_back((uint16_t)(k0 | (k1 << 8)));
-      }
-    off += 6 * m;
+    for (int ri = -m; ri < 2 * m; ++ri) {
+      int cls = ((ri % m) + m) % m;
+      int c0, c1;
+      if (!two_limb_split(cls, m, &c0, &c1)) return false;
+      int k0 = e2m1_code_of_limb(c0), k1 = e2m1_code_of_limb(c1);
+      if (k0 < 0 || k1 < 0) return false;
+      T.lut.push_back((uint16_t)(k0 | (k1 << 8)));
+    }
+    off += 3 * m;
   }
   // int8: three greedy limbs (X_3 = 732 >= 128)
   for (int v = -128; v < 128; ++v) {
@@ -220,7 +228,16 @@ inline bool build_tables(HostTables& T) {
     for (int l = 0; l < L; ++l) T.P[L].mul_small((uint32_t)T.moduli[l]);
     CrtConst& c = T.crt[L];
     c.L = L;
-    for (int q = 0; q < 4; ++q) c.Pc[q] = (double)T.P[L].bits(40 * q, 40);
+    c.nc = crt_chunks(L);
+    const int B = kCrtChunkBits;
+    if (T.P[L].bitlen() > c.nc * B) return false;
+    double Pd = 0.0;
+    for (int q = 0; q < 4; ++q) {
+      c.Pc[q] = (double)T.P[L].bits(B * q, B);
+      Pd += std::ldexp(c.Pc[q], B * q);
+    }
+    for (int q = 0; q < 4; ++q) c.Qc[q] = std::ldexp(1.0 / Pd, B * q);
+    c.sym_limit = 0.5 * Pd * (1.0 - std::ldexp(1.0, -30));
     for (int q = 0; q < 3; ++q) c.P[q] = T.P[L].bits(64 * q, 32) | (T.P[L].bits(64 * q + 32, 32) << 32);
     for (int l = 0; l < L; ++l) {
       int m = T.moduli[l];
@@ -234,8 +251,7 @@ inline bool build_tables(HostTables& T) {
       if (u < 0) return false;
       Big w = Mi;
       w.mul_small((uint32_t)u);           // w_l = M_l u_l < P
-      for (int q = 0; q < 4; ++q) c.W[l][q] = (double)w.bits(40 * q, 40);
-      c.F[l] = (double)u / (double)m;     // = w_l / P, correctly rounded
+      for (int q = 0; q < 4; ++q) c.W[l][q] = (double)w.bits(B * q, B);
     }
   }
   T.ok = true;
