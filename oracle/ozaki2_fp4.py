@@ -21,6 +21,8 @@ Readings where the paper is silent (the GPU library documents the same ones):
   * fewer than 19 moduli: the prefix of the greedy list (Sec. V-A); a 20th
     modulus is the next one the same greedy rule picks;
   * canonical two-limb split of a residue (see ``two_limb_split``);
+  * for the Karatsuba moduli, limbs whose sum is in S as well, all three
+    within +-8 (see ``sum_limb_split``);
   * residues r in [0, m); symmetric map x -> x - P when 2x > P (Sec. V-B);
   * one round-to-nearest-even of x * 2^-(s_i + t_j), subnormals and overflow
     included (Sec. IV-B, Sec. V-B).
@@ -40,6 +42,8 @@ __all__ = [
     "capacity_bits", "floor_log2", "shift_exponents", "to_integers",
     "to_integers_fraction", "residues", "two_limb_split", "two_limb_table",
     "e2m1_code", "e2m1_decode", "limb_planes", "exact_int_matmul",
+    "is_karatsuba_modulus", "karatsuba_moduli", "sum_limb_split", "sum_limb_table",
+    "limb_planes_karatsuba", "residue_products_karatsuba",
     "residue_products", "crt_reconstruct", "crt_reconstruct_paper",
     "round_scaled", "dgemm", "dgemm_definition", "int8_limbs", "igemm_s8",
     "igemm_s8_limbs", "fp32_exact_bound", "fp32_accumulate_emulated",
@@ -265,6 +269,49 @@ def two_limb_split(r: int, m: int) -> tuple[int, int]:
     raise ValueError(f"residue {r} has no two-limb split mod {m}")
 
 
+def is_karatsuba_modulus(m: int) -> bool:
+    """True when every class mod m has limbs c0, c1 in S with c0 + 13 c1 = r
+    (mod m) whose sum c0 + c1 is also in S, so that the cross term
+    a0 b1 + a1 b0 = (a0 + a1)(b0 + b1) - a0 b0 - a1 b1 takes one limb product
+    (Karatsuba, Sec. V-A)."""
+    S = doubled_set()
+    Sset = set(S)
+    return len({(c0 + 13 * c1) % m for c0 in S for c1 in S if c0 + c1 in Sset}) == m
+
+
+def karatsuba_moduli(moduli) -> list[int]:
+    """The moduli of the list that admit the Karatsuba product (Sec. V-A)."""
+    return [m for m in moduli if is_karatsuba_modulus(m)]
+
+
+def sum_limb_split(r: int, m: int) -> tuple[int, int]:
+    """Limbs (c0, c1) of r mod m for a Karatsuba modulus: c0, c1 and c0 + c1
+    all in S and at most 8 in magnitude (so each of the three limb products
+    a0 b0, a1 b1, (a0 + a1)(b0 + b1) keeps the FP32 bound of Lemma 3 with
+    |c| <= 8, one term each).
+
+    Reading (the paper only states that such limbs exist): the canonical split
+    when its sum qualifies; otherwise the qualifying split with the smallest
+    |c1|, then the smallest |c0| (unique for odd m).
+    """
+    S = doubled_set()
+    ok = {c for c in S if abs(c) <= 8}
+    c0, c1 = two_limb_split(r, m)
+    if c0 + c1 in ok:
+        return c0, c1
+    cands = [(abs(b), abs(a), a, b) for a in ok for b in ok
+             if (a + 13 * b - r) % m == 0 and a + b in ok]
+    if not cands:
+        raise ValueError(f"residue {r} has no sum-limb split mod {m}")
+    _, _, a, b = min(cands)
+    return a, b
+
+
+def sum_limb_table(m: int) -> list[tuple[int, int]]:
+    """The sum-limb split of every residue r in [0, m)."""
+    return [sum_limb_split(r, m) for r in range(m)]
+
+
 def two_limb_table(m: int) -> list[tuple[int, int]]:
     """The canonical split of every residue r in [0, m)."""
     return [two_limb_split(r, m) for r in range(m)]
@@ -293,6 +340,16 @@ def limb_planes(Xi: np.ndarray, m: int) -> tuple[np.ndarray, np.ndarray]:
     c1 = np.array([c for _, c in tab], dtype=np.int64)
     r = residues(Xi, m)
     return c0[r], c1[r]
+
+
+def limb_planes_karatsuba(Xi: np.ndarray, m: int) -> tuple[np.ndarray, np.ndarray, np.ndarray]:
+    """Limb planes (c0, c1, c0 + c1) of X~ mod m from the sum-limb split, for
+    a Karatsuba modulus (Sec. V-A)."""
+    tab = sum_limb_table(m)
+    c0 = np.array([c for c, _ in tab], dtype=np.int64)
+    c1 = np.array([c for _, c in tab], dtype=np.int64)
+    r = residues(Xi, m)
+    return c0[r], c1[r], c0[r] + c1[r]
 
 
 # ---------------------------------------------------------------------------
@@ -358,6 +415,19 @@ def residue_products(Ai: np.ndarray, Bi: np.ndarray, m: int) -> dict:
     return {"G0": G0, "G1": G1, "G2": G2, "r": r}
 
 
+def residue_products_karatsuba(Ai: np.ndarray, Bi: np.ndarray, m: int) -> dict:
+    """One Karatsuba modulus of the residue GEMM (Sec. V-A): three limb
+    products P0 = a0 b0, P2 = a1 b1, Ps = (a0 + a1)(b0 + b1); the cross term
+    is Ps - P0 - P2 and r = P0 + 13 (Ps - P0 - P2) + 169 P2 (mod m)."""
+    a0, a1, as_ = limb_planes_karatsuba(Ai, m)
+    b0, b1, bs = limb_planes_karatsuba(Bi, m)
+    P0 = _limb_matmul(a0, b0)
+    P2 = _limb_matmul(a1, b1)
+    Ps = _limb_matmul(as_, bs)
+    r = np.mod(P0 + 13 * (Ps - P0 - P2) + 169 * P2, m)
+    return {"P0": P0, "P2": P2, "Ps": Ps, "r": r}
+
+
 # ---------------------------------------------------------------------------
 # Sec. V-B: exact direct CRT reconstruction
 # ---------------------------------------------------------------------------
@@ -409,7 +479,7 @@ def round_scaled(x: int, shift: int) -> float:
 # ---------------------------------------------------------------------------
 
 def dgemm(A: np.ndarray, B: np.ndarray, n_moduli: int, rows=None, cols=None,
-          check_definition: bool = False) -> dict:
+          check_definition: bool = False, karatsuba: bool = True) -> dict:
     """C = A B by Ozaki scheme II on base-13 E2M1 limbs (Sec. IV-B, V).
 
     Optional `rows` / `cols` restrict the output to a sub-block (the scaling
@@ -420,7 +490,8 @@ def dgemm(A: np.ndarray, B: np.ndarray, n_moduli: int, rows=None, cols=None,
 
     With check_definition=True the reconstructed x is also compared with the
     exact integer product of the converted operands (Eq. (crt) guarantees
-    equality).
+    equality). With karatsuba=True the Karatsuba moduli take the three-product
+    route (residue_products_karatsuba); the residues are the same either way.
     """
     A = np.asarray(A, dtype=np.float64)
     B = np.asarray(B, dtype=np.float64)
@@ -437,7 +508,9 @@ def dgemm(A: np.ndarray, B: np.ndarray, n_moduli: int, rows=None, cols=None,
     Ai = to_integers(As, s, axis=1)
     Bi = to_integers(Bs, t, axis=0)
     assert np.all(np.abs(Ai) <= (1 << cA)) and np.all(np.abs(Bi) <= (1 << cB))
-    res = [residue_products(Ai, Bi, mod)["r"] for mod in moduli]
+    kset = set(karatsuba_moduli(moduli)) if karatsuba else set()
+    res = [(residue_products_karatsuba if mod in kset else residue_products)(Ai, Bi, mod)["r"]
+           for mod in moduli]
     x = crt_reconstruct(res, moduli)
     if check_definition:
         exact = exact_int_matmul(Ai, Bi)

@@ -130,3 +130,24 @@ def test_wrong_e2m1_code_table_is_caught(monkeypatch, bad_code):
         if int(2 * o.e2m1_decode(o.e2m1_code(c))) != c:
             bad = True
     assert bad
+
+
+def test_karatsuba_cross_term_without_p2_is_caught(monkeypatch):
+    orig = mod.residue_products_karatsuba
+
+    def bad(Ai, Bi, m):
+        out = orig(Ai, Bi, m)
+        out["r"] = np.mod(out["P0"] + 13 * (out["Ps"] - out["P0"]) + 169 * out["P2"], m)
+        return out
+    monkeypatch.setattr(mod, "residue_products_karatsuba", bad)
+    assert _tiny_mismatch()
+
+
+def test_karatsuba_wrong_sum_plane_is_caught(monkeypatch):
+    orig = mod.limb_planes_karatsuba
+
+    def bad(Xi, m):
+        c0, c1, _ = orig(Xi, m)
+        return c0, c1, c0 - c1
+    monkeypatch.setattr(mod, "limb_planes_karatsuba", bad)
+    assert _tiny_mismatch()

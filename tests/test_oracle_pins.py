@@ -171,9 +171,64 @@ def test_karatsuba_moduli(paper):
 
     got = [m for m in paper["moduli_L19"] if ok(m)]
     assert got == paper["karatsuba_moduli"]
+    assert o.karatsuba_moduli(paper["moduli_L19"]) == paper["karatsuba_moduli"]
     assert 4 * 19 - 1 - len(got) == paper["karatsuba_gemm_count"]
     assert 4 * 19 - 1 == paper["gemm_count_required"]
     assert 4 * 19 == paper["gemm_count_executed"]
+
+
+def test_sum_limb_split_valid_symmetric_and_bounded():
+    """Every residue of every Karatsuba modulus among the 20: the limbs and
+    their sum are in S, within +-8, congruent to r; the split of -r is the
+    negated split of r; where the canonical split already qualifies it is
+    kept. With |c| <= 8 and one term per accumulator the FP32 bound of
+    Lemma 3 holds up to the library's largest k."""
+    S = set(o.doubled_set())
+    kmods = o.karatsuba_moduli(o.select_moduli(20))
+    assert kmods == [83, 73, 71, 67, 61, 59, 53, 47]
+    changed = 0
+    for m in kmods:
+        for r in range(m):
+            c0, c1 = o.sum_limb_split(r, m)
+            assert (c0 + 13 * c1 - r) % m == 0
+            for c in (c0, c1, c0 + c1):
+                assert c in S and abs(c) <= 8
+            n0, n1 = o.sum_limb_split((-r) % m, m)
+            assert (n0, n1) == (-c0, -c1)
+            k0, k1 = o.two_limb_split(r, m)
+            if k0 + k1 in S and abs(k0 + k1) <= 8:
+                assert (c0, c1) == (k0, k1)
+            else:
+                changed += 1
+    assert changed > 0
+    assert o.fp32_exact_bound(o.MAX_K_FP32, max_limb=8, terms=1)
+    assert not o.fp32_exact_bound(o.MAX_K_FP32, max_limb=12, terms=1)
+
+
+def test_karatsuba_residues_equal_exact_product():
+    """r from the three Karatsuba products equals (A~ B~) mod m computed from
+    the exact integer product, for every Karatsuba modulus."""
+    rng = np.random.default_rng(11)
+    Ai = rng.integers(-(1 << 40), 1 << 40, size=(9, 37), dtype=np.int64)
+    Bi = rng.integers(-(1 << 40), 1 << 40, size=(37, 6), dtype=np.int64)
+    exact = o.exact_int_matmul(Ai, Bi)
+    for m in o.karatsuba_moduli(o.select_moduli(20)):
+        got = o.residue_products_karatsuba(Ai, Bi, m)
+        want = np.vectorize(lambda v: v % m, otypes=[object])(exact).astype(np.int64)
+        assert np.array_equal(got["r"], want), m
+        assert np.array_equal(got["r"], o.residue_products(Ai, Bi, m)["r"]), m
+        a0, a1, as_ = o.limb_planes_karatsuba(Ai, m)
+        assert np.array_equal(as_, a0 + a1)
+        assert np.array_equal(np.mod(a0 + 13 * a1 - Ai, m), np.zeros_like(Ai))
+
+
+def test_dgemm_karatsuba_route_identical():
+    rng = np.random.default_rng(5)
+    A = rng.standard_normal((7, 40))
+    B = rng.standard_normal((40, 5))
+    r1 = o.dgemm(A, B, 19, karatsuba=True, check_definition=True)
+    r2 = o.dgemm(A, B, 19, karatsuba=False)
+    assert np.array_equal(r1["C"].view(np.int64), r2["C"].view(np.int64))
 
 
 def test_best_18_set_below_printed_bound(paper):
