@@ -479,7 +479,7 @@ def round_scaled(x: int, shift: int) -> float:
 # ---------------------------------------------------------------------------
 
 def dgemm(A: np.ndarray, B: np.ndarray, n_moduli: int, rows=None, cols=None,
-          check_definition: bool = False, karatsuba: bool = True) -> dict:
+          check_definition: bool = False, karatsuba: bool = False) -> dict:
     """C = A B by Ozaki scheme II on base-13 E2M1 limbs (Sec. IV-B, V).
 
     Optional `rows` / `cols` restrict the output to a sub-block (the scaling
@@ -491,7 +491,8 @@ def dgemm(A: np.ndarray, B: np.ndarray, n_moduli: int, rows=None, cols=None,
     With check_definition=True the reconstructed x is also compared with the
     exact integer product of the converted operands (Eq. (crt) guarantees
     equality). With karatsuba=True the Karatsuba moduli take the three-product
-    route (residue_products_karatsuba); the residues are the same either way.
+    route of Sec. V-A (residue_products_karatsuba); the residues are the same
+    either way. The GPU library runs the four-product route.
     """
     A = np.asarray(A, dtype=np.float64)
     B = np.asarray(B, dtype=np.float64)

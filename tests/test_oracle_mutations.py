@@ -9,6 +9,9 @@ import oracle as o
 from oracle import ozaki2_fp4 as mod
 
 
+_ROUTE = {"karatsuba": False}
+
+
 def _tiny_mismatch():
     """True when the residue route disagrees with the exact definition on a
     few tiny matrices (the brute-force pin), or raises an internal check."""
@@ -18,7 +21,7 @@ def _tiny_mismatch():
         A = (rng.random((m, k)) - 0.5) * np.exp2(rng.integers(-30, 30, size=(m, k)))
         B = (rng.random((k, n)) - 0.5) * np.exp2(rng.integers(-30, 30, size=(k, n)))
         try:
-            got = o.dgemm(A, B, 14)["C"]
+            got = o.dgemm(A, B, 14, karatsuba=_ROUTE["karatsuba"])["C"]
         except (AssertionError, ValueError):
             return True
         if not np.array_equal(got, o.dgemm_definition(A, B, 14)):
@@ -140,6 +143,7 @@ def test_karatsuba_cross_term_without_p2_is_caught(monkeypatch):
         out["r"] = np.mod(out["P0"] + 13 * (out["Ps"] - out["P0"]) + 169 * out["P2"], m)
         return out
     monkeypatch.setattr(mod, "residue_products_karatsuba", bad)
+    monkeypatch.setitem(_ROUTE, "karatsuba", True)
     assert _tiny_mismatch()
 
 
@@ -150,4 +154,5 @@ def test_karatsuba_wrong_sum_plane_is_caught(monkeypatch):
         c0, c1, _ = orig(Xi, m)
         return c0, c1, c0 - c1
     monkeypatch.setattr(mod, "limb_planes_karatsuba", bad)
+    monkeypatch.setitem(_ROUTE, "karatsuba", True)
     assert _tiny_mismatch()
