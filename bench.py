@@ -11,7 +11,7 @@ CPU oracle timed on a bounded sample, a per-stage breakdown, native FP64
 matrix product on the same GPU and the INT8-on-FP4 path as context.
 
 Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--moduli L]
-                       [--size N] [--sweep] [--no-cpu-baseline] [--no-native]
+                       [--size N] [--sweep] [--no-cpu-baseline] [--no-native] [--no-karatsuba]
 """
 
 from __future__ import annotations
@@ -149,6 +149,8 @@ def main() -> int:
     ap.add_argument("--no-native", action="store_true")
     ap.add_argument("--no-int8", action="store_true")
     ap.add_argument("--no-accuracy", action="store_true")
+    ap.add_argument("--no-karatsuba", action="store_true",
+                    help="skip timing the three-product Karatsuba mode (comparison only)")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="also run a plain 1 GiB device copy (reference for HBM byte counters)")
     args = ap.parse_args()
@@ -270,7 +272,7 @@ def main() -> int:
 
     if not args.no_native:
         log("timing native FP64 torch.matmul")
-        Ar = Ad.contiguous() if False else torch.from_numpy(A).to("cuda")
+        Ar = torch.from_numpy(A).to("cuda")
         Br = torch.from_numpy(B).to("cuda")
         for _ in range(2):
             torch.matmul(Ar, Br)
@@ -284,6 +286,27 @@ def main() -> int:
         result["native_fp64"] = {"ms": nms, "tflops": 2.0 * N ** 3 / nms / 1e9,
                                  "speedup_of_emulation": nms / ms}
         del Ar, Br
+
+    if not args.no_karatsuba:
+        # the Karatsuba mode of Sec. V-A (three products for the sum-limb
+        # moduli): reported beside the default route, not as the headline
+        log("timing the Karatsuba mode")
+        Cref = C.clone()
+        ozfp4.ozfp4_set_karatsuba(True)
+        try:
+            nplanes, _ = ozfp4.ozfp4_plane_count(L)
+            kms, kst = time_dgemm(ozfp4, torch, Ad, Bd, C, L, max(3, args.steps // 2), 1)
+        finally:
+            ozfp4.ozfp4_set_karatsuba(False)
+        nk = nplanes - 2 * L
+        kprod = 4 * L - 1 - nk
+        result["karatsuba"] = {
+            "ms": kms, "tflops": 2.0 * N ** 3 / kms / 1e9, "gemm_ms": kst[3],
+            "products_per_element": kprod, "default_products_per_element": 4 * L - 1,
+            "fp4_tflops_gemm": kprod * 2.0 * N ** 3 / kst[3] / 1e9,
+            "c_bitwise_equal_to_default": bool(torch.equal(Cref.view(torch.int64),
+                                                           C.view(torch.int64)))}
+        del Cref
 
     if not args.no_int8:
         log("timing ozfp4_igemm_s8 8192^3")

@@ -100,6 +100,20 @@ int ozfp4_igemm_s8(int64_t m, int64_t n, int64_t k,
 /* Stream for subsequent calls (a hipStream_t; NULL = the null stream). */
 int ozfp4_set_stream(void* stream);
 
+/*
+ * ozfp4_set_karatsuba -- select the residue-GEMM route of subsequent
+ * ozfp4_dgemm calls and hooks (default 0). With 1, every Karatsuba modulus
+ * (Sec. V-A: each class has limbs c0, c1 whose sum c0 + c1 is in S; 83, 73,
+ * 71, 67, 61, 59, 53, 47 among the first 20) takes three limb products,
+ * a0 b0, a1 b1 and (a0 + a1)(b0 + b1), instead of four, from limbs chosen by
+ * ozfp4_sum_limb_table and a third operand plane holding c0 + c1. At 18
+ * moduli that is 65 products instead of 71. C and the residues are the same
+ * in both modes; the limb planes differ. The three-product route moves
+ * twice the operand bytes per MFMA and measured slower on MI355X, hence the
+ * default. A process-wide setting, like the stream.
+ */
+int ozfp4_set_karatsuba(int enable);
+
 /* Releases every device workspace and table of the library. */
 int ozfp4_finalize(void);
 
@@ -127,6 +141,22 @@ int ozfp4_capacity(int64_t k, int n_moduli, int32_t* c_a, int32_t* c_b);
  * codes 0..7, sign bit 0x8; a limb c is stored as the value c/2. */
 int ozfp4_two_limb_table(int modulus_index, uint8_t* out, int32_t* m_out);
 
+/* Limbs of every residue r in [0, m_l) of a Karatsuba modulus l for the
+ * Karatsuba mode (ozfp4_set_karatsuba): c0, c1 and c0 + c1 all in S and of
+ * magnitude <= 8 (which keeps each single-product accumulator within the
+ * FP32 bound up to OZFP4_MAX_K); the canonical split when it qualifies,
+ * otherwise the qualifying split with the smallest |c1|, then the smallest
+ * |c0|. HOST array out[m_l] in the format of ozfp4_two_limb_table. Returns
+ * OZFP4_EINVAL for a modulus that is not a Karatsuba modulus. */
+int ozfp4_sum_limb_table(int modulus_index, uint8_t* out, int32_t* m_out);
+
+/* Planes per operand of ozfp4_dgemm with n_moduli moduli in the current
+ * mode: 2 n_moduli limb planes, plus in the Karatsuba mode one sum plane
+ * (c0 + c1) per Karatsuba modulus among them. HOST outputs: *n_planes, and
+ * when sum_plane is not NULL the index of the sum plane of each modulus in
+ * sum_plane[n_moduli] (-1 for none). */
+int ozfp4_plane_count(int n_moduli, int32_t* n_planes, int32_t* sum_plane);
+
 /* Layout of the packed FP4 limb planes (the debug hook below returns them):
  * lines (rows of A, columns of B) are padded to rows_pad, k to k_pad, and
  * one plane holds rows_pad * k_pad / 2 bytes. */
@@ -147,9 +177,12 @@ int ozfp4_scales(int64_t m, int64_t n, int64_t k,
 /*
  * ozfp4_limb_planes -- the packed E2M1 limb planes of ozfp4_dgemm
  * (Sec. V-A two-limb residues, Sec. VI-B fused encoder), DEVICE buffers of
- * 2 * n_moduli * bytes_per_plane bytes each (ozfp4_plane_layout with the
- * line count m for A and n for B).
- * Plane p = 2 l + h holds limb h (0: c0, 1: c1) of modulus l. Inside a plane
+ * n_planes * bytes_per_plane bytes each (ozfp4_plane_count;
+ * ozfp4_plane_layout with the line count m for A and n for B).
+ * Plane p = 2 l + h holds limb h (0: c0, 1: c1) of modulus l, from the
+ * canonical split (ozfp4_two_limb_table), or in the Karatsuba mode for a
+ * Karatsuba modulus from ozfp4_sum_limb_table; there, plane 2 n_moduli + j
+ * holds the sum c0 + c1 of the j-th Karatsuba modulus. Inside a plane
  * the bytes are grouped in 1024-byte fragments of 32 lines x 64 k:
  * fragment (rb, kb) starts at ((rb * (k_pad / 64)) + kb) * 1024; byte
  * lane * 16 + j of a fragment, lane in [0, 64), j in [0, 16), holds line

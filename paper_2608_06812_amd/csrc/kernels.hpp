@@ -16,6 +16,8 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <type_traits>
+
 #include "crt_round.hpp"
 #include "tables.hpp"
 
@@ -129,36 +131,42 @@ __global__ void k_shifts(const uint64_t* __restrict__ amax, int64_t lines, int c
 }
 
 // ------------------------------------------------------------ Sec. V-A / VI-B
-// Fused integer conversion, residues for every modulus, canonical two-limb
-// split and E2M1 packing. One wave per fragment (32 lines x 64 k); lane
+// Fused integer conversion, residues for every modulus, two-limb split and
+// E2M1 packing. One wave per fragment (32 lines x 64 k); lane
 // (line % 32, k half) converts its 32 values once, then for each modulus
 // reduces them, looks the codes up in an LDS table and stores 16 bytes to
-// each of the two planes of that modulus.
+// each plane of that modulus: c0 (plane 2l), c1 (plane 2l + 1) and, in the
+// Karatsuba mode (kKar) for a Karatsuba modulus, c0 + c1 (plane
+// 2L + ksum).
 //   x = round_half_even(X * 2^s), |x| <= 2^53, is exact in FP64 and kept as
-//   2x. For each m, q = floor(2x * fl(1/m) / 2) is within one of
-//   floor(x / m), so 2r = 2x - q 2m (exact FMA) has r in [-m, 2m), and r
-//   indexes a table over [-m, 2m) that maps every estimate to the codes of
-//   the canonical split of its class. Adding 2^52 plus the table's byte
-//   offset to 2r gives a double in [2^52, 2^53) whose low 32 bits are the
-//   LDS byte address of the entry.
+//   E x, E = the table entry size in bytes (2, or 4 in the Karatsuba mode).
+//   For each m, q = floor(E x * fl(1/m) / E) is within one of floor(x / m),
+//   so E r = E x - q E m (exact FMA) has r in [-m, 2m), and r indexes a
+//   table over [-m, 2m) that maps every estimate to the codes of its class.
+//   Adding 2^52 plus the table's byte offset to E r gives a double in
+//   [2^52, 2^53) whose low 32 bits are the LDS byte address of the entry.
 constexpr int kEncWaves = 4;
-typedef __attribute__((address_space(3))) const uint16_t lds_u16;
 
+template <typename T>
 __device__ __forceinline__ uint32_t lut_lookup(double y) {
   const uint32_t addr = (uint32_t)__double_as_longlong(y);
-  return *reinterpret_cast<lds_u16*>((size_t)addr);
+  return *reinterpret_cast<__attribute__((address_space(3))) const T*>((size_t)addr);
 }
 
+template <bool kKar>
 __global__ __launch_bounds__(256) void k_encode_dgemm(
     const double* __restrict__ X, int64_t rs, int64_t ks, int64_t lines, int64_t k,
     const uint64_t* __restrict__ amax, int cap, uint8_t* __restrict__ planes,
     int64_t plane_bytes, int64_t nfrag, int64_t kblocks, int L,
-    const ModConst* __restrict__ mc, const uint16_t* __restrict__ lut, int lut_entries) {
-  extern __shared__ uint16_t s_lut[];
-  for (int i = threadIdx.x; i < lut_entries; i += 256) s_lut[i] = lut[i];
+    const ModConst* __restrict__ mc, const void* __restrict__ lut, int lut_entries) {
+  typedef typename std::conditional<kKar, uint32_t, uint16_t>::type Entry;
+  constexpr double kE = (double)sizeof(Entry);
+  extern __shared__ __attribute__((aligned(16))) uint8_t s_raw[];
+  Entry* s_lut = reinterpret_cast<Entry*>(s_raw);
+  const Entry* g_lut = reinterpret_cast<const Entry*>(lut);
+  for (int i = threadIdx.x; i < lut_entries; i += 256) s_lut[i] = g_lut[i];
   __syncthreads();
-  const uint32_t lds_base =
-      (uint32_t)(size_t)(__attribute__((address_space(3))) uint16_t*)s_lut;
+  const uint32_t lds_base = (uint32_t)(size_t)(__attribute__((address_space(3))) uint8_t*)s_raw;
   const int lane = threadIdx.x & 63;
   const int wave = threadIdx.x >> 6;
   for (int64_t f = (int64_t)blockIdx.x * kEncWaves + wave; f < nfrag;
@@ -168,55 +176,74 @@ __global__ __launch_bounds__(256) void k_encode_dgemm(
     const int64_t kbase = kb * kFragK + (lane >> 5) * 32;
     const bool live = line < lines;
     const int s = live ? line_shift(amax[line], cap) : 0;
-    double x2[32];
+    double xe[32];
     const double* src = X + (live ? line : 0) * rs + kbase * ks;
     if (live && kbase + 32 <= k) {
 #pragma unroll
       for (int e = 0; e < 32; ++e) {
-        x2[e] = *src;
+        xe[e] = *src;
         src += ks;
       }
     } else {
 #pragma unroll
       for (int e = 0; e < 32; ++e) {
-        x2[e] = (live && kbase + e < k) ? *src : 0.0;
+        xe[e] = (live && kbase + e < k) ? *src : 0.0;
         src += ks;
       }
     }
 #pragma unroll
     for (int e = 0; e < 32; ++e) {
-      const double t = __builtin_rint(__builtin_ldexp(x2[e], s));
+      const double t = __builtin_rint(__builtin_ldexp(xe[e], s));
       // finite inputs give |t| <= 2^53; NaN/Inf (reported by the scale
       // stage) must not drive the table address out of range
-      x2[e] = (__builtin_fabs(t) <= 0x1p53) ? 2.0 * t : 0.0;
+      xe[e] = (__builtin_fabs(t) <= 0x1p53) ? kE * t : 0.0;
     }
     uint8_t* out = planes + f * kFragBytes + lane * 16;
     for (int l = 0; l < L; ++l) {
       const int m = mc->m[l];
-      const double inv = 0.5 * mc->inv[l];
-      const double m2 = 2.0 * mc->md[l];
-      const double base = 0x1p52 + (double)(lds_base + 2u * (uint32_t)(mc->lut_off[l] + m));
-      uint32_t w0[4], w1[4];
+      const double inv = mc->inv[l] / kE;
+      const double mE = kE * mc->md[l];
+      const double base =
+          0x1p52 + (double)(lds_base + (uint32_t)kE * (uint32_t)(mc->lut_off[l] + m));
+      uint32_t w0[4], w1[4], w2[4];
 #pragma unroll
       for (int g = 0; g < 4; ++g) {
         uint32_t p[4];
 #pragma unroll
         for (int h = 0; h < 4; ++h) {
           const int e = g * 8 + h * 2;
-          const double q0 = __builtin_floor(x2[e] * inv);
-          const double q1 = __builtin_floor(x2[e + 1] * inv);
-          const uint32_t E0 = lut_lookup(__builtin_fma(-q0, m2, x2[e]) + base);
-          const uint32_t E1 = lut_lookup(__builtin_fma(-q1, m2, x2[e + 1]) + base);
-          p[h] = E0 | (E1 << 4);  // byte 0: plane-0 byte, byte 1: plane-1 byte
+          const double q0 = __builtin_floor(xe[e] * inv);
+          const double q1 = __builtin_floor(xe[e + 1] * inv);
+          const uint32_t E0 = lut_lookup<Entry>(__builtin_fma(-q0, mE, xe[e]) + base);
+          const uint32_t E1 = lut_lookup<Entry>(__builtin_fma(-q1, mE, xe[e + 1]) + base);
+          // byte 0: plane-0 byte, byte 1: plane-1 byte (byte 2: sum plane)
+          p[h] = E0 | (E1 << 4);
         }
-        const uint32_t u = p[0] | (p[1] << 16), v = p[2] | (p[3] << 16);
-        w0[g] = __builtin_amdgcn_perm(v, u, 0x06040200u);
-        w1[g] = __builtin_amdgcn_perm(v, u, 0x07050301u);
+        if constexpr (!kKar) {
+          const uint32_t u = p[0] | (p[1] << 16), v = p[2] | (p[3] << 16);
+          w0[g] = __builtin_amdgcn_perm(v, u, 0x06040200u);
+          w1[g] = __builtin_amdgcn_perm(v, u, 0x07050301u);
+        } else {
+          const uint32_t t01 = __builtin_amdgcn_perm(p[1], p[0], 0x05010400u);
+          const uint32_t t23 = __builtin_amdgcn_perm(p[3], p[2], 0x05010400u);
+          w0[g] = __builtin_amdgcn_perm(t23, t01, 0x05040100u);
+          w1[g] = __builtin_amdgcn_perm(t23, t01, 0x07060302u);
+          const uint32_t s01 = __builtin_amdgcn_perm(p[1], p[0], 0x00000602u);
+          const uint32_t s23 = __builtin_amdgcn_perm(p[3], p[2], 0x00000602u);
+          w2[g] = __builtin_amdgcn_perm(s23, s01, 0x05040100u);
+        }
       }
-      v4i p0 = {(int)w0[0], (int)w0[1], (int)w0[2], (int)w0[3]};
-      v4i p1 = {(int)w1[0], (int)w1[1], (int)w1[2], (int)w1[3]};
+      const v4i p0 = {(int)w0[0], (int)w0[1], (int)w0[2], (int)w0[3]};
+      const v4i p1 = {(int)w1[0], (int)w1[1], (int)w1[2], (int)w1[3]};
       *reinterpret_cast<v4i*>(out + (int64_t)(2 * l) * plane_bytes) = p0;
       *reinterpret_cast<v4i*>(out + (int64_t)(2 * l + 1) * plane_bytes) = p1;
+      if constexpr (kKar) {
+        const int ksum = mc->ksum[l];
+        if (ksum >= 0) {
+          const v4i p2 = {(int)w2[0], (int)w2[1], (int)w2[2], (int)w2[3]};
+          *reinterpret_cast<v4i*>(out + (int64_t)(2 * L + ksum) * plane_bytes) = p2;
+        }
+      }
     }
   }
 }
@@ -370,6 +397,43 @@ constexpr int kDmaPerWave = kStageFrags / kWaves;   // 6
 __device__ __forceinline__ constexpr int fragA(int p, int rb, int kbl) { return ((p * 8 + rb) * 2 + kbl) * kFragBytes; }
 __device__ __forceinline__ constexpr int fragB(int p, int cb, int kbl) { return (32 + (p * 4 + cb) * 2 + kbl) * kFragBytes; }
 
+// Epilogue of a block tile: r = (W0 acc0 + W1 acc1 + W2 acc2) mod m for the
+// wave's 64 x 64 outputs, one byte per element, four rows per 32-bit store.
+// The accumulators hold exact multiples of 1/4 (Lemma 3), the FP64 sum is
+// exact, and floor(d fl(1/m)) is within one of floor(d / m).
+template <int W0, int W1, int W2>
+__device__ __forceinline__ void store_residues(const v16f (&acc)[3][2][2], int l, int64_t tm,
+                                               int64_t tn, int wm, int wn, int lane,
+                                               uint8_t* __restrict__ R, int64_t ldr,
+                                               int64_t rplane, const ModConst* __restrict__ mc) {
+  const int m = mc->m[l];
+  const double inv = mc->inv[l], md = mc->md[l];
+  uint8_t* Rl = R + (int64_t)l * rplane;
+#pragma unroll
+  for (int i = 0; i < 2; ++i)
+#pragma unroll
+    for (int j = 0; j < 2; ++j) {
+      const int64_t col = tn * kTileN + wn * 64 + j * 32 + (lane & 31);
+#pragma unroll
+      for (int g = 0; g < 4; ++g) {
+        const int64_t row = tm * kTileM + wm * 64 + i * 32 + g * 8 + (lane >> 5) * 4;
+        uint32_t word = 0;
+#pragma unroll
+        for (int v4 = 0; v4 < 4; ++v4) {
+          const int v = g * 4 + v4;
+          double d = (double)W0 * (double)acc[0][i][j][v] + (double)W1 * (double)acc[1][i][j][v] +
+                     (double)W2 * (double)acc[2][i][j][v];
+          double qd = __builtin_floor(d * inv);
+          int r = (int)__builtin_fma(-qd, md, d);
+          r += (r < 0) ? m : 0;
+          r -= (r >= m) ? m : 0;
+          word |= (uint32_t)r << (8 * v4);
+        }
+        *reinterpret_cast<uint32_t*>(Rl + col * ldr + row) = word;
+      }
+    }
+}
+
 // One block tile of modulus l. kSkipA1B1: m = 169 = 13^2, where 169 a1 b1 is
 // 0 mod m (Sec. V-A), so the a1 b1 products are not issued (acc2 stays 0).
 template <bool kSkipA1B1>
@@ -490,45 +554,175 @@ __device__ __forceinline__ void gemm_res_tile(
   stage_body(s + 2);
   mfma_tail();
 
-  // epilogue: residue composition mod m (Sec. V-A, Lemma 3)
-  const int m = mc->m[l];
-  const double inv = mc->inv[l], md = mc->md[l];
-  uint8_t* Rl = R + (int64_t)l * rplane;
-#pragma unroll
-  for (int i = 0; i < 2; ++i)
-#pragma unroll
-    for (int j = 0; j < 2; ++j) {
-      const int64_t col = tn * kTileN + wn * 64 + j * 32 + (lane & 31);
-#pragma unroll
-      for (int g = 0; g < 4; ++g) {
-        const int64_t row = tm * kTileM + wm * 64 + i * 32 + g * 8 + (lane >> 5) * 4;
-        uint32_t word = 0;
-#pragma unroll
-        for (int v4 = 0; v4 < 4; ++v4) {
-          const int v = g * 4 + v4;
-          double d = 4.0 * (double)acc[0][i][j][v] + 52.0 * (double)acc[1][i][j][v] +
-                     676.0 * (double)acc[2][i][j][v];
-          double qd = __builtin_floor(d * inv);
-          int r = (int)__builtin_fma(-qd, md, d);
-          r += (r < 0) ? m : 0;
-          r -= (r >= m) ? m : 0;
-          word |= (uint32_t)r << (8 * v4);
-        }
-        *reinterpret_cast<uint32_t*>(Rl + col * ldr + row) = word;
-      }
-    }
+  store_residues<4, 52, 676>(acc, l, tm, tn, wm, wn, lane, R, ldr, rplane, mc);
 }
 
+// Karatsuba moduli (Sec. V-A): three planes per operand, c0 (2l), c1
+// (2l + 1) and c0 + c1 (2L + ksum), and three products per k, P0 = a0 b0 in
+// acc0, Ps = (a0 + a1)(b0 + b1) in acc1 and P2 = a1 b1 in acc2. With the
+// MFMA's factor 1/4 on each product, r = 4 (P0 + 13 (Ps - P0 - P2) + 169 P2)
+// = -48 P0 + 52 Ps + 624 P2 (mod m). Same block tile and waves as above; k
+// in stages of 64, 36 fragments (A: 3 planes x 8 line blocks, then B: 3
+// planes x 4 line blocks), in a 4-slot ring of 36 KiB that waves 0..5 fill
+// with 6 fragments each, up to four stages ahead.
+constexpr int kRingK = 4;
+constexpr int kStageFragsK = 36;
+constexpr int kStageBytesK = kStageFragsK * kFragBytes;
+constexpr int kDmaWavesK = kStageFragsK / kDmaPerWave;   // 6
+static_assert(kRingK * kStageBytesK <= kRing * kStageBytes, "Karatsuba ring exceeds the LDS array");
+__device__ __forceinline__ constexpr int fragAK(int p, int rb) { return (p * 8 + rb) * kFragBytes; }
+__device__ __forceinline__ constexpr int fragBK(int p, int cb) { return (24 + p * 4 + cb) * kFragBytes; }
+
+__device__ __forceinline__ void gemm_res_tile_k(
+    uint8_t* lds, int l, int L, int64_t tm, int64_t tn, const uint8_t* __restrict__ PA,
+    const uint8_t* __restrict__ PB, uint8_t* __restrict__ R, int64_t plane_a, int64_t plane_b,
+    int64_t kblocks, int64_t ldr, int64_t rplane, const ModConst* __restrict__ mc) {
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int wm = wave >> 1, wn = wave & 1;
+  const int rbw = 2 * wm, cbw = 2 * wn;
+  const int psum = 2 * L + mc->ksum[l];
+
+  // fragment f = wave * 6 + j of a stage (LDS offset f KiB), waves 0..5
+  const uint8_t* gsrc[kDmaPerWave];
+#pragma unroll
+  for (int j = 0; j < kDmaPerWave; ++j) {
+    const int f = wave * kDmaPerWave + j;
+    if (f < 24) {
+      const int p = f >> 3, rb = f & 7;
+      const int plane = p < 2 ? 2 * l + p : psum;
+      gsrc[j] = PA + (int64_t)plane * plane_a + (tm * 8 + rb) * kblocks * kFragBytes;
+    } else {
+      const int g = f < 36 ? f - 24 : 0, p = g >> 2, cb = g & 3;
+      const int plane = p < 2 ? 2 * l + p : psum;
+      gsrc[j] = PB + (int64_t)plane * plane_b + (tn * 4 + cb) * kblocks * kFragBytes;
+    }
+  }
+  const bool dma_wave = wave < kDmaWavesK;
+  const int lane16 = lane * 16;
+  const int nst = (int)kblocks;
+  auto issue = [&](int s) {
+    if (dma_wave) {
+      uint8_t* dst = lds + (s & (kRingK - 1)) * kStageBytesK + wave * kDmaPerWave * kFragBytes;
+#pragma unroll
+      for (int j = 0; j < kDmaPerWave; ++j)
+        dma16(gsrc[j] + (int64_t)s * kFragBytes + lane16, dst + j * kFragBytes);
+    }
+  };
+
+  v16f acc[3][2][2];
+#pragma unroll
+  for (int a = 0; a < 3; ++a)
+#pragma unroll
+    for (int i = 0; i < 2; ++i)
+#pragma unroll
+      for (int j = 0; j < 2; ++j)
+#pragma unroll
+        for (int v = 0; v < 16; ++v) acc[a][i][j][v] = 0.0f;
+
+  // Per stage: P0 (4 MFMAs), read the sum fragments, P2 (4), the handover
+  // (wait for stage s + 1 and this wave's reads, barrier, refill the slot of
+  // stage s with stage s + 4), Ps (4), read c0 / c1 fragments of stage s + 1.
+#pragma unroll
+  for (int s = 0; s < kRingK; ++s) issue(s);   // nst >= 6 > kRingK by padding
+  wait_vm_lgkm0<(kRingK - 1) * kDmaPerWave>();
+  block_sync();
+
+  v4i a0[2], a1[2], b0[2], b1[2], as[2], bs[2];
+  auto slot = [&](int s) { return lds + (s & (kRingK - 1)) * kStageBytesK; };
+  auto read_lo = [&](const uint8_t* sb) {
+#pragma unroll
+    for (int i = 0; i < 2; ++i) {
+      a0[i] = *reinterpret_cast<const v4i*>(sb + fragAK(0, rbw + i) + lane16);
+      b0[i] = *reinterpret_cast<const v4i*>(sb + fragBK(0, cbw + i) + lane16);
+      a1[i] = *reinterpret_cast<const v4i*>(sb + fragAK(1, rbw + i) + lane16);
+      b1[i] = *reinterpret_cast<const v4i*>(sb + fragBK(1, cbw + i) + lane16);
+    }
+  };
+  auto read_sum = [&](const uint8_t* sb) {
+#pragma unroll
+    for (int i = 0; i < 2; ++i) {
+      as[i] = *reinterpret_cast<const v4i*>(sb + fragAK(2, rbw + i) + lane16);
+      bs[i] = *reinterpret_cast<const v4i*>(sb + fragBK(2, cbw + i) + lane16);
+    }
+  };
+  auto mfma_p0 = [&]() {
+#pragma unroll
+    for (int i = 0; i < 2; ++i)
+#pragma unroll
+      for (int j = 0; j < 2; ++j) acc[0][i][j] = mfma_fp4(a0[i], b0[j], acc[0][i][j]);
+  };
+  auto mfma_p2 = [&]() {
+#pragma unroll
+    for (int i = 0; i < 2; ++i)
+#pragma unroll
+      for (int j = 0; j < 2; ++j) acc[2][i][j] = mfma_fp4(a1[i], b1[j], acc[2][i][j]);
+  };
+  auto mfma_ps = [&]() {
+#pragma unroll
+    for (int i = 0; i < 2; ++i)
+#pragma unroll
+      for (int j = 0; j < 2; ++j) acc[1][i][j] = mfma_fp4(as[i], bs[j], acc[1][i][j]);
+  };
+  auto head = [&](int s) {   // stage s up to the handover
+    mfma_p0();
+    read_sum(slot(s));
+    mfma_p2();
+    __builtin_amdgcn_sched_barrier(0);
+  };
+
+  read_lo(slot(0));
+  int s = 0;
+  for (; s + kRingK < nst; ++s) {   // steady state: the refill is always due
+    head(s);
+    wait_vm_lgkm0<(kRingK - 2) * kDmaPerWave>();   // stage s + 1 landed; reads done
+    block_sync();
+    issue(s + kRingK);
+    __builtin_amdgcn_sched_barrier(0);
+    mfma_ps();
+    read_lo(slot(s + 1));
+    __builtin_amdgcn_sched_barrier(0);
+  }
+  // the last four stages
+  head(s);
+  wait_vm_lgkm0<2 * kDmaPerWave>();
+  block_sync();
+  mfma_ps();
+  read_lo(slot(s + 1));
+  __builtin_amdgcn_sched_barrier(0);
+  head(s + 1);
+  wait_vm_lgkm0<kDmaPerWave>();
+  block_sync();
+  mfma_ps();
+  read_lo(slot(s + 2));
+  __builtin_amdgcn_sched_barrier(0);
+  head(s + 2);
+  wait_vm_lgkm0<0>();
+  block_sync();
+  mfma_ps();
+  read_lo(slot(s + 3));
+  __builtin_amdgcn_sched_barrier(0);
+  head(s + 3);
+  mfma_ps();
+
+  store_residues<-48, 52, 624>(acc, l, tm, tn, wm, wn, lane, R, ldr, rplane, mc);
+}
+
+// kKar: the Karatsuba mode, where the Karatsuba moduli take the
+// three-product tile; a separate kernel, so the default kernel is unchanged.
+template <bool kKar>
 __global__ __launch_bounds__(512, 1) void k_gemm_res(
     const uint8_t* __restrict__ PA, const uint8_t* __restrict__ PB, uint8_t* __restrict__ R,
     int64_t plane_a, int64_t plane_b, int64_t kblocks, int64_t tiles_m, int64_t tiles_n,
-    int64_t nblocks, int64_t ldr, int64_t rplane, const ModConst* __restrict__ mc) {
+    int64_t nblocks, int64_t ldr, int64_t rplane, const ModConst* __restrict__ mc, int L) {
   __shared__ __attribute__((aligned(1024))) uint8_t lds[kRing * kStageBytes];
   int l;
   int64_t tm, tn;
   tile_coords(blockIdx.x, nblocks, tiles_m, tiles_n, &l, &tm, &tn);
   if (mc->m[l] == 169)
     gemm_res_tile<true>(lds, l, tm, tn, PA, PB, R, plane_a, plane_b, kblocks, ldr, rplane, mc);
+  else if (kKar && mc->ksum[l] >= 0)
+    gemm_res_tile_k(lds, l, L, tm, tn, PA, PB, R, plane_a, plane_b, kblocks, ldr, rplane, mc);
   else
     gemm_res_tile<false>(lds, l, tm, tn, PA, PB, R, plane_a, plane_b, kblocks, ldr, rplane, mc);
 }

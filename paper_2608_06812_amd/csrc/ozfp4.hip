@@ -24,6 +24,7 @@ struct DeviceState {
   ModConst* d_mod = nullptr;
   CrtConst* d_crt = nullptr;  // kMaxModuli + 1 entries, index L
   uint16_t* d_lut = nullptr;
+  uint32_t* d_lut_k = nullptr;   // encoder LUT of the Karatsuba mode
   uint16_t* d_lut8 = nullptr;
   uint8_t* ws = nullptr;
   size_t ws_bytes = 0;
@@ -37,6 +38,7 @@ std::once_flag g_tables_once;
 DeviceState g_dev[kMaxDevices];
 hipStream_t g_stream = nullptr;
 bool g_profile = false;
+bool g_karatsuba = false;
 double g_stage_ms[kMaxStages];
 int g_nstages = 0;
 int g_pending_stages = 0;   // events recorded by the last profiled call
@@ -65,10 +67,13 @@ int device_state(DeviceState** out) {
     HIP_TRY(hipMalloc(&d.d_mod, sizeof(ModConst)));
     HIP_TRY(hipMalloc(&d.d_crt, sizeof(CrtConst) * (kMaxModuli + 1)));
     HIP_TRY(hipMalloc(&d.d_lut, T->lut.size() * sizeof(uint16_t)));
+    HIP_TRY(hipMalloc(&d.d_lut_k, T->lut_k.size() * sizeof(uint32_t)));
     HIP_TRY(hipMalloc(&d.d_lut8, sizeof(T->lut8)));
     HIP_TRY(hipMemcpy(d.d_mod, &T->mod, sizeof(ModConst), hipMemcpyHostToDevice));
     HIP_TRY(hipMemcpy(d.d_crt, T->crt, sizeof(CrtConst) * (kMaxModuli + 1), hipMemcpyHostToDevice));
     HIP_TRY(hipMemcpy(d.d_lut, T->lut.data(), T->lut.size() * sizeof(uint16_t), hipMemcpyHostToDevice));
+    HIP_TRY(hipMemcpy(d.d_lut_k, T->lut_k.data(), T->lut_k.size() * sizeof(uint32_t),
+                      hipMemcpyHostToDevice));
     HIP_TRY(hipMemcpy(d.d_lut8, T->lut8, sizeof(T->lut8), hipMemcpyHostToDevice));
     HIP_TRY(hipHostMalloc(reinterpret_cast<void**>(&d.h_flag), sizeof(int), hipHostMallocDefault));
     for (int i = 0; i <= kMaxStages; ++i) HIP_TRY(hipEventCreate(&d.ev[i]));
@@ -102,6 +107,8 @@ struct DgemmPlan {
   int L, cA, cB;
   int64_t m_pad, n_pad, k_pad, kblocks;
   int64_t plane_a, plane_b;  // bytes per plane
+  bool kar;                  // Karatsuba mode
+  int nplanes;               // planes per operand: 2L, plus the sum planes in the Karatsuba mode
   // workspace offsets
   size_t off_amax_a, off_amax_b, off_flag, off_pa, off_pb, off_r, total;
 };
@@ -131,12 +138,14 @@ int make_dgemm_plan(int64_t m, int64_t n, int64_t k, int L, DgemmPlan* p) {
   p->kblocks = p->k_pad / kFragK;
   p->plane_a = p->m_pad * p->k_pad / 2;
   p->plane_b = p->n_pad * p->k_pad / 2;
+  p->kar = g_karatsuba;
+  p->nplanes = 2 * L + (p->kar ? T->nk[L] : 0);
   size_t off = 0;
   p->off_amax_a = off; off = align256(off + sizeof(uint64_t) * p->m_pad);
   p->off_amax_b = off; off = align256(off + sizeof(uint64_t) * p->n_pad);
   p->off_flag = off;   off = align256(off + 256);
-  p->off_pa = off;     off = align256(off + (size_t)p->plane_a * 2 * L);
-  p->off_pb = off;     off = align256(off + (size_t)p->plane_b * 2 * L);
+  p->off_pa = off;     off = align256(off + (size_t)p->plane_a * p->nplanes);
+  p->off_pb = off;     off = align256(off + (size_t)p->plane_b * p->nplanes);
   p->off_r = off;      off = align256(off + (size_t)p->m_pad * p->n_pad * L);
   p->total = off;
   return OZFP4_OK;
@@ -186,17 +195,19 @@ int run_dgemm(const DgemmPlan& p, DeviceState* d, const double* A, int64_t lda, 
 
   // stage 1, 2: fused conversion + residues + limbs + E2M1 packing
   const int lut_entries = T->mod.lut_off[L - 1] + 3 * T->mod.m[L - 1];
-  const size_t lut_bytes = sizeof(uint16_t) * (size_t)lut_entries;
+  const size_t lut_bytes = (p.kar ? sizeof(uint32_t) : sizeof(uint16_t)) * (size_t)lut_entries;
+  const void* lut = p.kar ? static_cast<const void*>(d->d_lut_k) : static_cast<const void*>(d->d_lut);
   const int64_t nfa = (p.m_pad / kFragLines) * p.kblocks;
   const int64_t nfb = (p.n_pad / kFragLines) * p.kblocks;
-  hipLaunchKernelGGL(k_encode_dgemm, dim3(encode_grid(nfa)), dim3(256), lut_bytes, g_stream, A,
+  auto encode = p.kar ? k_encode_dgemm<true> : k_encode_dgemm<false>;
+  hipLaunchKernelGGL(encode, dim3(encode_grid(nfa)), dim3(256), lut_bytes, g_stream, A,
                      (int64_t)1, lda, p.m, p.k, amax_a, p.cA, pa, p.plane_a, nfa, p.kblocks, L,
-                     d->d_mod, d->d_lut, lut_entries);
+                     d->d_mod, lut, lut_entries);
   HIP_TRY(hipGetLastError());
   record(d, 2);
-  hipLaunchKernelGGL(k_encode_dgemm, dim3(encode_grid(nfb)), dim3(256), lut_bytes, g_stream, B,
+  hipLaunchKernelGGL(encode, dim3(encode_grid(nfb)), dim3(256), lut_bytes, g_stream, B,
                      ldb, (int64_t)1, p.n, p.k, amax_b, p.cB, pb, p.plane_b, nfb, p.kblocks, L,
-                     d->d_mod, d->d_lut, lut_entries);
+                     d->d_mod, lut, lut_entries);
   HIP_TRY(hipGetLastError());
   record(d, 3);
   if (last < 3) return OZFP4_OK;
@@ -204,9 +215,10 @@ int run_dgemm(const DgemmPlan& p, DeviceState* d, const double* A, int64_t lda, 
   // stage 3: fused residue GEMM for all moduli
   const int64_t tiles_m = p.m_pad / kTileM, tiles_n = p.n_pad / kTileN;
   const int64_t nblocks = tiles_m * tiles_n * L;
-  hipLaunchKernelGGL(k_gemm_res, dim3((unsigned)nblocks), dim3(kWaves * 64), 0, g_stream, pa, pb, R,
+  auto gemm = p.kar ? k_gemm_res<true> : k_gemm_res<false>;
+  hipLaunchKernelGGL(gemm, dim3((unsigned)nblocks), dim3(kWaves * 64), 0, g_stream, pa, pb, R,
                      p.plane_a, p.plane_b, p.kblocks, tiles_m, tiles_n, nblocks, p.m_pad,
-                     p.m_pad * p.n_pad, d->d_mod);
+                     p.m_pad * p.n_pad, d->d_mod, L);
   HIP_TRY(hipGetLastError());
   record(d, 4);
   if (last < 4) return OZFP4_OK;
@@ -343,6 +355,7 @@ int ozfp4_finalize(void) {
     (void)hipFree(d.d_mod);
     (void)hipFree(d.d_crt);
     (void)hipFree(d.d_lut);
+    (void)hipFree(d.d_lut_k);
     (void)hipFree(d.d_lut8);
     (void)hipHostFree(d.h_flag);
     for (int e = 0; e <= kMaxStages; ++e) (void)hipEventDestroy(d.ev[e]);
@@ -396,6 +409,38 @@ int ozfp4_two_limb_table(int modulus_index, uint8_t* out, int32_t* m_out) {
     out[r] = (uint8_t)((e & 0xf) | ((e >> 8) & 0xf) << 4);
   }
   *m_out = m;
+  return OZFP4_OK;
+}
+
+int ozfp4_sum_limb_table(int modulus_index, uint8_t* out, int32_t* m_out) {
+  if (modulus_index < 0 || modulus_index >= OZFP4_MAX_MODULI || !out || !m_out) return OZFP4_EINVAL;
+  const HostTables* T = tables();
+  if (!T) return OZFP4_EHIP;
+  if (T->mod.ksum[modulus_index] < 0) return OZFP4_EINVAL;
+  const int m = T->moduli[modulus_index];
+  const uint32_t* lut = T->lut_k.data() + T->mod.lut_off[modulus_index];
+  for (int r = 0; r < m; ++r) {
+    const uint32_t e = lut[r + m];  // entry of the remainder estimate r itself
+    out[r] = (uint8_t)((e & 0xf) | ((e >> 8) & 0xf) << 4);
+  }
+  *m_out = m;
+  return OZFP4_OK;
+}
+
+int ozfp4_set_karatsuba(int enable) {
+  g_karatsuba = enable != 0;
+  return OZFP4_OK;
+}
+
+int ozfp4_plane_count(int n_moduli, int32_t* n_planes, int32_t* sum_plane) {
+  if (n_moduli < OZFP4_MIN_MODULI || n_moduli > OZFP4_MAX_MODULI) return OZFP4_EMODULI;
+  if (!n_planes) return OZFP4_EINVAL;
+  const HostTables* T = tables();
+  if (!T) return OZFP4_EHIP;
+  *n_planes = 2 * n_moduli + (g_karatsuba ? T->nk[n_moduli] : 0);
+  if (sum_plane)
+    for (int l = 0; l < n_moduli; ++l)
+      sum_plane[l] = (g_karatsuba && T->mod.ksum[l] >= 0) ? 2 * n_moduli + T->mod.ksum[l] : -1;
   return OZFP4_OK;
 }
 

@@ -6,7 +6,8 @@
 //   * the capacity split (c_A, c_B) for an inner dimension k (Sec. IV-B with
 //     Eq. (crt));
 //   * the canonical two-limb split of every residue and its E2M1 codes
-//     (Sec. III, Sec. V-A), as lookup tables for the encoder;
+//     (Sec. III, Sec. V-A), and for the Karatsuba moduli the split whose
+//     limb sum is representable too, as lookup tables for the encoder;
 //   * the three greedy limbs of every int8 (Sec. III).
 #pragma once
 
@@ -14,6 +15,7 @@
 
 #include <algorithm>
 #include <cmath>
+#include <cstdlib>
 #include <cstring>
 #include <vector>
 
@@ -146,9 +148,52 @@ inline bool two_limb_split(int r, int m, int* c0, int* c1) {
   return false;
 }
 
+// Sec. V-A, Karatsuba: every class of m has limbs c0, c1 in S whose sum
+// c0 + c1 is in S as well
+inline bool is_karatsuba(int m) {
+  static const int S[] = {-12, -8, -6, -4, -3, -2, -1, 0, 1, 2, 3, 4, 6, 8, 12};
+  std::vector<char> seen(m, 0);
+  int count = 0;
+  for (int a : S)
+    for (int b : S) {
+      if (!limb_in_S(a + b)) continue;
+      int r = ((a + 13 * b) % m + m) % m;
+      if (!seen[r]) { seen[r] = 1; ++count; }
+    }
+  return count == m;
+}
+
+// limbs of residue r for a Karatsuba modulus: c0, c1, c0 + c1 in S, all
+// within +-8; the canonical split when it qualifies, else the qualifying
+// split with the smallest |c1|, then the smallest |c0|
+inline bool sum_limb_split(int r, int m, int* c0, int* c1) {
+  auto ok = [](int c) { return limb_in_S(c) && c >= -8 && c <= 8; };
+  int a, b;
+  if (two_limb_split(r, m, &a, &b) && ok(a + b)) {
+    *c0 = a;
+    *c1 = b;
+    return true;
+  }
+  bool found = false;
+  int best1 = 0, best0 = 0;
+  for (int y = -8; y <= 8; ++y) {
+    if (!ok(y)) continue;
+    for (int x = -8; x <= 8; ++x) {
+      if (!ok(x) || !ok(x + y) || (((x + 13 * y - r) % m) + m) % m != 0) continue;
+      const bool better = !found || std::abs(y) < std::abs(best1) ||
+                          (std::abs(y) == std::abs(best1) && std::abs(x) < std::abs(best0));
+      if (better) { found = true; best1 = y; best0 = x; }
+    }
+  }
+  *c0 = best0;
+  *c1 = best1;
+  return found;
+}
+
 // ---- device-side constant blocks (plain data, copied once per device) ----
 struct ModConst {
   int m[kMaxModuli];
+  int ksum[kMaxModuli];      // index among the Karatsuba moduli of the list, or -1
   int lut_off[kMaxModuli];   // start of modulus l in the encoder LUT (entries)
   double inv[kMaxModuli];    // fl(1 / m)
   double md[kMaxModuli];     // m as double
@@ -177,6 +222,8 @@ struct HostTables {
   ModConst mod;
   CrtConst crt[kMaxModuli + 1];            // index L (2..20)
   std::vector<uint16_t> lut;               // encoder LUT, all 20 moduli
+  std::vector<uint32_t> lut_k;             // encoder LUT of the Karatsuba mode
+  int nk[kMaxModuli + 1];                  // Karatsuba moduli among the first L
   uint16_t lut8[256];                      // int8 -> three limb codes
   Big P[kMaxModuli + 1];                   // product of the first L moduli
   bool ok = false;
@@ -184,16 +231,24 @@ struct HostTables {
 
 // Encoder LUT of modulus m: 3m entries, index r + m for a remainder
 // estimate r in [-m, 2m) of a signed integer x; entry = code(c0) |
-// code(c1) << 8 for the canonical split of the class of x mod m.
+// code(c1) << 8 for the canonical split of the class of x mod m. The LUT of
+// the Karatsuba mode has the same indexing and 32-bit entries code(c0) |
+// code(c1) << 8 | code(c0 + c1) << 16 from the sum-limb split of a Karatsuba
+// modulus (the canonical split and a zero sum code for the others).
 inline bool build_tables(HostTables& T) {
   T.moduli = greedy_moduli();
   if ((int)T.moduli.size() != kMaxModuli) return false;
   std::memset(&T.mod, 0, sizeof(T.mod));
-  int off = 0;
+  int off = 0, nk = 0;
   T.lut.clear();
+  T.lut_k.clear();
+  T.nk[0] = 0;
   for (int l = 0; l < kMaxModuli; ++l) {
     int m = T.moduli[l];
+    const bool kar = is_karatsuba(m);
     T.mod.m[l] = m;
+    T.mod.ksum[l] = kar ? nk++ : -1;
+    T.nk[l + 1] = nk;
     T.mod.lut_off[l] = off;
     T.mod.inv[l] = 1.0 / (double)m;
     T.mod.md[l] = (double)m;
@@ -204,6 +259,14 @@ inline bool build_tables(HostTables& T) {
       int k0 = e2m1_code_of_limb(c0), k1 = e2m1_code_of_limb(c1);
       if (k0 < 0 || k1 < 0) return false;
       T.lut.push_back((uint16_t)(k0 | (k1 << 8)));
+      if (kar) {
+        if (!sum_limb_split(cls, m, &c0, &c1)) return false;
+        k0 = e2m1_code_of_limb(c0);
+        k1 = e2m1_code_of_limb(c1);
+      }
+      const int ks = kar ? e2m1_code_of_limb(c0 + c1) : 0;
+      if (k0 < 0 || k1 < 0 || ks < 0) return false;
+      T.lut_k.push_back((uint32_t)k0 | ((uint32_t)k1 << 8) | ((uint32_t)ks << 16));
     }
     off += 3 * m;
   }

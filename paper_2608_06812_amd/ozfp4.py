@@ -44,6 +44,9 @@ _SIGNATURES = {
     "ozfp4_moduli": (_int, [_int, _p]),
     "ozfp4_capacity": (_int, [_i64, _int, _p, _p]),
     "ozfp4_two_limb_table": (_int, [_int, _p, _p]),
+    "ozfp4_sum_limb_table": (_int, [_int, _p, _p]),
+    "ozfp4_plane_count": (_int, [_int, _p, _p]),
+    "ozfp4_set_karatsuba": (_int, [_int]),
     "ozfp4_plane_layout": (_int, [_i64, _i64, _p, _p, _p]),
     "ozfp4_scales": (_int, [_i64, _i64, _i64, _p, _i64, _p, _i64, _int, _p, _p]),
     "ozfp4_limb_planes": (_int, [_i64, _i64, _i64, _p, _i64, _p, _i64, _int, _p, _p]),
@@ -113,6 +116,24 @@ def ozfp4_two_limb_table(modulus_index: int) -> tuple[int, bytes]:
     m = ctypes.c_int32()
     _check(load().ozfp4_two_limb_table(modulus_index, out, ctypes.byref(m)), "ozfp4_two_limb_table")
     return m.value, bytes(out)[: m.value]
+
+
+def ozfp4_sum_limb_table(modulus_index: int) -> tuple[int, bytes]:
+    out = (ctypes.c_uint8 * 256)()
+    m = ctypes.c_int32()
+    _check(load().ozfp4_sum_limb_table(modulus_index, out, ctypes.byref(m)), "ozfp4_sum_limb_table")
+    return m.value, bytes(out)[: m.value]
+
+
+def ozfp4_plane_count(n_moduli: int) -> tuple[int, list[int]]:
+    n = ctypes.c_int32()
+    idx = (ctypes.c_int32 * max(1, n_moduli))()
+    _check(load().ozfp4_plane_count(n_moduli, ctypes.byref(n), idx), "ozfp4_plane_count")
+    return n.value, list(idx)[:n_moduli]
+
+
+def ozfp4_set_karatsuba(enable: bool) -> int:
+    return load().ozfp4_set_karatsuba(1 if enable else 0)
 
 
 def ozfp4_plane_layout(lines: int, k: int) -> tuple[int, int, int]:
@@ -238,8 +259,8 @@ def scales(A, B, n_moduli: int = 19):
 
 def limb_planes(A, B, n_moduli: int = 19):
     """Packed E2M1 limb planes of A and B (uint8 device tensors of shape
-    (2 n_moduli, bytes_per_plane)) in the fragment layout of
-    include/ozfp4.h."""
+    (n_planes, bytes_per_plane), n_planes from ozfp4_plane_count) in the
+    fragment layout of include/ozfp4.h."""
     import torch
     A, lda = _cm(A, torch.float64, "A")
     B, ldb = _cm(B, torch.float64, "B")
@@ -247,8 +268,9 @@ def limb_planes(A, B, n_moduli: int = 19):
     n = B.shape[1]
     _, _, bpa = ozfp4_plane_layout(m, k)
     _, _, bpb = ozfp4_plane_layout(n, k)
-    pa = torch.empty((2 * n_moduli, bpa), dtype=torch.uint8, device=A.device)
-    pb = torch.empty((2 * n_moduli, bpb), dtype=torch.uint8, device=A.device)
+    nplanes, _ = ozfp4_plane_count(n_moduli)
+    pa = torch.empty((nplanes, bpa), dtype=torch.uint8, device=A.device)
+    pb = torch.empty((nplanes, bpb), dtype=torch.uint8, device=A.device)
     _use_torch_stream(A.device)
     _check(ozfp4_limb_planes(m, n, k, A.data_ptr(), lda, B.data_ptr(), ldb, n_moduli, pa.data_ptr(),
                              pb.data_ptr()), "ozfp4_limb_planes")

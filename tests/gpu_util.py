@@ -48,13 +48,23 @@ def unpack_planes(buf: np.ndarray, rows_pad: int, k_pad: int) -> np.ndarray:
 _code_lut = {c: o.e2m1_code(c) for c in o.doubled_set()}
 
 
-def oracle_plane_codes(Xi: np.ndarray, moduli, rows_pad: int, k_pad: int) -> np.ndarray:
-    """Expected codes (2L, rows_pad, k_pad) of integer lines Xi (lines x k)."""
+def oracle_plane_codes(Xi: np.ndarray, moduli, rows_pad: int, k_pad: int,
+                       karatsuba: bool = False) -> np.ndarray:
+    """Expected codes (planes, rows_pad, k_pad) of integer lines Xi (lines x k):
+    planes 2l, 2l + 1 hold c0, c1 of modulus l; in the Karatsuba mode a
+    Karatsuba modulus uses the sum-limb split and plane 2L + j holds c0 + c1
+    of the j-th Karatsuba modulus."""
     vec = np.vectorize(lambda c: _code_lut[int(c)], otypes=[np.uint8])
-    out = np.zeros((2 * len(moduli), rows_pad, k_pad), dtype=np.uint8)
+    kset = o.karatsuba_moduli(moduli) if karatsuba else []
+    L = len(moduli)
+    out = np.zeros((2 * L + len(kset), rows_pad, k_pad), dtype=np.uint8)
     lines, k = Xi.shape
     for l, m in enumerate(moduli):
-        c0, c1 = o.limb_planes(Xi, m)
+        if m in kset:
+            c0, c1, cs = o.limb_planes_karatsuba(Xi, m)
+            out[2 * L + kset.index(m), :lines, :k] = vec(cs)
+        else:
+            c0, c1 = o.limb_planes(Xi, m)
         out[2 * l, :lines, :k] = vec(c0)
         out[2 * l + 1, :lines, :k] = vec(c1)
     return out

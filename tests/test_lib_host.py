@@ -33,7 +33,8 @@ def lib():
 def test_header_declares_the_boundary():
     names = _declared_symbols()
     for required in ("ozfp4_dgemm", "ozfp4_igemm_s8", "ozfp4_set_stream", "ozfp4_finalize",
-                     "ozfp4_strerror", "ozfp4_scales", "ozfp4_limb_planes", "ozfp4_residues"):
+                     "ozfp4_strerror", "ozfp4_scales", "ozfp4_limb_planes", "ozfp4_residues",
+                     "ozfp4_sum_limb_table", "ozfp4_plane_count", "ozfp4_set_karatsuba"):
         assert required in names
 
 
@@ -71,6 +72,39 @@ def test_two_limb_tables_match_oracle(lib):
         for r in range(m):
             c0, c1 = o.two_limb_split(r, m)
             assert table[r] == (o.e2m1_code(c0) | (o.e2m1_code(c1) << 4)), (m, r)
+
+
+def test_sum_limb_tables_match_oracle(lib):
+    ms = o.select_moduli(20)
+    kset = o.karatsuba_moduli(ms)
+    for idx, m in enumerate(ms):
+        if m not in kset:
+            with pytest.raises(ozfp4.OzFP4Error) as ei:
+                ozfp4.ozfp4_sum_limb_table(idx)
+            assert ei.value.code == ozfp4.OZFP4_EINVAL
+            continue
+        got_m, table = ozfp4.ozfp4_sum_limb_table(idx)
+        assert got_m == m
+        for r in range(m):
+            c0, c1 = o.sum_limb_split(r, m)
+            assert table[r] == (o.e2m1_code(c0) | (o.e2m1_code(c1) << 4)), (m, r)
+
+
+def test_plane_count_in_both_modes(lib):
+    ms = o.select_moduli(20)
+    try:
+        for mode in (False, True):
+            ozfp4.ozfp4_set_karatsuba(mode)
+            for L in range(2, 21):
+                sub = ms[:L]
+                ks = o.karatsuba_moduli(sub) if mode else []
+                n, idx = ozfp4.ozfp4_plane_count(L)
+                assert n == 2 * L + len(ks)
+                assert idx == [2 * L + ks.index(m) if m in ks else -1 for m in sub]
+        assert ozfp4.ozfp4_plane_count(18)[0] == 36 + 6
+    finally:
+        ozfp4.ozfp4_set_karatsuba(False)
+    assert ozfp4.ozfp4_plane_count(18)[0] == 36
 
 
 def test_plane_layout(lib):
