@@ -727,44 +727,48 @@ __global__ __launch_bounds__(512, 1) void k_gemm_res(
     gemm_res_tile<false>(lds, l, tm, tn, PA, PB, R, plane_a, plane_b, kblocks, ldr, rplane, mc);
 }
 
-// INT8 variant: three planes per operand, five accumulators G_g (g = i + j),
-// epilogue C = sum_g 13^g * 4 G_g in wrapping int32. Block tile 128 x 64,
-// four waves of 64 x 32 (2 x 1 MFMA tiles) so the five accumulator sets stay
-// in registers. LDS stage: A [plane][32-line block 0..3][k fragment] then
-// B [plane][32-line block 0..1][k fragment], 1 KiB each.
+// INT8 variant (Sec. III): three planes per operand, five accumulators
+// G_g = sum_{i + j = g} a_i b_j, epilogue C = sum_g 13^g * 4 G_g in wrapping
+// int32. Block tile 128 x 128, eight waves (two per SIMD) of 64 x 32 (2 x 1
+// MFMA tiles, five accumulator sets = 160 registers). A stage covers k = 128:
+// 48 fragments (A: 3 planes x 4 line blocks x 2 k fragments, then B the
+// same), 48 KiB, streamed into the 3-slot LDS ring by LDS DMA as in the
+// residue GEMM, 6 fragments per wave.
 constexpr int kTileS8M = 128;
-constexpr int kTileS8N = 64;
-__global__ __launch_bounds__(256, 1) void k_gemm_s8(
+constexpr int kTileS8N = 128;
+__device__ __forceinline__ constexpr int fragA8(int p, int rb, int kbl) { return ((p * 4 + rb) * 2 + kbl) * kFragBytes; }
+__device__ __forceinline__ constexpr int fragB8(int p, int cb, int kbl) { return (24 + (p * 4 + cb) * 2 + kbl) * kFragBytes; }
+
+__global__ __launch_bounds__(512, 1) void k_gemm_s8(
     const uint8_t* __restrict__ PA, const uint8_t* __restrict__ PB, int32_t* __restrict__ C,
     int64_t plane_a, int64_t plane_b, int64_t kblocks, int64_t tiles_m, int64_t tiles_n,
     int64_t nblocks, int64_t m, int64_t n, int64_t ldc) {
-  constexpr int NP = 3;
-  constexpr int kABytes = NP * 4 * 2 * kFragBytes;   // 24 KiB
-  constexpr int kBBytes = NP * 2 * 2 * kFragBytes;   // 12 KiB
-  constexpr int kStage = kABytes + kBBytes;
-  constexpr int kPerA = kABytes / 16 / 256;          // 6
-  constexpr int kPerB = kBBytes / 16 / 256;          // 3
-  __shared__ __attribute__((aligned(16))) uint8_t lds[2 * kStage];
-
+  __shared__ __attribute__((aligned(1024))) uint8_t lds[kRing * kStageBytes];
   int l;
   int64_t tm, tn;
   tile_coords(blockIdx.x, nblocks, tiles_m, tiles_n, &l, &tm, &tn);
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int wm = wave >> 1, wn = wave & 1;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int wm = wave >> 2, wn = wave & 3;
+  const int rbw = 2 * wm;   // this wave's first A line block; its B line block is wn
 
-  // A piece q: plane q >> 1, 32-line block ((q & 1) << 1) | ((tid >> 7) & 1);
-  // B piece q: plane q, 32-line block (tid >> 7) & 1; both k fragment
-  // (tid >> 6) & 1 and 16-byte piece tid & 63.
-  const int64_t toffA = (((tid >> 7) & 1) * kblocks + ((tid >> 6) & 1)) * kFragBytes + (tid & 63) * 16;
-  const int64_t toffB = toffA;
-  const uint8_t* gA[kPerA];
-  const uint8_t* gB[kPerB];
+  const uint8_t* gsrc[kDmaPerWave];
 #pragma unroll
-  for (int q = 0; q < kPerA; ++q)
-    gA[q] = PA + (int64_t)(q >> 1) * plane_a + (tm * 4 + 2 * (q & 1)) * kblocks * kFragBytes;
-#pragma unroll
-  for (int q = 0; q < kPerB; ++q) gB[q] = PB + (int64_t)q * plane_b + tn * 2 * kblocks * kFragBytes;
+  for (int j = 0; j < kDmaPerWave; ++j) {
+    const int f = wave * kDmaPerWave + j;
+    const int g = f < 24 ? f : f - 24;
+    const int kbl = g & 1, blk = (g >> 1) & 3, p = g >> 3;
+    gsrc[j] = f < 24 ? PA + (int64_t)p * plane_a + ((tm * 4 + blk) * kblocks + kbl) * kFragBytes
+                     : PB + (int64_t)p * plane_b + ((tn * 4 + blk) * kblocks + kbl) * kFragBytes;
+  }
+  const int lane16 = lane * 16;
   const int nst = (int)(kblocks / 2);
+  auto issue = [&](int s) {
+    uint8_t* dst = lds + (s % kRing) * kStageBytes + wave * kDmaPerWave * kFragBytes;
+#pragma unroll
+    for (int j = 0; j < kDmaPerWave; ++j)
+      dma16(gsrc[j] + (int64_t)s * 2 * kFragBytes + lane16, dst + j * kFragBytes);
+  };
 
   v16f acc[5][2];
 #pragma unroll
@@ -774,66 +778,99 @@ __global__ __launch_bounds__(256, 1) void k_gemm_s8(
 #pragma unroll
       for (int v = 0; v < 16; ++v) acc[a][i][v] = 0.0f;
 
-  v4i sa[kPerA], sbv[kPerB];
 #pragma unroll
-  for (int q = 0; q < kPerA; ++q) sa[q] = *reinterpret_cast<const v4i*>(gA[q] + toffA);
-#pragma unroll
-  for (int q = 0; q < kPerB; ++q) sbv[q] = *reinterpret_cast<const v4i*>(gB[q] + toffB);
-#pragma unroll
-  for (int q = 0; q < kPerA; ++q) *reinterpret_cast<v4i*>(lds + (q * 256 + tid) * 16) = sa[q];
-#pragma unroll
-  for (int q = 0; q < kPerB; ++q) *reinterpret_cast<v4i*>(lds + kABytes + (q * 256 + tid) * 16) = sbv[q];
-  __syncthreads();
+  for (int s = 0; s < kRing; ++s) issue(s);     // nst >= kRing by padding
+  wait_vm_lgkm0<2 * kDmaPerWave>();
+  block_sync();
 
-  for (int s = 0; s < nst; ++s) {
-    const int buf = s & 1;
-    if (s + 1 < nst) {
-      const int64_t adv = (int64_t)(s + 1) * 2 * kFragBytes;
+  v4i a[3][2], b[3];
+  auto read_frags = [&](const uint8_t* sb, int kbl) {
 #pragma unroll
-      for (int q = 0; q < kPerA; ++q) sa[q] = *reinterpret_cast<const v4i*>(gA[q] + toffA + adv);
+    for (int p = 0; p < 3; ++p) {
 #pragma unroll
-      for (int q = 0; q < kPerB; ++q) sbv[q] = *reinterpret_cast<const v4i*>(gB[q] + toffB + adv);
+      for (int i = 0; i < 2; ++i) a[p][i] = *reinterpret_cast<const v4i*>(sb + fragA8(p, rbw + i, kbl) + lane16);
+      b[p] = *reinterpret_cast<const v4i*>(sb + fragB8(p, wn, kbl) + lane16);
     }
-    const uint8_t* sb = lds + buf * kStage;
+  };
+  // the products with i + j <= 2 (12 MFMAs); those with i + j >= 3 (6 MFMAs)
+  // form the tail, which follows the stage handover
+  auto mfma_head = [&]() {
 #pragma unroll
-    for (int kbl = 0; kbl < 2; ++kbl) {
-      v4i a[NP][2], b[NP];
-#pragma unroll
-      for (int p = 0; p < NP; ++p) {
-#pragma unroll
-        for (int i = 0; i < 2; ++i)
-          a[p][i] = *reinterpret_cast<const v4i*>(sb + ((p * 4 + 2 * wm + i) * 2 + kbl) * kFragBytes + lane * 16);
-        b[p] = *reinterpret_cast<const v4i*>(sb + kABytes + ((p * 2 + wn) * 2 + kbl) * kFragBytes + lane * 16);
-      }
-#pragma unroll
-      for (int pa = 0; pa < NP; ++pa)
-#pragma unroll
-        for (int pb = 0; pb < NP; ++pb)
-#pragma unroll
-          for (int i = 0; i < 2; ++i) acc[pa + pb][i] = mfma_fp4(a[pa][i], b[pb], acc[pa + pb][i]);
+    for (int i = 0; i < 2; ++i) {
+      acc[0][i] = mfma_fp4(a[0][i], b[0], acc[0][i]);
+      acc[1][i] = mfma_fp4(a[0][i], b[1], acc[1][i]);
+      acc[1][i] = mfma_fp4(a[1][i], b[0], acc[1][i]);
+      acc[2][i] = mfma_fp4(a[0][i], b[2], acc[2][i]);
+      acc[2][i] = mfma_fp4(a[1][i], b[1], acc[2][i]);
+      acc[2][i] = mfma_fp4(a[2][i], b[0], acc[2][i]);
     }
-    if (s + 1 < nst) {
-      uint8_t* db = lds + (buf ^ 1) * kStage;
+  };
+  auto mfma_tail = [&]() {
 #pragma unroll
-      for (int q = 0; q < kPerA; ++q) *reinterpret_cast<v4i*>(db + (q * 256 + tid) * 16) = sa[q];
-#pragma unroll
-      for (int q = 0; q < kPerB; ++q) *reinterpret_cast<v4i*>(db + kABytes + (q * 256 + tid) * 16) = sbv[q];
+    for (int i = 0; i < 2; ++i) {
+      acc[3][i] = mfma_fp4(a[1][i], b[2], acc[3][i]);
+      acc[3][i] = mfma_fp4(a[2][i], b[1], acc[3][i]);
+      acc[4][i] = mfma_fp4(a[2][i], b[2], acc[4][i]);
     }
-    __syncthreads();
+  };
+  auto stage_body = [&](int s) {
+    const uint8_t* sb = lds + (s % kRing) * kStageBytes;
+    read_frags(sb, 0);
+    mfma_head();
+    mfma_tail();
+    __builtin_amdgcn_sched_barrier(0);
+    read_frags(sb, 1);
+    mfma_head();
+    __builtin_amdgcn_sched_barrier(0);
+  };
+
+  int s = 0;
+  for (; s + kRing < nst; ++s) {
+    stage_body(s);
+    wait_vm_lgkm0<kDmaPerWave>();  // stage s + 1 landed; reads of stage s done
+    block_sync();
+    issue(s + kRing);
+    mfma_tail();
+    __builtin_amdgcn_sched_barrier(0);
   }
+  stage_body(s);
+  wait_vm_lgkm0<kDmaPerWave>();
+  block_sync();
+  mfma_tail();
+  __builtin_amdgcn_sched_barrier(0);
+  stage_body(s + 1);
+  wait_vm_lgkm0<0>();
+  block_sync();
+  mfma_tail();
+  __builtin_amdgcn_sched_barrier(0);
+  stage_body(s + 2);
+  mfma_tail();
 
-  const int64_t col = tn * kTileS8N + wn * 32 + (lane & 31);
+  // compose every output first (the other four accumulator sets die), then
+  // store with the bounds check
+  uint32_t out[2][16];
 #pragma unroll
   for (int i = 0; i < 2; ++i)
 #pragma unroll
     for (int v = 0; v < 16; ++v) {
-      const int64_t row = tm * kTileS8M + wm * 64 + i * 32 + (v >> 2) * 8 + (lane >> 5) * 4 + (v & 3);
       uint32_t c = (uint32_t)(int)(4.0f * acc[0][i][v]);
       c += 13u * (uint32_t)(int)(4.0f * acc[1][i][v]);
       c += 169u * (uint32_t)(int)(4.0f * acc[2][i][v]);
       c += 2197u * (uint32_t)(int)(4.0f * acc[3][i][v]);
       c += 28561u * (uint32_t)(int)(4.0f * acc[4][i][v]);
-      if (row < m && col < n) C[row + col * ldc] = (int32_t)c;
+      out[i][v] = c;
+      // keeps the composition (and the MFMAs it reads) ahead of the guarded
+      // stores below instead of sunk into their branches
+      asm volatile("" ::"v"(out[i][v]));
+    }
+  const int64_t col = tn * kTileS8N + wn * 32 + (lane & 31);
+  const int64_t row0 = tm * kTileS8M + wm * 64 + (lane >> 5) * 4;
+#pragma unroll
+  for (int i = 0; i < 2; ++i)
+#pragma unroll
+    for (int v = 0; v < 16; ++v) {
+      const int64_t row = row0 + i * 32 + (v >> 2) * 8 + (v & 3);
+      if (row < m && col < n) C[row + col * ldc] = (int32_t)out[i][v];
     }
 }
 

@@ -327,7 +327,7 @@ int ozfp4_igemm_s8(int64_t m, int64_t n, int64_t k, const int8_t* A, int64_t lda
   record(d, 2);
   const int64_t tiles_m = m_pad / kTileS8M, tiles_n = n_pad / kTileS8N;
   const int64_t nblocks = tiles_m * tiles_n;
-  hipLaunchKernelGGL(k_gemm_s8, dim3((unsigned)nblocks), dim3(256), 0, g_stream, pa, pb, C,
+  hipLaunchKernelGGL(k_gemm_s8, dim3((unsigned)nblocks), dim3(kWaves * 64), 0, g_stream, pa, pb, C,
                      plane_a, plane_b, kblocks, tiles_m, tiles_n, nblocks, m, n, ldc);
   record(d, 3);
   HIP_TRY(hipGetLastError());
