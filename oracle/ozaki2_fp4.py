@@ -17,7 +17,8 @@ Readings where the paper is silent (the GPU library documents the same ones):
   * integer conversion rounds half to even (Sec. IV-B says "round");
   * capacity: b is the largest integer with 2 k 2^b < P (Eq. (crt)),
     c_A = min(53, ceil(b/2)), c_B = min(53, b - c_A); with the paper's L = 19
-    and k <= 76,549 this is its c = 53;
+    and k <= 76,549 this is its c = 53 (the wide-range extension raises the
+    cap to at most 63 with more moduli, see capacity_bits);
   * fewer than 19 moduli: the prefix of the greedy list (Sec. V-A); a 20th
     modulus is the next one the same greedy rule picks;
   * canonical two-limb split of a residue (see ``two_limb_split``);
@@ -173,14 +174,19 @@ def crt_weights(moduli) -> list[int]:
 # Sec. IV-B: shared-exponent scaling and integer conversion
 # ---------------------------------------------------------------------------
 
-def capacity_bits(k: int, moduli) -> tuple[int, int]:
+def capacity_bits(k: int, moduli, cmax: int = 53) -> tuple[int, int]:
     """(c_A, c_B): bits of the converted operands (reading of Sec. IV-B with
     Eq. (crt)).
 
     b is the largest integer with 2 k 2^b < P, so that |sum_k A~ B~| <=
     k 2^(c_A + c_B) stays inside the symmetric CRT range. Each side is capped
-    at 53 bits, the range in which integers are exact in FP64.
+    at cmax bits: 53 in the paper's method, where the converted value is an
+    exact FP64 integer below 2^53; up to 63 for the wide-range extension,
+    where the converted values are the exact doubles A 2^s, which are integers
+    once they reach 2^53, held below 2^63.
     """
+    if not 53 <= cmax <= 63:
+        raise ValueError("cmax must be in [53, 63]")
     if k < 1:
         raise ValueError("k must be positive")
     P = moduli_product(moduli)
@@ -188,8 +194,8 @@ def capacity_bits(k: int, moduli) -> tuple[int, int]:
     b = q.bit_length() - 1
     if b < 2:
         raise ValueError("too few moduli for this k")
-    cA = min(53, (b + 1) // 2)
-    cB = min(53, b - cA)
+    cA = min(cmax, (b + 1) // 2)
+    cB = min(cmax, b - cA)
     return cA, cB
 
 
@@ -232,7 +238,7 @@ def to_integers(X: np.ndarray, shifts: np.ndarray, axis: int) -> np.ndarray:
     ldexp by the shared shift is exact except where the product underflows to
     a subnormal; such a product is below 2^-1022 < 0.5 and its subnormal
     rounding cannot reach 0.5, so rounding to an integer still gives 0. rint
-    rounds half to even. |A 2^s| < 2^c <= 2^53, so int64 holds the result.
+    rounds half to even. |A 2^s| < 2^c <= 2^63, so int64 holds the result.
     """
     X = np.asarray(X, dtype=np.float64)
     sh = shifts[:, None] if axis == 1 else shifts[None, :]
@@ -479,7 +485,7 @@ def round_scaled(x: int, shift: int) -> float:
 # ---------------------------------------------------------------------------
 
 def dgemm(A: np.ndarray, B: np.ndarray, n_moduli: int, rows=None, cols=None,
-          check_definition: bool = False, karatsuba: bool = False) -> dict:
+          check_definition: bool = False, karatsuba: bool = False, cmax: int = 53) -> dict:
     """C = A B by Ozaki scheme II on base-13 E2M1 limbs (Sec. IV-B, V).
 
     Optional `rows` / `cols` restrict the output to a sub-block (the scaling
@@ -492,7 +498,8 @@ def dgemm(A: np.ndarray, B: np.ndarray, n_moduli: int, rows=None, cols=None,
     exact integer product of the converted operands (Eq. (crt) guarantees
     equality). With karatsuba=True the Karatsuba moduli take the three-product
     route of Sec. V-A (residue_products_karatsuba); the residues are the same
-    either way. The GPU library runs the four-product route.
+    either way. The GPU library runs the four-product route. cmax caps the
+    capacities (see capacity_bits).
     """
     A = np.asarray(A, dtype=np.float64)
     B = np.asarray(B, dtype=np.float64)
@@ -502,7 +509,7 @@ def dgemm(A: np.ndarray, B: np.ndarray, n_moduli: int, rows=None, cols=None,
     rows = np.arange(m) if rows is None else np.asarray(rows)
     cols = np.arange(n) if cols is None else np.asarray(cols)
     moduli = select_moduli(n_moduli)
-    cA, cB = capacity_bits(k, moduli)
+    cA, cB = capacity_bits(k, moduli, cmax)
     As, Bs = A[rows, :], B[:, cols]
     s = shift_exponents(As, axis=1, c=cA)
     t = shift_exponents(Bs, axis=0, c=cB)
@@ -524,7 +531,7 @@ def dgemm(A: np.ndarray, B: np.ndarray, n_moduli: int, rows=None, cols=None,
             "Bi": Bi, "r": res, "x": x, "C": C}
 
 
-def dgemm_definition(A: np.ndarray, B: np.ndarray, n_moduli: int) -> np.ndarray:
+def dgemm_definition(A: np.ndarray, B: np.ndarray, n_moduli: int, cmax: int = 53) -> np.ndarray:
     """The defined result without the residue route: C_ij =
     RN(sum_k A~_ik B~_kj 2^-(s_i+t_j)) by Python-int sums (tiny inputs)."""
     A = np.asarray(A, dtype=np.float64)
@@ -532,7 +539,7 @@ def dgemm_definition(A: np.ndarray, B: np.ndarray, n_moduli: int) -> np.ndarray:
     m, k = A.shape
     n = B.shape[1]
     moduli = select_moduli(n_moduli)
-    cA, cB = capacity_bits(k, moduli)
+    cA, cB = capacity_bits(k, moduli, cmax)
     s = shift_exponents(A, axis=1, c=cA)
     t = shift_exponents(B, axis=0, c=cB)
     Ai = to_integers_fraction(A, s, axis=1)

@@ -231,6 +231,76 @@ def test_dgemm_karatsuba_route_identical():
     assert np.array_equal(r1["C"].view(np.int64), r2["C"].view(np.int64))
 
 
+def test_greedy_moduli_beyond_twenty_keep_the_rule():
+    """The wide-range extension takes the next moduli of the same greedy rule
+    (Sec. V-A): every pick is a two-limb modulus coprime to all earlier ones,
+    and every skipped two-limb modulus between picks shares a factor with an
+    earlier pick."""
+    ms = o.select_moduli(27)
+    assert ms[:19] == o.select_moduli(19)
+    assert ms[19:] == [47, 43, 41, 31, 29, 19, 17, 11]
+    two = set(o.two_limb_moduli())
+    for i, m in enumerate(ms):
+        assert m in two
+        assert all(math.gcd(m, q) == 1 for q in ms[:i])
+    for i in range(1, len(ms)):
+        for skipped in range(ms[i] + 1, ms[i - 1]):
+            if skipped in two:
+                assert any(math.gcd(skipped, q) > 1 for q in ms[:i]), skipped
+    # 42-bit CRT chunks stay exact: R (2^42 - 1) < 2^53 with R = sum (m - 1)
+    assert sum(m - 1 for m in ms) * ((1 << 42) - 1) < (1 << 53)
+    assert o.moduli_product(ms).bit_length() <= 4 * 42
+
+
+def test_wide_capacity_closed_form():
+    """c_A = min(cmax, ceil(b/2)), c_B = min(cmax, b - c_A) with b the largest
+    integer such that 2 k 2^b < P; 23 moduli at k = 32768 give c = 63."""
+    for L, k in ((23, 32768), (24, 131072), (21, 4096), (19, 32768)):
+        ms = o.select_moduli(L)
+        P = o.moduli_product(ms)
+        for cmax in (53, 58, 63):
+            cA, cB = o.capacity_bits(k, ms, cmax)
+            b = max(bb for bb in range(400) if 2 * k * (1 << bb) < P)
+            assert (cA, cB) == (min(cmax, (b + 1) // 2), min(cmax, b - min(cmax, (b + 1) // 2)))
+            assert k * (1 << (cA + cB)) * 2 < P
+    assert o.capacity_bits(32768, o.select_moduli(23), 63) == (63, 63)
+    assert o.capacity_bits(32768, o.select_moduli(23)) == (53, 53)
+    with pytest.raises(ValueError):
+        o.capacity_bits(100, o.select_moduli(19), 64)
+
+
+def test_wide_capacity_tiny_matrices_against_definition():
+    """Brute force with c up to 63: the residue route equals the exact
+    definition (Python-int sums of the converted operands, one rounding)."""
+    rng = np.random.default_rng(17)
+    for trial in range(6):
+        m, n, k = 3, 4, 5 + trial
+        A = (rng.random((m, k)) - 0.5) * np.exp2(rng.integers(-40, 40, size=(m, k)))
+        B = (rng.random((k, n)) - 0.5) * np.exp2(rng.integers(-40, 40, size=(k, n)))
+        for L in (21, 23, 25):
+            got = o.dgemm(A, B, L, cmax=63, check_definition=True)
+            assert max(got["cA"], got["cB"]) > 53
+            want = o.dgemm_definition(A, B, L, cmax=63)
+            assert np.array_equal(got["C"].view(np.int64), want.view(np.int64))
+
+
+def test_wide_capacity_is_more_accurate_at_phi_4():
+    """With rows spanning many binades (phi = 4) the 53-bit cap truncates the
+    small elements; 63 bits with 23 moduli cut the normalized error by at
+    least 2^8 on a sample."""
+    from paper_2608_06812_amd.workloads import dgemm_inputs
+    A, B = dgemm_inputs(6, 6, 2048, 4.0, 404)
+    e53 = e63 = 0.0
+    c53 = o.dgemm(A, B, 19)["C"]
+    c63 = o.dgemm(A, B, 23, cmax=63)["C"]
+    for i in range(6):
+        for j in range(6):
+            e53 = max(e53, o.normalized_error(c53[i, j], A, B, i, j))
+            e63 = max(e63, o.normalized_error(c63[i, j], A, B, i, j))
+    assert e63 * 2 ** 8 <= e53
+    assert e63 < 2.0 ** -40
+
+
 def test_best_18_set_below_printed_bound(paper):
     """Branch and bound over pairwise-coprime 18-subsets of the two-limb
     moduli: the best product is below 2^117.80 and below 2^121, so L = 19 is
