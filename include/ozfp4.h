@@ -35,14 +35,14 @@ extern "C" {
 /* Error codes. */
 #define OZFP4_OK           0
 #define OZFP4_EINVAL      -1  /* bad size, leading dimension or null pointer      */
-#define OZFP4_EMODULI     -2  /* n_moduli outside [2, 20], or too few moduli for k */
+#define OZFP4_EMODULI     -2  /* n_moduli outside [2, 27], or too few moduli for k */
 #define OZFP4_EKBOUND     -3  /* k above the FP32-exactness bound                  */
 #define OZFP4_ENONFINITE  -4  /* NaN or Inf in A or B; C is unspecified            */
 #define OZFP4_ENOMEM      -5  /* device workspace allocation failed                */
 #define OZFP4_EHIP        -6  /* a HIP runtime call failed                         */
 
 #define OZFP4_MIN_MODULI   2
-#define OZFP4_MAX_MODULI  20
+#define OZFP4_MAX_MODULI  27
 /* With greedy limbs |c| <= 8 every prefix of the three residue accumulators
  * (the cross term holds two products per k) is a multiple of 1/4 of
  * magnitude <= 2^22, exact in FP32, for k <= 131072 (Lemma 2, Lemma 3). */
@@ -62,15 +62,17 @@ extern "C" {
  * B~_kj likewise with one shift per column of B (Sec. IV-B). The shifts put
  * each row (column) maximum into [2^(c-1), 2^c] with capacities c_A, c_B
  * chosen from k and the moduli: b is the largest integer with
- * 2 k 2^b < P = prod m_l (Eq. (crt)), c_A = min(53, ceil(b/2)),
- * c_B = min(53, b - c_A); an all-zero row or column has shift 0. The
+ * 2 k 2^b < P = prod m_l (Eq. (crt)), c_A = min(cmax, ceil(b/2)),
+ * c_B = min(cmax, b - c_A), with cmax = 53 (the paper's rule) unless
+ * ozfp4_set_max_capacity raised it; an all-zero row or column has shift 0. The
  * integer product is exact; the only roundings are the conversion and one
  * final round-to-nearest-even (subnormal results and overflow to +-inf
  * included).
  *
- * n_moduli: number L of moduli, 2..20; the moduli are the first L of the
+ * n_moduli: number L of moduli, 2..27; the moduli are the first L of the
  *   greedy pairwise-coprime list 169, 115, 113, 112, ..., 53 (Sec. V-A),
- *   with 47 as the 20th. The paper uses L = 19.
+ *   continued by the same rule with 47, 43, 41, 31, 29, 19, 17, 11. The
+ *   paper uses L = 19.
  * Returns OZFP4_EMODULI when L moduli cannot hold k (b < 2), OZFP4_EKBOUND
  * for k > OZFP4_MAX_K, OZFP4_ENONFINITE if A or B holds NaN/Inf.
  * k == 0 writes zeros to C; m == 0 or n == 0 does nothing.
@@ -114,6 +116,19 @@ int ozfp4_set_stream(void* stream);
  */
 int ozfp4_set_karatsuba(int enable);
 
+/*
+ * ozfp4_set_max_capacity -- the cap cmax on the capacities c_A, c_B of
+ * subsequent ozfp4_dgemm calls and hooks, 53..63 (default 53, the paper's
+ * rule: converted integers are exact FP64 values below 2^53). Above 53 the
+ * converted value A 2^s is still an exact double (an integer once it
+ * reaches 2^53) below 2^63, and elements far below their row's maximum keep
+ * up to cmax - 53 more bits; with enough moduli (e.g. 23 for k = 32768)
+ * this cuts the error of rows that span many binades by up to 2^(cmax-53).
+ * The result is still one rounding of the exact integer product. Returns
+ * OZFP4_EINVAL outside 53..63. A process-wide setting, like the stream.
+ */
+int ozfp4_set_max_capacity(int bits);
+
 /* Releases every device workspace and table of the library. */
 int ozfp4_finalize(void);
 
@@ -127,7 +142,7 @@ const char* ozfp4_strerror(int code);
 int ozfp4_moduli(int n_moduli, int32_t* out);
 
 /* Capacities (c_A, c_B) used for inner dimension k with n_moduli moduli
- * (see ozfp4_dgemm). HOST pointers. */
+ * and the current capacity cap (see ozfp4_dgemm). HOST pointers. */
 int ozfp4_capacity(int64_t k, int n_moduli, int32_t* c_a, int32_t* c_b);
 
 /* Canonical two-limb split of every residue r in [0, m_l) of modulus l

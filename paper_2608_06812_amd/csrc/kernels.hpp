@@ -145,6 +145,10 @@ __global__ void k_shifts(const uint64_t* __restrict__ amax, int64_t lines, int c
 //   table over [-m, 2m) that maps every estimate to the codes of its class.
 //   Adding 2^52 plus the table's byte offset to E r gives a double in
 //   [2^52, 2^53) whose low 32 bits are the LDS byte address of the entry.
+//   kWide (capacity above 53 bits): x = A 2^s is an exact double below
+//   2^63; the same floor step first brings E x down to an exact E d with
+//   |d| < 2^15 (the quotient is within 2^8 of floor(x / m), and the FMA's
+//   result is representable, so exact), and the step above then runs on d.
 constexpr int kEncWaves = 4;
 
 template <typename T>
@@ -153,7 +157,7 @@ __device__ __forceinline__ uint32_t lut_lookup(double y) {
   return *reinterpret_cast<__attribute__((address_space(3))) const T*>((size_t)addr);
 }
 
-template <bool kKar>
+template <bool kKar, bool kWide>
 __global__ __launch_bounds__(256) void k_encode_dgemm(
     const double* __restrict__ X, int64_t rs, int64_t ks, int64_t lines, int64_t k,
     const uint64_t* __restrict__ amax, int cap, uint8_t* __restrict__ planes,
@@ -194,9 +198,9 @@ __global__ __launch_bounds__(256) void k_encode_dgemm(
 #pragma unroll
     for (int e = 0; e < 32; ++e) {
       const double t = __builtin_rint(__builtin_ldexp(xe[e], s));
-      // finite inputs give |t| <= 2^53; NaN/Inf (reported by the scale
-      // stage) must not drive the table address out of range
-      xe[e] = (__builtin_fabs(t) <= 0x1p53) ? kE * t : 0.0;
+      // finite inputs give |t| <= 2^53 (2^63 when wide); NaN/Inf (reported
+      // by the scale stage) must not drive the table address out of range
+      xe[e] = (__builtin_fabs(t) <= (kWide ? 0x1p63 : 0x1p53)) ? kE * t : 0.0;
     }
     uint8_t* out = planes + f * kFragBytes + lane * 16;
     for (int l = 0; l < L; ++l) {
@@ -212,10 +216,15 @@ __global__ __launch_bounds__(256) void k_encode_dgemm(
 #pragma unroll
         for (int h = 0; h < 4; ++h) {
           const int e = g * 8 + h * 2;
-          const double q0 = __builtin_floor(xe[e] * inv);
-          const double q1 = __builtin_floor(xe[e + 1] * inv);
-          const uint32_t E0 = lut_lookup<Entry>(__builtin_fma(-q0, mE, xe[e]) + base);
-          const uint32_t E1 = lut_lookup<Entry>(__builtin_fma(-q1, mE, xe[e + 1]) + base);
+          double x0 = xe[e], x1 = xe[e + 1];
+          if constexpr (kWide) {
+            x0 = __builtin_fma(-__builtin_floor(x0 * inv), mE, x0);
+            x1 = __builtin_fma(-__builtin_floor(x1 * inv), mE, x1);
+          }
+          const double q0 = __builtin_floor(x0 * inv);
+          const double q1 = __builtin_floor(x1 * inv);
+          const uint32_t E0 = lut_lookup<Entry>(__builtin_fma(-q0, mE, x0) + base);
+          const uint32_t E1 = lut_lookup<Entry>(__builtin_fma(-q1, mE, x1) + base);
           // byte 0: plane-0 byte, byte 1: plane-1 byte (byte 2: sum plane)
           p[h] = E0 | (E1 << 4);
         }

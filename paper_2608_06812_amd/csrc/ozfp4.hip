@@ -39,6 +39,7 @@ DeviceState g_dev[kMaxDevices];
 hipStream_t g_stream = nullptr;
 bool g_profile = false;
 bool g_karatsuba = false;
+int g_cmax = 53;             // capacity cap: 53 (the paper's rule) .. 63
 double g_stage_ms[kMaxStages];
 int g_nstages = 0;
 int g_pending_stages = 0;   // events recorded by the last profiled call
@@ -131,7 +132,7 @@ int make_dgemm_plan(int64_t m, int64_t n, int64_t k, int L, DgemmPlan* p) {
   const HostTables* T = tables();
   if (!T) return OZFP4_EHIP;
   p->m = m; p->n = n; p->k = k; p->L = L;
-  if (!capacity_split(T->P[L], k, &p->cA, &p->cB)) return OZFP4_EMODULI;
+  if (!capacity_split(T->P[L], k, g_cmax, &p->cA, &p->cB)) return OZFP4_EMODULI;
   p->m_pad = round_up(m, kTile);
   p->n_pad = round_up(n, kTile);
   p->k_pad = std::max<int64_t>(kMinKPad, round_up(k, kStageK));
@@ -199,13 +200,17 @@ int run_dgemm(const DgemmPlan& p, DeviceState* d, const double* A, int64_t lda, 
   const void* lut = p.kar ? static_cast<const void*>(d->d_lut_k) : static_cast<const void*>(d->d_lut);
   const int64_t nfa = (p.m_pad / kFragLines) * p.kblocks;
   const int64_t nfb = (p.n_pad / kFragLines) * p.kblocks;
-  auto encode = p.kar ? k_encode_dgemm<true> : k_encode_dgemm<false>;
-  hipLaunchKernelGGL(encode, dim3(encode_grid(nfa)), dim3(256), lut_bytes, g_stream, A,
+  // an operand whose capacity exceeds 53 bits takes the wide encoder
+  auto pick = [&](int c) {
+    if (p.kar) return c > 53 ? k_encode_dgemm<true, true> : k_encode_dgemm<true, false>;
+    return c > 53 ? k_encode_dgemm<false, true> : k_encode_dgemm<false, false>;
+  };
+  hipLaunchKernelGGL(pick(p.cA), dim3(encode_grid(nfa)), dim3(256), lut_bytes, g_stream, A,
                      (int64_t)1, lda, p.m, p.k, amax_a, p.cA, pa, p.plane_a, nfa, p.kblocks, L,
                      d->d_mod, lut, lut_entries);
   HIP_TRY(hipGetLastError());
   record(d, 2);
-  hipLaunchKernelGGL(encode, dim3(encode_grid(nfb)), dim3(256), lut_bytes, g_stream, B,
+  hipLaunchKernelGGL(pick(p.cB), dim3(encode_grid(nfb)), dim3(256), lut_bytes, g_stream, B,
                      ldb, (int64_t)1, p.n, p.k, amax_b, p.cB, pb, p.plane_b, nfb, p.kblocks, L,
                      d->d_mod, lut, lut_entries);
   HIP_TRY(hipGetLastError());
@@ -392,7 +397,7 @@ int ozfp4_capacity(int64_t k, int n_moduli, int32_t* c_a, int32_t* c_b) {
   const HostTables* T = tables();
   if (!T) return OZFP4_EHIP;
   int a, b;
-  if (!capacity_split(T->P[n_moduli], k, &a, &b)) return OZFP4_EMODULI;
+  if (!capacity_split(T->P[n_moduli], k, g_cmax, &a, &b)) return OZFP4_EMODULI;
   *c_a = a;
   *c_b = b;
   return OZFP4_OK;
@@ -429,6 +434,12 @@ int ozfp4_sum_limb_table(int modulus_index, uint8_t* out, int32_t* m_out) {
 
 int ozfp4_set_karatsuba(int enable) {
   g_karatsuba = enable != 0;
+  return OZFP4_OK;
+}
+
+int ozfp4_set_max_capacity(int bits) {
+  if (bits < 53 || bits > 63) return OZFP4_EINVAL;
+  g_cmax = bits;
   return OZFP4_OK;
 }
 

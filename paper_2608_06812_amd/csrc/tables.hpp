@@ -21,7 +21,7 @@
 
 namespace ozfp4 {
 
-constexpr int kMaxModuli = 20;
+constexpr int kMaxModuli = 27;   // the greedy list: the printed 19, then 47, 43, 41, 31, 29, 19, 17, 11
 
 // ---- minimal unsigned multiword integer (little-endian 32-bit words) ----
 struct Big {
@@ -199,11 +199,11 @@ struct ModConst {
   double md[kMaxModuli];     // m as double
 };
 
-// Chunk width of the exact FP64 CRT sums. With R = sum (m_l - 1) <= 1799
-// for up to 20 moduli, R (2^42 - 1) < 2^53, so every chunk sum
+// Chunk width of the exact FP64 CRT sums. With R = sum (m_l - 1) <= 1983
+// for up to 27 moduli, R (2^42 - 1) < 2^53, so every chunk sum
 // sum r_l w_l,c, every q P_c with q <= R, and every carry-normalised chunk
 // is an integer below 2^53 and exact in FP64. Three chunks (126 bits) cover
-// P for up to 19 moduli (P < 2^124), four for 20.
+// P for up to 19 moduli (P < 2^124), four (168 bits) up to 27 (P < 2^162).
 constexpr int kCrtChunkBits = 42;
 inline int crt_chunks(int L) { return L <= 19 ? 3 : 4; }
 
@@ -220,7 +220,7 @@ struct CrtConst {
 struct HostTables {
   std::vector<int> moduli;                 // 20, greedy order
   ModConst mod;
-  CrtConst crt[kMaxModuli + 1];            // index L (2..20)
+  CrtConst crt[kMaxModuli + 1];            // index L (2..27)
   std::vector<uint16_t> lut;               // encoder LUT, all 20 moduli
   std::vector<uint32_t> lut_k;             // encoder LUT of the Karatsuba mode
   int nk[kMaxModuli + 1];                  // Karatsuba moduli among the first L
@@ -321,9 +321,10 @@ inline bool build_tables(HostTables& T) {
   return true;
 }
 
-// Largest b with 2 k 2^b < P (Eq. (crt)) and the split c_A = min(53,
-// ceil(b/2)), c_B = min(53, b - c_A) (Sec. IV-B). Returns false if b < 2.
-inline bool capacity_split(const Big& P, int64_t k, int* cA, int* cB) {
+// Largest b with 2 k 2^b < P (Eq. (crt)) and the split c_A = min(cmax,
+// ceil(b/2)), c_B = min(cmax, b - c_A) (Sec. IV-B); cmax = 53 is the
+// paper's rule, up to 63 the wide-range extension. Returns false if b < 2.
+inline bool capacity_split(const Big& P, int64_t k, int cmax, int* cA, int* cB) {
   if (k < 1) return false;
   // 2 k 2^b < P  <=>  2^(b+1) <= floor((P - 1) / k)
   Big q = P;
@@ -331,9 +332,9 @@ inline bool capacity_split(const Big& P, int64_t k, int* cA, int* cB) {
   q.div_small((uint32_t)k);
   int b = q.bitlen() - 2;
   if (b < 2) return false;
-  int a = std::min(53, (b + 1) / 2);
+  int a = std::min(cmax, (b + 1) / 2);
   *cA = a;
-  *cB = std::min(53, b - a);
+  *cB = std::min(cmax, b - a);
   return true;
 }
 

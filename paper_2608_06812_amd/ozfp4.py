@@ -28,7 +28,7 @@ OZFP4_ENONFINITE = -4
 OZFP4_ENOMEM = -5
 OZFP4_EHIP = -6
 OZFP4_MIN_MODULI = 2
-OZFP4_MAX_MODULI = 20
+OZFP4_MAX_MODULI = 27
 OZFP4_MAX_K = 131072
 OZFP4_MAX_K_S8 = 87381
 
@@ -47,6 +47,7 @@ _SIGNATURES = {
     "ozfp4_sum_limb_table": (_int, [_int, _p, _p]),
     "ozfp4_plane_count": (_int, [_int, _p, _p]),
     "ozfp4_set_karatsuba": (_int, [_int]),
+    "ozfp4_set_max_capacity": (_int, [_int]),
     "ozfp4_plane_layout": (_int, [_i64, _i64, _p, _p, _p]),
     "ozfp4_scales": (_int, [_i64, _i64, _i64, _p, _i64, _p, _i64, _int, _p, _p]),
     "ozfp4_limb_planes": (_int, [_i64, _i64, _i64, _p, _i64, _p, _i64, _int, _p, _p]),
@@ -134,6 +135,10 @@ def ozfp4_plane_count(n_moduli: int) -> tuple[int, list[int]]:
 
 def ozfp4_set_karatsuba(enable: bool) -> int:
     return load().ozfp4_set_karatsuba(1 if enable else 0)
+
+
+def ozfp4_set_max_capacity(bits: int) -> int:
+    return load().ozfp4_set_max_capacity(bits)
 
 
 def ozfp4_plane_layout(lines: int, k: int) -> tuple[int, int, int]:

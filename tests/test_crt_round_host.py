@@ -70,7 +70,7 @@ def _cases(L, rng):
     return [(x, e2, [x % m for m in ms]) for x, e2 in xs]
 
 
-@pytest.mark.parametrize("L", [2, 9, 14, 17, 18, 19, 20])
+@pytest.mark.parametrize("L", [2, 9, 14, 17, 18, 19, 20, 23, 27])
 def test_crt_round_matches_exact_rational(crt_bin, L):
     rng = random.Random(1000 + L)
     cases = _cases(L, rng)

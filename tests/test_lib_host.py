@@ -34,7 +34,8 @@ def test_header_declares_the_boundary():
     names = _declared_symbols()
     for required in ("ozfp4_dgemm", "ozfp4_igemm_s8", "ozfp4_set_stream", "ozfp4_finalize",
                      "ozfp4_strerror", "ozfp4_scales", "ozfp4_limb_planes", "ozfp4_residues",
-                     "ozfp4_sum_limb_table", "ozfp4_plane_count", "ozfp4_set_karatsuba"):
+                     "ozfp4_sum_limb_table", "ozfp4_plane_count", "ozfp4_set_karatsuba",
+                     "ozfp4_set_max_capacity"):
         assert required in names
 
 
@@ -49,24 +50,33 @@ def test_library_exports_every_declared_symbol(lib):
 def test_moduli_match_oracle_and_paper(lib, paper):
     assert ozfp4.ozfp4_moduli(19) == paper["moduli_L19"]
     assert ozfp4.ozfp4_moduli(20) == o.select_moduli(20)
+    assert ozfp4.ozfp4_moduli(27) == o.select_moduli(27)
 
 
 def test_capacity_matches_oracle(lib):
-    for L in range(2, 21):
-        ms = o.select_moduli(L)
-        for k in (1, 2, 3, 100, 256, 4096, 8192, 16384, 32768, 65536, 131072):
-            try:
-                want = o.capacity_bits(k, ms)
-            except ValueError:
-                with pytest.raises(ozfp4.OzFP4Error) as ei:
-                    ozfp4.ozfp4_capacity(k, L)
-                assert ei.value.code == ozfp4.OZFP4_EMODULI
-                continue
-            assert ozfp4.ozfp4_capacity(k, L) == want, (k, L)
+    try:
+        for cmax in (53, 58, 63):
+            assert ozfp4.ozfp4_set_max_capacity(cmax) == ozfp4.OZFP4_OK
+            for L in range(2, 28):
+                ms = o.select_moduli(L)
+                for k in (1, 2, 3, 100, 256, 4096, 8192, 16384, 32768, 65536, 131072):
+                    try:
+                        want = o.capacity_bits(k, ms, cmax)
+                    except ValueError:
+                        with pytest.raises(ozfp4.OzFP4Error) as ei:
+                            ozfp4.ozfp4_capacity(k, L)
+                        assert ei.value.code == ozfp4.OZFP4_EMODULI
+                        continue
+                    assert ozfp4.ozfp4_capacity(k, L) == want, (k, L, cmax)
+    finally:
+        ozfp4.ozfp4_set_max_capacity(53)
+    assert ozfp4.ozfp4_set_max_capacity(52) == ozfp4.OZFP4_EINVAL
+    assert ozfp4.ozfp4_set_max_capacity(64) == ozfp4.OZFP4_EINVAL
+    assert ozfp4.ozfp4_capacity(32768, 23) == (53, 53)
 
 
 def test_two_limb_tables_match_oracle(lib):
-    for idx, m in enumerate(o.select_moduli(20)):
+    for idx, m in enumerate(o.select_moduli(27)):
         got_m, table = ozfp4.ozfp4_two_limb_table(idx)
         assert got_m == m
         for r in range(m):
@@ -75,7 +85,7 @@ def test_two_limb_tables_match_oracle(lib):
 
 
 def test_sum_limb_tables_match_oracle(lib):
-    ms = o.select_moduli(20)
+    ms = o.select_moduli(27)
     kset = o.karatsuba_moduli(ms)
     for idx, m in enumerate(ms):
         if m not in kset:
@@ -91,11 +101,11 @@ def test_sum_limb_tables_match_oracle(lib):
 
 
 def test_plane_count_in_both_modes(lib):
-    ms = o.select_moduli(20)
+    ms = o.select_moduli(27)
     try:
         for mode in (False, True):
             ozfp4.ozfp4_set_karatsuba(mode)
-            for L in range(2, 21):
+            for L in range(2, 28):
                 sub = ms[:L]
                 ks = o.karatsuba_moduli(sub) if mode else []
                 n, idx = ozfp4.ozfp4_plane_count(L)
@@ -130,7 +140,7 @@ def test_strerror(lib):
     ((4, 4, 4, 0, 4, 1, 4, 1, 4, 19), ozfp4.OZFP4_EINVAL),           # null A
     ((4, 4, 4, 1, 4, 0, 4, 1, 4, 19), ozfp4.OZFP4_EINVAL),           # null B
     ((4, 4, 4, 1, 4, 1, 4, 1, 4, 1), ozfp4.OZFP4_EMODULI),           # too few moduli
-    ((4, 4, 4, 1, 4, 1, 4, 1, 4, 21), ozfp4.OZFP4_EMODULI),          # too many moduli
+    ((4, 4, 4, 1, 4, 1, 4, 1, 4, 28), ozfp4.OZFP4_EMODULI),          # too many moduli
     ((4, 4, 131073, 1, 4, 1, 131073, 1, 4, 19), ozfp4.OZFP4_EKBOUND),
     ((4, 4, 65536, 1, 4, 1, 65536, 1, 4, 2), ozfp4.OZFP4_EMODULI),   # P too small for k
 ])
