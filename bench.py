@@ -12,6 +12,7 @@ matrix product on the same GPU and the INT8-on-FP4 path as context.
 
 Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--moduli L]
                        [--size N] [--sweep] [--no-cpu-baseline] [--no-native] [--no-karatsuba]
+                       [--no-phi4]
 """
 
 from __future__ import annotations
@@ -149,6 +150,8 @@ def main() -> int:
     ap.add_argument("--no-native", action="store_true")
     ap.add_argument("--no-int8", action="store_true")
     ap.add_argument("--no-accuracy", action="store_true")
+    ap.add_argument("--no-phi4", action="store_true",
+                    help="skip the phi = 4 workload (8192 x 8192 x 32768) at both capacity caps")
     ap.add_argument("--no-karatsuba", action="store_true",
                     help="skip timing the three-product Karatsuba mode (comparison only)")
     ap.add_argument("--copy-calibration", action="store_true",
@@ -333,6 +336,34 @@ def main() -> int:
                           "tops": 2.0 * 8192 ** 3 / ims / 1e9,
                           "gemm_ms": gms, "fp4_tflops_gemm": 9 * 2.0 * 8192 ** 3 / gms / 1e9,
                           "fp4_frac": 9 * 2.0 * 8192 ** 3 / gms / 1e9 / FP4_PEAK_TFLOPS}
+
+    if not args.no_phi4:
+        # the wide-dynamic-range workload: the paper's 53-bit cap with 19
+        # moduli, and the wide-range extension (63 bits, 23 moduli)
+        log("phi = 4 workload 8192 x 8192 x 32768")
+        Ad = Bd = C = None
+        torch.cuda.empty_cache()
+        M4, K4 = 8192, 32768
+        A4, B4 = dgemm_inputs(M4, M4, K4, 4.0, SEED + 4)
+        A4d, B4d = dev_cm(A4, torch), dev_cm(B4, torch)
+        C4 = torch.empty_strided((M4, M4), (1, M4), dtype=torch.float64, device="cuda")
+        rows4 = np.arange(0, M4, M4 // 64)[:64]
+        ref4 = exact_reference(A4, B4, rows4, rows4)
+        runs = []
+        for L4, cmax in ((19, 53), (23, 63)):
+            ozfp4.ozfp4_set_max_capacity(cmax)
+            try:
+                ms4, st4 = time_dgemm(ozfp4, torch, A4d, B4d, C4, L4, 3, 1)
+            finally:
+                ozfp4.ozfp4_set_max_capacity(53)
+            bits4, worst4 = accuracy_bits(block_of(C4, rows4, rows4, torch), ref4)
+            runs.append({"n_moduli": L4, "max_capacity": cmax, "ms": ms4,
+                         "tflops": 2.0 * M4 * M4 * K4 / ms4 / 1e9, "gemm_ms": st4[3],
+                         "error_bits": bits4, "max_normalized_error": worst4})
+            log(json.dumps(runs[-1]))
+        result["phi4"] = {"workload": "dgemm m=n=8192, k=32768, phi=4",
+                          "block": "64x64 (every 128th row and column)", "runs": runs}
+        del A4d, B4d, C4
 
     if not args.no_cpu_baseline:
         log("timing the CPU oracle on a sample")
