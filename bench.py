@@ -35,21 +35,34 @@ METRIC = "emulated DGEMM TFLOPS at N=16384 + % of FP4 MFMA peak, 1xMI355X"
 
 # HBM bytes per launch of the residue GEMM at m = n = k = 16384, 18 moduli,
 # from rocprofv3 FETCH_SIZE / WRITE_SIZE runs scaled by a 1 GiB copy
-# (profiles/k_gemm_res_dgemm_16384_L18.md). Valid only for the kernel source
-# they were taken on, identified by its hash.
+# (profiles/k_gemm_res_dgemm_16384_L18.md). Valid only for the GEMM source
+# they were taken on, identified by the hash of its section of kernels.hpp.
 MEASURED_TRAFFIC = {
-    "kernel_source_sha256_16": "aee5735df3c17835",
+    "kernel_source_sha256_16": "df7fdb5db9a7f81d",
     "workload": (16384, 16384, 16384, 18),
-    "read_GB": 154.6, "write_GB": 4.88,
+    "read_GB": 154.6, "write_GB": 4.87,
 }
 SEED = 20260806
 
 
+GEMM_SOURCES = (  # (file, first line of the section, first line after it)
+    ("device_common.hpp", "// ------------------------------------------------------------ Sec. VI-D", None),
+    ("kernels.hpp", "// The residue GEMM over all moduli", "// INT8 variant (Sec. III)"),
+)
+
+
 def kernel_source_hash() -> str:
+    """sha256 (16 hex digits) of the residue GEMM's source: the tile mapping,
+    the MFMA and LDS-DMA helpers and the block tiles (device_common.hpp), and
+    the kernel itself (kernels.hpp)."""
     import hashlib
-    path = os.path.join(ROOT, "paper_2608_06812_amd", "csrc", "kernels.hpp")
-    with open(path, "rb") as f:
-        return hashlib.sha256(f.read()).hexdigest()[:16]
+    h = hashlib.sha256()
+    for name, start, end in GEMM_SOURCES:
+        with open(os.path.join(ROOT, "paper_2608_06812_amd", "csrc", name), encoding="utf-8") as f:
+            text = f.read()
+        a = text.index(start)
+        h.update(text[a:text.index(end) if end else len(text)].encode())
+    return h.hexdigest()[:16]
 
 
 def log(msg: str) -> None:

@@ -173,8 +173,9 @@ int ozfp4_sum_limb_table(int modulus_index, uint8_t* out, int32_t* m_out);
 int ozfp4_plane_count(int n_moduli, int32_t* n_planes, int32_t* sum_plane);
 
 /* Layout of the packed FP4 limb planes (the debug hook below returns them):
- * lines (rows of A, columns of B) are padded to rows_pad, k to k_pad, and
- * one plane holds rows_pad * k_pad / 2 bytes. */
+ * lines (rows of A, columns of B) are padded to rows_pad (a multiple of 256)
+ * and k to k_pad (a multiple of 128, at least 384); one plane holds
+ * rows_pad * k_pad / 2 bytes. */
 int ozfp4_plane_layout(int64_t lines, int64_t k, int64_t* rows_pad,
                        int64_t* k_pad, int64_t* bytes_per_plane);
 

@@ -12,9 +12,12 @@ import sys
 HERE = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(HERE)
 LIB = os.path.join(HERE, "libozfp4.so")
-SOURCES = [os.path.join(HERE, "csrc", "ozfp4.hip")]
-HEADERS = [os.path.join(HERE, "csrc", "kernels.hpp"), os.path.join(HERE, "csrc", "tables.hpp"),
-           os.path.join(ROOT, "include", "ozfp4.h")]
+# two translation units: the API with the default kernels, and the Karatsuba
+# mode's kernels (kept apart so they cannot change the default kernels' code)
+SOURCES = [os.path.join(HERE, "csrc", "ozfp4.hip"), os.path.join(HERE, "csrc", "karatsuba.hip")]
+HEADERS = [os.path.join(HERE, "csrc", n) for n in
+           ("device_common.hpp", "kernels.hpp", "karatsuba.hpp", "crt_round.hpp", "tables.hpp")] + \
+          [os.path.join(ROOT, "include", "ozfp4.h")]
 
 # -packed-fp32-ops: keep the compiler from emitting packed FP32 arithmetic.
 FLAGS = [

@@ -1,57 +1,13 @@
-// gfx950 kernels of the Ozaki-II-on-FP4 path. Included by ozfp4.hip only.
-//
-// Data layout (HBM):
-//   * limb planes: per operand, plane p holds one limb of one modulus for
-//     every (line, k); it is a sequence of 1 KiB fragments of 32 lines x 64 k
-//     in the exact register order of the A/B operand of
-//     v_mfma_scale_f32_32x32x64_f8f6f4 in FP4 mode (lane = line % 32 +
-//     32 * (k / 32 % 2), 16 bytes per lane, two E2M1 codes per byte, low
-//     nibble first). A wave therefore moves a fragment with one 16-byte
-//     load per lane, coalesced in HBM and conflict-free in LDS. Fragments
-//     of one 32-line block are contiguous along k.
-//   * residues: one byte per (modulus, i, j), column-major per modulus with
-//     the padded row count as leading dimension.
+// gfx950 kernels of the default path: line maxima and shifts, the INT8
+// encoder, the residue GEMM, the INT8 GEMM and the CRT. Included by
+// ozfp4.hip only (the Karatsuba kernels live in karatsuba.hip, a separate
+// translation unit, so that their code cannot change how the compiler
+// schedules these).
 #pragma once
 
-#include <hip/hip_runtime.h>
-#include <stdint.h>
-
-#include <type_traits>
-
-#include "crt_round.hpp"
-#include "tables.hpp"
+#include "device_common.hpp"
 
 namespace ozfp4 {
-
-typedef int v4i __attribute__((ext_vector_type(4)));
-typedef int v8i __attribute__((ext_vector_type(8)));
-typedef float v16f __attribute__((ext_vector_type(16)));
-
-constexpr int kFragLines = 32;   // lines per fragment
-constexpr int kFragK = 64;       // k per fragment
-constexpr int kFragBytes = 1024;
-constexpr int kTile = 256;       // line padding of every operand (multiple of both GEMM block tiles)
-constexpr int kStageK = 128;     // k per pipeline stage (two fragments)
-constexpr int kMinKPad = 384;    // k is padded to at least three stages
-
-constexpr uint64_t kAbsMask = 0x7fffffffffffffffull;
-constexpr uint64_t kNonFinite = 0x7ff0000000000000ull;
-
-// ------------------------------------------------------------ Sec. IV-B
-// floor(log2 |x|) from the bit pattern of the line maximum |x| (finite,
-// nonzero), subnormals included; shift c - 1 - e, or 0 for a zero line.
-__device__ __forceinline__ int line_shift(uint64_t amax_bits, int cap) {
-  if (amax_bits == 0) return 0;
-  int ex = (int)(amax_bits >> 52);
-  int e;
-  if (ex == 0) {
-    uint64_t mant = amax_bits & 0x000fffffffffffffull;
-    e = (63 - __clzll((long long)mant)) - 1074;
-  } else {
-    e = ex - 1023;
-  }
-  return cap - 1 - e;
-}
 
 __global__ void k_fill_u64(uint64_t* __restrict__ p, int64_t n, uint64_t v) {
   int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
@@ -130,133 +86,6 @@ __global__ void k_shifts(const uint64_t* __restrict__ amax, int64_t lines, int c
   if (i < lines) out[i] = line_shift(amax[i], cap);
 }
 
-// ------------------------------------------------------------ Sec. V-A / VI-B
-// Fused integer conversion, residues for every modulus, two-limb split and
-// E2M1 packing. One wave per fragment (32 lines x 64 k); lane
-// (line % 32, k half) converts its 32 values once, then for each modulus
-// reduces them, looks the codes up in an LDS table and stores 16 bytes to
-// each plane of that modulus: c0 (plane 2l), c1 (plane 2l + 1) and, in the
-// Karatsuba mode (kKar) for a Karatsuba modulus, c0 + c1 (plane
-// 2L + ksum).
-//   x = round_half_even(X * 2^s), |x| <= 2^53, is exact in FP64 and kept as
-//   E x, E = the table entry size in bytes (2, or 4 in the Karatsuba mode).
-//   For each m, q = floor(E x * fl(1/m) / E) is within one of floor(x / m),
-//   so E r = E x - q E m (exact FMA) has r in [-m, 2m), and r indexes a
-//   table over [-m, 2m) that maps every estimate to the codes of its class.
-//   Adding 2^52 plus the table's byte offset to E r gives a double in
-//   [2^52, 2^53) whose low 32 bits are the LDS byte address of the entry.
-//   kWide (capacity above 53 bits): x = A 2^s is an exact double below
-//   2^63; the same floor step first brings E x down to an exact E d with
-//   |d| < 2^15 (the quotient is within 2^8 of floor(x / m), and the FMA's
-//   result is representable, so exact), and the step above then runs on d.
-constexpr int kEncWaves = 4;
-
-template <typename T>
-__device__ __forceinline__ uint32_t lut_lookup(double y) {
-  const uint32_t addr = (uint32_t)__double_as_longlong(y);
-  return *reinterpret_cast<__attribute__((address_space(3))) const T*>((size_t)addr);
-}
-
-template <bool kKar, bool kWide>
-__global__ __launch_bounds__(256) void k_encode_dgemm(
-    const double* __restrict__ X, int64_t rs, int64_t ks, int64_t lines, int64_t k,
-    const uint64_t* __restrict__ amax, int cap, uint8_t* __restrict__ planes,
-    int64_t plane_bytes, int64_t nfrag, int64_t kblocks, int L,
-    const ModConst* __restrict__ mc, const void* __restrict__ lut, int lut_entries) {
-  typedef typename std::conditional<kKar, uint32_t, uint16_t>::type Entry;
-  constexpr double kE = (double)sizeof(Entry);
-  extern __shared__ __attribute__((aligned(16))) uint8_t s_raw[];
-  Entry* s_lut = reinterpret_cast<Entry*>(s_raw);
-  const Entry* g_lut = reinterpret_cast<const Entry*>(lut);
-  for (int i = threadIdx.x; i < lut_entries; i += 256) s_lut[i] = g_lut[i];
-  __syncthreads();
-  const uint32_t lds_base = (uint32_t)(size_t)(__attribute__((address_space(3))) uint8_t*)s_raw;
-  const int lane = threadIdx.x & 63;
-  const int wave = threadIdx.x >> 6;
-  for (int64_t f = (int64_t)blockIdx.x * kEncWaves + wave; f < nfrag;
-       f += (int64_t)gridDim.x * kEncWaves) {
-    const int64_t rb = f / kblocks, kb = f - rb * kblocks;
-    const int64_t line = rb * kFragLines + (lane & 31);
-    const int64_t kbase = kb * kFragK + (lane >> 5) * 32;
-    const bool live = line < lines;
-    const int s = live ? line_shift(amax[line], cap) : 0;
-    double xe[32];
-    const double* src = X + (live ? line : 0) * rs + kbase * ks;
-    if (live && kbase + 32 <= k) {
-#pragma unroll
-      for (int e = 0; e < 32; ++e) {
-        xe[e] = *src;
-        src += ks;
-      }
-    } else {
-#pragma unroll
-      for (int e = 0; e < 32; ++e) {
-        xe[e] = (live && kbase + e < k) ? *src : 0.0;
-        src += ks;
-      }
-    }
-#pragma unroll
-    for (int e = 0; e < 32; ++e) {
-      const double t = __builtin_rint(__builtin_ldexp(xe[e], s));
-      // finite inputs give |t| <= 2^53 (2^63 when wide); NaN/Inf (reported
-      // by the scale stage) must not drive the table address out of range
-      xe[e] = (__builtin_fabs(t) <= (kWide ? 0x1p63 : 0x1p53)) ? kE * t : 0.0;
-    }
-    uint8_t* out = planes + f * kFragBytes + lane * 16;
-    for (int l = 0; l < L; ++l) {
-      const int m = mc->m[l];
-      const double inv = mc->inv[l] / kE;
-      const double mE = kE * mc->md[l];
-      const double base =
-          0x1p52 + (double)(lds_base + (uint32_t)kE * (uint32_t)(mc->lut_off[l] + m));
-      uint32_t w0[4], w1[4], w2[4];
-#pragma unroll
-      for (int g = 0; g < 4; ++g) {
-        uint32_t p[4];
-#pragma unroll
-        for (int h = 0; h < 4; ++h) {
-          const int e = g * 8 + h * 2;
-          double x0 = xe[e], x1 = xe[e + 1];
-          if constexpr (kWide) {
-            x0 = __builtin_fma(-__builtin_floor(x0 * inv), mE, x0);
-            x1 = __builtin_fma(-__builtin_floor(x1 * inv), mE, x1);
-          }
-          const double q0 = __builtin_floor(x0 * inv);
-          const double q1 = __builtin_floor(x1 * inv);
-          const uint32_t E0 = lut_lookup<Entry>(__builtin_fma(-q0, mE, x0) + base);
-          const uint32_t E1 = lut_lookup<Entry>(__builtin_fma(-q1, mE, x1) + base);
-          // byte 0: plane-0 byte, byte 1: plane-1 byte (byte 2: sum plane)
-          p[h] = E0 | (E1 << 4);
-        }
-        if constexpr (!kKar) {
-          const uint32_t u = p[0] | (p[1] << 16), v = p[2] | (p[3] << 16);
-          w0[g] = __builtin_amdgcn_perm(v, u, 0x06040200u);
-          w1[g] = __builtin_amdgcn_perm(v, u, 0x07050301u);
-        } else {
-          const uint32_t t01 = __builtin_amdgcn_perm(p[1], p[0], 0x05010400u);
-          const uint32_t t23 = __builtin_amdgcn_perm(p[3], p[2], 0x05010400u);
-          w0[g] = __builtin_amdgcn_perm(t23, t01, 0x05040100u);
-          w1[g] = __builtin_amdgcn_perm(t23, t01, 0x07060302u);
-          const uint32_t s01 = __builtin_amdgcn_perm(p[1], p[0], 0x00000602u);
-          const uint32_t s23 = __builtin_amdgcn_perm(p[3], p[2], 0x00000602u);
-          w2[g] = __builtin_amdgcn_perm(s23, s01, 0x05040100u);
-        }
-      }
-      const v4i p0 = {(int)w0[0], (int)w0[1], (int)w0[2], (int)w0[3]};
-      const v4i p1 = {(int)w1[0], (int)w1[1], (int)w1[2], (int)w1[3]};
-      *reinterpret_cast<v4i*>(out + (int64_t)(2 * l) * plane_bytes) = p0;
-      *reinterpret_cast<v4i*>(out + (int64_t)(2 * l + 1) * plane_bytes) = p1;
-      if constexpr (kKar) {
-        const int ksum = mc->ksum[l];
-        if (ksum >= 0) {
-          const v4i p2 = {(int)w2[0], (int)w2[1], (int)w2[2], (int)w2[3]};
-          *reinterpret_cast<v4i*>(out + (int64_t)(2 * L + ksum) * plane_bytes) = p2;
-        }
-      }
-    }
-  }
-}
-
 // INT8 encoder (Sec. III): three greedy limbs per value from a 256-entry
 // table (codes of c0, c1, c2 in bits 0-3, 4-7, 8-11), three planes.
 __global__ __launch_bounds__(256) void k_encode_s8(
@@ -301,437 +130,18 @@ __global__ __launch_bounds__(256) void k_encode_s8(
   }
 }
 
-// ------------------------------------------------------------ Sec. VI-D
-// Block tile index -> (modulus, tile row, tile column). Consecutive block
-// ids go to the 8 XCDs round-robin. When the tile count T of one modulus is
-// a multiple of 8, XCD x takes tiles [x T/8, (x+1) T/8) of every modulus in
-// turn: every XCD then carries the same mix of moduli, the blocks an XCD
-// runs together share the A and B panels of one modulus in its L2, and all
-// XCDs stream the same B panels at about the same time. Otherwise each XCD
-// takes a contiguous range of the flattened (modulus, tile) order. Tiles
-// are ordered in groups of kGroupM tile rows.
-#ifndef OZFP4_GROUP_M
-#define OZFP4_GROUP_M 4
-#endif
-constexpr int kGroupM = OZFP4_GROUP_M;
-__device__ __forceinline__ void tile_coords(int64_t bid, int64_t nblocks, int64_t tiles_m,
-                                            int64_t tiles_n, int* l, int64_t* tm, int64_t* tn) {
-  const int64_t xcd = bid & 7, local = bid >> 3;
-  const int64_t T = tiles_m * tiles_n;
-  int64_t t;
-  if ((T & 7) == 0) {
-    const int64_t per = T >> 3;
-    *l = (int)(local / per);
-    t = xcd * per + (local - (int64_t)(*l) * per);
-  } else {
-    const int64_t base = nblocks >> 3, rem = nblocks & 7;
-    const int64_t logical = xcd * base + min(xcd, rem) + local;
-    *l = (int)(logical / T);
-    t = logical - (int64_t)(*l) * T;
-  }
-  const int64_t group = t / (kGroupM * tiles_n);
-  const int64_t first = group * kGroupM;
-  const int64_t gm = min(tiles_m - first, (int64_t)kGroupM);
-  const int64_t in = t - group * kGroupM * tiles_n;
-  *tm = first + in % gm;
-  *tn = in / gm;
-}
-
-__device__ __forceinline__ v16f mfma_fp4(v4i a, v4i b, v16f c) {
-  v8i a8 = {a.x, a.y, a.z, a.w, 0, 0, 0, 0};
-  v8i b8 = {b.x, b.y, b.z, b.w, 0, 0, 0, 0};
-  // cbsz = blgp = 4: both operands E2M1; E8M0 scales 127 = 2^0
-  return __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(a8, b8, c, 4, 4, 0, 127, 0, 127);
-}
-
-// Fused limb-product GEMM over a 128 x 128 block tile, k in stages of 128.
-// NP planes per operand; product (i, j) of plane i of A and plane j of B is
-// accumulated into accumulator acc_index(i, j). Four waves, each 64 x 64
-// (2 x 2 MFMA tiles of 32 x 32). LDS holds two stages (double buffer);
-// global -> register -> LDS staging, one stage ahead.
-//   LDS stage layout: [operand][plane][32-line block 0..3][k fragment 0..1]
-//   x 1 KiB.
-template <int NP>
-struct StageLayout {
-  static constexpr int kBytes = 2 * NP * 4 * 2 * kFragBytes;
-  static constexpr int kChunks = kBytes / 16;            // 16-byte pieces
-  static constexpr int kPerThread = kChunks / 256;       // 4 * NP
-  __device__ static constexpr int frag(int op, int p, int rbl, int kbl) {
-    return (((op * NP + p) * 4 + rbl) * 2 + kbl) * kFragBytes;
-  }
-};
-
-// LDS DMA: each lane copies 16 bytes from global memory to LDS at
-// lds_base + 16 * lane (global_load_lds_dwordx4); lds_base must be
-// wave-uniform. Completion is tracked by vmcnt like any vector load.
-__device__ __forceinline__ void dma16(const uint8_t* gsrc, uint8_t* lds_base) {
-  __builtin_amdgcn_global_load_lds(gsrc, (__attribute__((address_space(3))) void*)lds_base, 16, 0, 0);
-}
-
-// s_waitcnt vmcnt(N) lgkmcnt(0) (expcnt untouched): this wave's vector
-// loads except the newest N have landed, and its LDS reads are complete.
-template <int N>
-__device__ __forceinline__ void wait_vm_lgkm0() {
-  static_assert(N >= 0 && N < 64, "vmcnt range");
-  __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4));
-}
-
-__device__ __forceinline__ void block_sync() {
-  asm volatile("" ::: "memory");
-  __builtin_amdgcn_s_barrier();
-  asm volatile("" ::: "memory");
-}
-
-// Dgemm residue GEMM: planes 2l (c0) and 2l+1 (c1) of modulus l;
-// accumulators acc0 = a0 b0, acc1 = a0 b1 + a1 b0, acc2 = a1 b1; epilogue
-// r = (4 acc0 + 52 acc1 + 676 acc2) mod m, one byte per element.
-//
-// Block tile 256 (lines of A) x 128 (lines of B), k in stages of 128. Eight
-// waves, two per SIMD, each 64 x 64 (2 x 2 MFMA tiles of 32 x 32, three
-// accumulator sets = 192 registers, everything within 256 registers so two
-// waves share a SIMD and cover each other's LDS and barrier waits). A stage
-// is 48 fragments (A: 2 planes x 8 line blocks x 2 k fragments, then B:
-// 2 planes x 4 line blocks x 2 k fragments), 48 KiB, copied into a 3-slot
-// LDS ring by LDS DMA (6 whole fragments per wave, each 1 KiB contiguous in
-// HBM), up to three stages ahead of the one being multiplied.
-constexpr int kTileM = 256;        // lines of A per block
-constexpr int kTileN = 128;        // lines of B per block
-constexpr int kRing = 3;           // LDS slots
-constexpr int kWaves = 8;
-constexpr int kStageFrags = 48;
-constexpr int kStageBytes = kStageFrags * kFragBytes;
-constexpr int kDmaPerWave = kStageFrags / kWaves;   // 6
-
-// LDS offset of fragment (plane p, line block rb / cb, k fragment kbl)
-__device__ __forceinline__ constexpr int fragA(int p, int rb, int kbl) { return ((p * 8 + rb) * 2 + kbl) * kFragBytes; }
-__device__ __forceinline__ constexpr int fragB(int p, int cb, int kbl) { return (32 + (p * 4 + cb) * 2 + kbl) * kFragBytes; }
-
-// Epilogue of a block tile: r = (W0 acc0 + W1 acc1 + W2 acc2) mod m for the
-// wave's 64 x 64 outputs, one byte per element, four rows per 32-bit store.
-// The accumulators hold exact multiples of 1/4 (Lemma 3), the FP64 sum is
-// exact, and floor(d fl(1/m)) is within one of floor(d / m).
-template <int W0, int W1, int W2>
-__device__ __forceinline__ void store_residues(const v16f (&acc)[3][2][2], int l, int64_t tm,
-                                               int64_t tn, int wm, int wn, int lane,
-                                               uint8_t* __restrict__ R, int64_t ldr,
-                                               int64_t rplane, const ModConst* __restrict__ mc) {
-  const int m = mc->m[l];
-  const double inv = mc->inv[l], md = mc->md[l];
-  uint8_t* Rl = R + (int64_t)l * rplane;
-#pragma unroll
-  for (int i = 0; i < 2; ++i)
-#pragma unroll
-    for (int j = 0; j < 2; ++j) {
-      const int64_t col = tn * kTileN + wn * 64 + j * 32 + (lane & 31);
-#pragma unroll
-      for (int g = 0; g < 4; ++g) {
-        const int64_t row = tm * kTileM + wm * 64 + i * 32 + g * 8 + (lane >> 5) * 4;
-        uint32_t word = 0;
-#pragma unroll
-        for (int v4 = 0; v4 < 4; ++v4) {
-          const int v = g * 4 + v4;
-          double d = (double)W0 * (double)acc[0][i][j][v] + (double)W1 * (double)acc[1][i][j][v] +
-                     (double)W2 * (double)acc[2][i][j][v];
-          double qd = __builtin_floor(d * inv);
-          int r = (int)__builtin_fma(-qd, md, d);
-          r += (r < 0) ? m : 0;
-          r -= (r >= m) ? m : 0;
-          word |= (uint32_t)r << (8 * v4);
-        }
-        *reinterpret_cast<uint32_t*>(Rl + col * ldr + row) = word;
-      }
-    }
-}
-
-// One block tile of modulus l. kSkipA1B1: m = 169 = 13^2, where 169 a1 b1 is
-// 0 mod m (Sec. V-A), so the a1 b1 products are not issued (acc2 stays 0).
-template <bool kSkipA1B1>
-__device__ __forceinline__ void gemm_res_tile(
-    uint8_t* lds, int l, int64_t tm, int64_t tn, const uint8_t* __restrict__ PA,
-    const uint8_t* __restrict__ PB, uint8_t* __restrict__ R, int64_t plane_a, int64_t plane_b,
-    int64_t kblocks, int64_t ldr, int64_t rplane, const ModConst* __restrict__ mc) {
-  const int tid = threadIdx.x, lane = tid & 63;
-  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-  const int wm = wave >> 1, wn = wave & 1;
-  const int rbw = 2 * wm, cbw = 2 * wn;   // this wave's first A / B line block
-
-  // fragment f = wave * 6 + j of a stage (LDS offset f KiB): uniform base
-  const uint8_t* gsrc[kDmaPerWave];
-#pragma unroll
-  for (int j = 0; j < kDmaPerWave; ++j) {
-    const int f = wave * kDmaPerWave + j;
-    if (f < 32) {
-      const int kbl = f & 1, rb = (f >> 1) & 7, p = f >> 4;
-      gsrc[j] = PA + (int64_t)(2 * l + p) * plane_a + ((tm * 8 + rb) * kblocks + kbl) * kFragBytes;
-    } else {
-      const int g = f - 32, kbl = g & 1, cb = (g >> 1) & 3, p = g >> 3;
-      gsrc[j] = PB + (int64_t)(2 * l + p) * plane_b + ((tn * 4 + cb) * kblocks + kbl) * kFragBytes;
-    }
-  }
-  const int lane16 = lane * 16;
-  const int nst = (int)(kblocks / 2);
-  auto issue = [&](int s) {
-    uint8_t* dst = lds + (s % kRing) * kStageBytes + wave * kDmaPerWave * kFragBytes;
-#pragma unroll
-    for (int j = 0; j < kDmaPerWave; ++j)
-      dma16(gsrc[j] + (int64_t)s * 2 * kFragBytes + lane16, dst + j * kFragBytes);
-  };
-
-  v16f acc[3][2][2];
-#pragma unroll
-  for (int a = 0; a < 3; ++a)
-#pragma unroll
-    for (int i = 0; i < 2; ++i)
-#pragma unroll
-      for (int j = 0; j < 2; ++j)
-#pragma unroll
-        for (int v = 0; v < 16; ++v) acc[a][i][j][v] = 0.0f;
-
-  // Per stage: k fragment 0 (read, 16 MFMAs), k fragment 1 (read, 12
-  // MFMAs), then the stage handover: wait until stage s + 1 has landed and
-  // this wave's reads are done, barrier, refill the slot of stage s with
-  // stage s + 3, and only then issue the last 4 MFMAs of stage s, so the
-  // matrix pipe still has queued work while the waves synchronise.
-#pragma unroll
-  for (int s = 0; s < kRing; ++s) issue(s);     // nst >= kRing by padding
-  wait_vm_lgkm0<2 * kDmaPerWave>();
-  block_sync();
-
-  v4i a[2][2], b[2][2];   // [plane][i] of A, [plane][j] of B
-  auto read_frags = [&](const uint8_t* sb, int kbl) {
-#pragma unroll
-    for (int p = 0; p < 2; ++p)
-#pragma unroll
-      for (int i = 0; i < 2; ++i) {
-        a[p][i] = *reinterpret_cast<const v4i*>(sb + fragA(p, rbw + i, kbl) + lane16);
-        b[p][i] = *reinterpret_cast<const v4i*>(sb + fragB(p, cbw + i, kbl) + lane16);
-      }
-  };
-  // every product except a1 b1 (acc2), which is issued after the handover
-  auto mfma_head = [&]() {
-#pragma unroll
-    for (int i = 0; i < 2; ++i)
-#pragma unroll
-      for (int j = 0; j < 2; ++j) {
-        acc[0][i][j] = mfma_fp4(a[0][i], b[0][j], acc[0][i][j]);
-        acc[1][i][j] = mfma_fp4(a[0][i], b[1][j], acc[1][i][j]);
-      }
-#pragma unroll
-    for (int i = 0; i < 2; ++i)
-#pragma unroll
-      for (int j = 0; j < 2; ++j) acc[1][i][j] = mfma_fp4(a[1][i], b[0][j], acc[1][i][j]);
-  };
-  auto mfma_tail = [&]() {
-    if constexpr (!kSkipA1B1) {
-#pragma unroll
-      for (int i = 0; i < 2; ++i)
-#pragma unroll
-        for (int j = 0; j < 2; ++j) acc[2][i][j] = mfma_fp4(a[1][i], b[1][j], acc[2][i][j]);
-    }
-  };
-  auto stage_body = [&](int s) {   // everything of stage s before the handover
-    const uint8_t* sb = lds + (s % kRing) * kStageBytes;
-    read_frags(sb, 0);
-    mfma_head();
-    mfma_tail();
-    __builtin_amdgcn_sched_barrier(0);
-    read_frags(sb, 1);
-    mfma_head();
-    __builtin_amdgcn_sched_barrier(0);
-  };
-
-  int s = 0;
-  for (; s + kRing < nst; ++s) {   // steady state: the refill is always due
-    stage_body(s);
-    wait_vm_lgkm0<kDmaPerWave>();  // stage s + 1 landed; reads of stage s done
-    block_sync();
-    issue(s + kRing);              // refills the slot of stage s
-    mfma_tail();
-    __builtin_amdgcn_sched_barrier(0);
-  }
-  // the last three stages (k is padded to at least three stages)
-  stage_body(s);
-  wait_vm_lgkm0<kDmaPerWave>();
-  block_sync();
-  mfma_tail();
-  __builtin_amdgcn_sched_barrier(0);
-  stage_body(s + 1);
-  wait_vm_lgkm0<0>();
-  block_sync();
-  mfma_tail();
-  __builtin_amdgcn_sched_barrier(0);
-  stage_body(s + 2);
-  mfma_tail();
-
-  store_residues<4, 52, 676>(acc, l, tm, tn, wm, wn, lane, R, ldr, rplane, mc);
-}
-
-// Karatsuba moduli (Sec. V-A): three planes per operand, c0 (2l), c1
-// (2l + 1) and c0 + c1 (2L + ksum), and three products per k, P0 = a0 b0 in
-// acc0, Ps = (a0 + a1)(b0 + b1) in acc1 and P2 = a1 b1 in acc2. With the
-// MFMA's factor 1/4 on each product, r = 4 (P0 + 13 (Ps - P0 - P2) + 169 P2)
-// = -48 P0 + 52 Ps + 624 P2 (mod m). Same block tile and waves as above; k
-// in stages of 64, 36 fragments (A: 3 planes x 8 line blocks, then B: 3
-// planes x 4 line blocks), in a 4-slot ring of 36 KiB that waves 0..5 fill
-// with 6 fragments each, up to four stages ahead.
-constexpr int kRingK = 4;
-constexpr int kStageFragsK = 36;
-constexpr int kStageBytesK = kStageFragsK * kFragBytes;
-constexpr int kDmaWavesK = kStageFragsK / kDmaPerWave;   // 6
-static_assert(kRingK * kStageBytesK <= kRing * kStageBytes, "Karatsuba ring exceeds the LDS array");
-__device__ __forceinline__ constexpr int fragAK(int p, int rb) { return (p * 8 + rb) * kFragBytes; }
-__device__ __forceinline__ constexpr int fragBK(int p, int cb) { return (24 + p * 4 + cb) * kFragBytes; }
-
-__device__ __forceinline__ void gemm_res_tile_k(
-    uint8_t* lds, int l, int L, int64_t tm, int64_t tn, const uint8_t* __restrict__ PA,
-    const uint8_t* __restrict__ PB, uint8_t* __restrict__ R, int64_t plane_a, int64_t plane_b,
-    int64_t kblocks, int64_t ldr, int64_t rplane, const ModConst* __restrict__ mc) {
-  const int tid = threadIdx.x, lane = tid & 63;
-  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-  const int wm = wave >> 1, wn = wave & 1;
-  const int rbw = 2 * wm, cbw = 2 * wn;
-  const int psum = 2 * L + mc->ksum[l];
-
-  // fragment f = wave * 6 + j of a stage (LDS offset f KiB), waves 0..5
-  const uint8_t* gsrc[kDmaPerWave];
-#pragma unroll
-  for (int j = 0; j < kDmaPerWave; ++j) {
-    const int f = wave * kDmaPerWave + j;
-    if (f < 24) {
-      const int p = f >> 3, rb = f & 7;
-      const int plane = p < 2 ? 2 * l + p : psum;
-      gsrc[j] = PA + (int64_t)plane * plane_a + (tm * 8 + rb) * kblocks * kFragBytes;
-    } else {
-      const int g = f < 36 ? f - 24 : 0, p = g >> 2, cb = g & 3;
-      const int plane = p < 2 ? 2 * l + p : psum;
-      gsrc[j] = PB + (int64_t)plane * plane_b + (tn * 4 + cb) * kblocks * kFragBytes;
-    }
-  }
-  const bool dma_wave = wave < kDmaWavesK;
-  const int lane16 = lane * 16;
-  const int nst = (int)kblocks;
-  auto issue = [&](int s) {
-    if (dma_wave) {
-      uint8_t* dst = lds + (s & (kRingK - 1)) * kStageBytesK + wave * kDmaPerWave * kFragBytes;
-#pragma unroll
-      for (int j = 0; j < kDmaPerWave; ++j)
-        dma16(gsrc[j] + (int64_t)s * kFragBytes + lane16, dst + j * kFragBytes);
-    }
-  };
-
-  v16f acc[3][2][2];
-#pragma unroll
-  for (int a = 0; a < 3; ++a)
-#pragma unroll
-    for (int i = 0; i < 2; ++i)
-#pragma unroll
-      for (int j = 0; j < 2; ++j)
-#pragma unroll
-        for (int v = 0; v < 16; ++v) acc[a][i][j][v] = 0.0f;
-
-  // Per stage: P0 (4 MFMAs), read the sum fragments, P2 (4), the handover
-  // (wait for stage s + 1 and this wave's reads, barrier, refill the slot of
-  // stage s with stage s + 4), Ps (4), read c0 / c1 fragments of stage s + 1.
-#pragma unroll
-  for (int s = 0; s < kRingK; ++s) issue(s);   // nst >= 6 > kRingK by padding
-  wait_vm_lgkm0<(kRingK - 1) * kDmaPerWave>();
-  block_sync();
-
-  v4i a0[2], a1[2], b0[2], b1[2], as[2], bs[2];
-  auto slot = [&](int s) { return lds + (s & (kRingK - 1)) * kStageBytesK; };
-  auto read_lo = [&](const uint8_t* sb) {
-#pragma unroll
-    for (int i = 0; i < 2; ++i) {
-      a0[i] = *reinterpret_cast<const v4i*>(sb + fragAK(0, rbw + i) + lane16);
-      b0[i] = *reinterpret_cast<const v4i*>(sb + fragBK(0, cbw + i) + lane16);
-      a1[i] = *reinterpret_cast<const v4i*>(sb + fragAK(1, rbw + i) + lane16);
-      b1[i] = *reinterpret_cast<const v4i*>(sb + fragBK(1, cbw + i) + lane16);
-    }
-  };
-  auto read_sum = [&](const uint8_t* sb) {
-#pragma unroll
-    for (int i = 0; i < 2; ++i) {
-      as[i] = *reinterpret_cast<const v4i*>(sb + fragAK(2, rbw + i) + lane16);
-      bs[i] = *reinterpret_cast<const v4i*>(sb + fragBK(2, cbw + i) + lane16);
-    }
-  };
-  auto mfma_p0 = [&]() {
-#pragma unroll
-    for (int i = 0; i < 2; ++i)
-#pragma unroll
-      for (int j = 0; j < 2; ++j) acc[0][i][j] = mfma_fp4(a0[i], b0[j], acc[0][i][j]);
-  };
-  auto mfma_p2 = [&]() {
-#pragma unroll
-    for (int i = 0; i < 2; ++i)
-#pragma unroll
-      for (int j = 0; j < 2; ++j) acc[2][i][j] = mfma_fp4(a1[i], b1[j], acc[2][i][j]);
-  };
-  auto mfma_ps = [&]() {
-#pragma unroll
-    for (int i = 0; i < 2; ++i)
-#pragma unroll
-      for (int j = 0; j < 2; ++j) acc[1][i][j] = mfma_fp4(as[i], bs[j], acc[1][i][j]);
-  };
-  auto head = [&](int s) {   // stage s up to the handover
-    mfma_p0();
-    read_sum(slot(s));
-    mfma_p2();
-    __builtin_amdgcn_sched_barrier(0);
-  };
-
-  read_lo(slot(0));
-  int s = 0;
-  for (; s + kRingK < nst; ++s) {   // steady state: the refill is always due
-    head(s);
-    wait_vm_lgkm0<(kRingK - 2) * kDmaPerWave>();   // stage s + 1 landed; reads done
-    block_sync();
-    issue(s + kRingK);
-    __builtin_amdgcn_sched_barrier(0);
-    mfma_ps();
-    read_lo(slot(s + 1));
-    __builtin_amdgcn_sched_barrier(0);
-  }
-  // the last four stages
-  head(s);
-  wait_vm_lgkm0<2 * kDmaPerWave>();
-  block_sync();
-  mfma_ps();
-  read_lo(slot(s + 1));
-  __builtin_amdgcn_sched_barrier(0);
-  head(s + 1);
-  wait_vm_lgkm0<kDmaPerWave>();
-  block_sync();
-  mfma_ps();
-  read_lo(slot(s + 2));
-  __builtin_amdgcn_sched_barrier(0);
-  head(s + 2);
-  wait_vm_lgkm0<0>();
-  block_sync();
-  mfma_ps();
-  read_lo(slot(s + 3));
-  __builtin_amdgcn_sched_barrier(0);
-  head(s + 3);
-  mfma_ps();
-
-  store_residues<-48, 52, 624>(acc, l, tm, tn, wm, wn, lane, R, ldr, rplane, mc);
-}
-
-// kKar: the Karatsuba mode, where the Karatsuba moduli take the
-// three-product tile; a separate kernel, so the default kernel is unchanged.
-template <bool kKar>
+// The residue GEMM over all moduli (Sec. VI-D): one block tile of one
+// modulus per block, 169 without its a1 b1 products.
 __global__ __launch_bounds__(512, 1) void k_gemm_res(
     const uint8_t* __restrict__ PA, const uint8_t* __restrict__ PB, uint8_t* __restrict__ R,
     int64_t plane_a, int64_t plane_b, int64_t kblocks, int64_t tiles_m, int64_t tiles_n,
-    int64_t nblocks, int64_t ldr, int64_t rplane, const ModConst* __restrict__ mc, int L) {
+    int64_t nblocks, int64_t ldr, int64_t rplane, const ModConst* __restrict__ mc) {
   __shared__ __attribute__((aligned(1024))) uint8_t lds[kRing * kStageBytes];
   int l;
   int64_t tm, tn;
   tile_coords(blockIdx.x, nblocks, tiles_m, tiles_n, &l, &tm, &tn);
   if (mc->m[l] == 169)
     gemm_res_tile<true>(lds, l, tm, tn, PA, PB, R, plane_a, plane_b, kblocks, ldr, rplane, mc);
-  else if (kKar && mc->ksum[l] >= 0)
-    gemm_res_tile_k(lds, l, L, tm, tn, PA, PB, R, plane_a, plane_b, kblocks, ldr, rplane, mc);
   else
     gemm_res_tile<false>(lds, l, tm, tn, PA, PB, R, plane_a, plane_b, kblocks, ldr, rplane, mc);
 }

@@ -8,6 +8,7 @@
 #include <cstring>
 #include <mutex>
 
+#include "karatsuba.hpp"
 #include "kernels.hpp"
 #include "ozfp4.h"
 #include "tables.hpp"
@@ -51,6 +52,12 @@ const HostTables* tables() {
 }
 
 inline int64_t round_up(int64_t v, int64_t a) { return (v + a - 1) / a * a; }
+
+// Padded k of the limb planes: a multiple of the GEMM stage, at least
+// kMinKPad (three stages).
+inline int64_t plane_k_pad(int64_t k) {
+  return std::max<int64_t>(kMinKPad, round_up(k, kStageK));
+}
 
 #define HIP_TRY(expr)                                  \
   do {                                                 \
@@ -135,7 +142,7 @@ int make_dgemm_plan(int64_t m, int64_t n, int64_t k, int L, DgemmPlan* p) {
   if (!capacity_split(T->P[L], k, g_cmax, &p->cA, &p->cB)) return OZFP4_EMODULI;
   p->m_pad = round_up(m, kTile);
   p->n_pad = round_up(n, kTile);
-  p->k_pad = std::max<int64_t>(kMinKPad, round_up(k, kStageK));
+  p->k_pad = plane_k_pad(k);
   p->kblocks = p->k_pad / kFragK;
   p->plane_a = p->m_pad * p->k_pad / 2;
   p->plane_b = p->n_pad * p->k_pad / 2;
@@ -200,19 +207,32 @@ int run_dgemm(const DgemmPlan& p, DeviceState* d, const double* A, int64_t lda, 
   const void* lut = p.kar ? static_cast<const void*>(d->d_lut_k) : static_cast<const void*>(d->d_lut);
   const int64_t nfa = (p.m_pad / kFragLines) * p.kblocks;
   const int64_t nfb = (p.n_pad / kFragLines) * p.kblocks;
-  // an operand whose capacity exceeds 53 bits takes the wide encoder
-  auto pick = [&](int c) {
-    if (p.kar) return c > 53 ? k_encode_dgemm<true, true> : k_encode_dgemm<true, false>;
-    return c > 53 ? k_encode_dgemm<false, true> : k_encode_dgemm<false, false>;
-  };
-  hipLaunchKernelGGL(pick(p.cA), dim3(encode_grid(nfa)), dim3(256), lut_bytes, g_stream, A,
-                     (int64_t)1, lda, p.m, p.k, amax_a, p.cA, pa, p.plane_a, nfa, p.kblocks, L,
-                     d->d_mod, lut, lut_entries);
+  // an operand whose capacity exceeds 53 bits takes the wide encoder; the
+  // Karatsuba mode's encoder lives in its own translation unit
+  if (p.kar) {
+    HIP_TRY(launch_encode_kar(p.cA > 53, (unsigned)encode_grid(nfa), lut_bytes, g_stream, A,
+                              (int64_t)1, lda, p.m, p.k, amax_a, p.cA, pa, p.plane_a, nfa,
+                              p.kblocks, L, d->d_mod, lut, lut_entries));
+  } else {
+    auto enc = p.cA > 53 ? k_encode_dgemm<false, true> : k_encode_dgemm<false, false>;
+    hipLaunchKernelGGL(enc,
+                       dim3(encode_grid(nfa)), dim3(256), lut_bytes, g_stream, A, (int64_t)1, lda,
+                       p.m, p.k, amax_a, p.cA, pa, p.plane_a, nfa, p.kblocks, L, d->d_mod, lut,
+                       lut_entries);
+  }
   HIP_TRY(hipGetLastError());
   record(d, 2);
-  hipLaunchKernelGGL(pick(p.cB), dim3(encode_grid(nfb)), dim3(256), lut_bytes, g_stream, B,
-                     ldb, (int64_t)1, p.n, p.k, amax_b, p.cB, pb, p.plane_b, nfb, p.kblocks, L,
-                     d->d_mod, lut, lut_entries);
+  if (p.kar) {
+    HIP_TRY(launch_encode_kar(p.cB > 53, (unsigned)encode_grid(nfb), lut_bytes, g_stream, B, ldb,
+                              (int64_t)1, p.n, p.k, amax_b, p.cB, pb, p.plane_b, nfb, p.kblocks,
+                              L, d->d_mod, lut, lut_entries));
+  } else {
+    auto enc = p.cB > 53 ? k_encode_dgemm<false, true> : k_encode_dgemm<false, false>;
+    hipLaunchKernelGGL(enc,
+                       dim3(encode_grid(nfb)), dim3(256), lut_bytes, g_stream, B, ldb, (int64_t)1,
+                       p.n, p.k, amax_b, p.cB, pb, p.plane_b, nfb, p.kblocks, L, d->d_mod, lut,
+                       lut_entries);
+  }
   HIP_TRY(hipGetLastError());
   record(d, 3);
   if (last < 3) return OZFP4_OK;
@@ -220,10 +240,15 @@ int run_dgemm(const DgemmPlan& p, DeviceState* d, const double* A, int64_t lda, 
   // stage 3: fused residue GEMM for all moduli
   const int64_t tiles_m = p.m_pad / kTileM, tiles_n = p.n_pad / kTileN;
   const int64_t nblocks = tiles_m * tiles_n * L;
-  auto gemm = p.kar ? k_gemm_res<true> : k_gemm_res<false>;
-  hipLaunchKernelGGL(gemm, dim3((unsigned)nblocks), dim3(kWaves * 64), 0, g_stream, pa, pb, R,
-                     p.plane_a, p.plane_b, p.kblocks, tiles_m, tiles_n, nblocks, p.m_pad,
-                     p.m_pad * p.n_pad, d->d_mod, L);
+  if (p.kar) {
+    HIP_TRY(launch_gemm_res_kar((unsigned)nblocks, g_stream, pa, pb, R, p.plane_a, p.plane_b,
+                                p.kblocks, tiles_m, tiles_n, nblocks, p.m_pad, p.m_pad * p.n_pad,
+                                d->d_mod, L));
+  } else {
+    hipLaunchKernelGGL(k_gemm_res, dim3((unsigned)nblocks), dim3(kWaves * 64), 0, g_stream, pa,
+                       pb, R, p.plane_a, p.plane_b, p.kblocks, tiles_m, tiles_n, nblocks, p.m_pad,
+                       p.m_pad * p.n_pad, d->d_mod);
+  }
   HIP_TRY(hipGetLastError());
   record(d, 4);
   if (last < 4) return OZFP4_OK;
@@ -315,7 +340,7 @@ int ozfp4_igemm_s8(int64_t m, int64_t n, int64_t k, const int8_t* A, int64_t lda
   }
   if (!A || !B) return OZFP4_EINVAL;
   const int64_t m_pad = round_up(m, kTile), n_pad = round_up(n, kTile);
-  const int64_t k_pad = std::max<int64_t>(kMinKPad, round_up(k, kStageK)), kblocks = k_pad / kFragK;
+  const int64_t k_pad = plane_k_pad(k), kblocks = k_pad / kFragK;
   const int64_t plane_a = m_pad * k_pad / 2, plane_b = n_pad * k_pad / 2;
   const size_t off_pb = align256((size_t)plane_a * 3);
   rc = ensure_workspace(d, off_pb + align256((size_t)plane_b * 3));
@@ -459,7 +484,7 @@ int ozfp4_plane_layout(int64_t lines, int64_t k, int64_t* rows_pad, int64_t* k_p
                        int64_t* bytes_per_plane) {
   if (lines < 0 || k < 0 || !rows_pad || !k_pad || !bytes_per_plane) return OZFP4_EINVAL;
   *rows_pad = round_up(lines, kTile);
-  *k_pad = std::max<int64_t>(kMinKPad, round_up(k, kStageK));
+  *k_pad = plane_k_pad(k);
   *bytes_per_plane = *rows_pad * *k_pad / 2;
   return OZFP4_OK;
 }
