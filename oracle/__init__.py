@@ -1,4 +1,5 @@
-"""CPU oracle for FP64 matrix multiplication through Ozaki scheme II on base-13 E2M1 limbs.
+"""CPU oracle for FP64 matrix multiplication through Ozaki schemes II and I on
+base-13 E2M1 limbs.
 
 TEST INFRASTRUCTURE ONLY. Nothing in the product path may import, call or
 execute this package: only ``tests/``, ``__graft_entry__.smoke()`` and the
@@ -12,4 +13,8 @@ inputs. No function is "parity unpinned".
 """
 
 from .ozaki2_fp4 import *  # noqa: F401,F403
-from .ozaki2_fp4 import __all__  # noqa: F401
+from .ozaki2_fp4 import __all__ as _all2
+from .ozaki1_fp4 import *  # noqa: F401,F403
+from .ozaki1_fp4 import __all__ as _all1
+
+__all__ = list(_all2) + list(_all1)

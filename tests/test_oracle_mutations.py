@@ -156,3 +156,74 @@ def test_karatsuba_wrong_sum_plane_is_caught(monkeypatch):
     monkeypatch.setattr(mod, "limb_planes_karatsuba", bad)
     monkeypatch.setitem(_ROUTE, "karatsuba", True)
     assert _tiny_mismatch()
+
+
+# ---------------------------------------------------------------- scheme I
+
+from oracle import ozaki1_fp4 as mod1  # noqa: E402
+
+
+def _ozi_mismatch():
+    """True when the scheme-I oracle breaks one of its pins on small inputs:
+    limbs outside S, the expansion differing from the integer product, or C
+    differing from scheme II's (both at c = 53)."""
+    S = set(o.doubled_set())
+    rng = np.random.default_rng(2)
+    for _ in range(3):
+        m, n, k = 4, 3, 9
+        A = (rng.random((m, k)) - 0.5) * np.exp2(rng.integers(-20, 20, size=(m, k)))
+        B = (rng.random((k, n)) - 0.5) * np.exp2(rng.integers(-20, 20, size=(k, n)))
+        try:
+            res = o.dgemm_ozi(A, B, 15)
+        except (AssertionError, ValueError):
+            return True
+        if any(not set(np.unique(a).tolist()) <= S for a in res["a"] + res["b"]):
+            return True
+        if not np.all(res["x"] == o.exact_int_matmul(res["Ai"], res["Bi"])):
+            return True
+        if not np.array_equal(res["C"], o.dgemm(A, B, 18)["C"]):
+            return True
+    return False
+
+
+def test_unmutated_scheme1_passes():
+    assert not _ozi_mismatch()
+
+
+def test_scheme1_wrong_group_weight_is_caught(monkeypatch):
+    def bad(G):
+        x = np.zeros(G[0].shape, dtype=object)
+        for g, Gg in enumerate(G):
+            x = x + Gg.astype(object) * (13 ** (g + (1 if g == len(G) - 1 else 0)))
+        return x
+    monkeypatch.setattr(mod1, "ozi_compose", bad)
+    assert _ozi_mismatch()
+
+
+def test_scheme1_off_by_one_group_is_caught(monkeypatch):
+    def bad(a, b):
+        p, q = len(a), len(b)
+        G = []
+        for g in range(p + q - 1):
+            acc = np.zeros((a[0].shape[0], b[0].shape[1]), dtype=np.int64)
+            for i in range(p):
+                j = g - i + 1            # shifted anti-diagonal
+                if 0 <= j < q:
+                    acc = acc + mod._limb_matmul(a[i], b[j])
+            G.append(acc)
+        return G
+    monkeypatch.setattr(mod1, "ozi_group_products", bad)
+    assert _ozi_mismatch()
+
+
+def test_scheme1_missing_minus5_substitution_is_caught(monkeypatch):
+    def bad(Xi, p):
+        rest = np.asarray(Xi, dtype=np.int64).copy()
+        out = []
+        for _ in range(p):
+            c = np.mod(rest + 6, 13) - 6          # +-5 kept: not in S
+            out.append(c)
+            rest = (rest - c) // 13
+        return out
+    monkeypatch.setattr(mod1, "ozi_limbs", bad)
+    assert _ozi_mismatch()
