@@ -8,11 +8,12 @@ reconstruction. The printed JSON line carries the emulated-DGEMM rate
 2 m n k / t, the residue GEMM against the FP4 matrix-core peak (stage time
 measured with HIP events on the library's stream over the timed steps), the
 CPU oracle timed on a bounded sample, a per-stage breakdown, native FP64
-matrix product on the same GPU and the INT8-on-FP4 path as context.
+matrix product on the same GPU, Ozaki scheme I on the same limbs (checked
+bit for bit against scheme II) and the INT8-on-FP4 path as context.
 
 Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--moduli L]
                        [--size N] [--sweep] [--no-cpu-baseline] [--no-native] [--no-karatsuba]
-                       [--no-phi4]
+                       [--no-phi4] [--no-ozi]
 """
 
 from __future__ import annotations
@@ -77,14 +78,19 @@ def dev_cm(X, torch):
 def time_dgemm(ozfp4, torch, Ad, Bd, C, L, steps, warmup, profile=True):
     """Median-free protocol of the contract: W untimed calls, then K calls
     bracketed by synchronisations. Returns (ms per step, mean stage ms)."""
+    return time_call(ozfp4, torch, lambda: ozfp4.dgemm(Ad, Bd, L, out=C), steps, warmup, profile)
+
+
+def time_call(ozfp4, torch, call, steps, warmup, profile=True):
+    """time_dgemm for any library call (stage times from ozfp4_stage_times)."""
     for _ in range(warmup):
-        ozfp4.dgemm(Ad, Bd, L, out=C)
+        call()
     torch.cuda.synchronize()
     ozfp4.ozfp4_profile(profile)
     stage_sum = None
     t0 = time.perf_counter()
     for _ in range(steps):
-        ozfp4.dgemm(Ad, Bd, L, out=C)
+        call()
         if profile:
             st = ozfp4.ozfp4_stage_times()
             stage_sum = st if stage_sum is None else [a + b for a, b in zip(stage_sum, st)]
@@ -167,6 +173,8 @@ def main() -> int:
                     help="skip the phi = 4 workload (8192 x 8192 x 32768) at both capacity caps")
     ap.add_argument("--no-karatsuba", action="store_true",
                     help="skip timing the three-product Karatsuba mode (comparison only)")
+    ap.add_argument("--no-ozi", action="store_true",
+                    help="skip Ozaki scheme I (15 limbs) and its bitwise check against scheme II")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="also run a plain 1 GiB device copy (reference for HBM byte counters)")
     args = ap.parse_args()
@@ -323,6 +331,28 @@ def main() -> int:
             "c_bitwise_equal_to_default": bool(torch.equal(Cref.view(torch.int64),
                                                            C.view(torch.int64)))}
         del Cref
+
+    if not args.no_ozi:
+        # Ozaki scheme I on the same limbs (Sec. IV): 15 limbs, 225 limb
+        # products; its C is compared bit for bit with scheme II at 19
+        # moduli, where both convert with 53-bit capacities (Sec. VII-A)
+        log("scheme II with 19 moduli, then timing ozfp4_dgemm_ozi with 15 limbs")
+        C19 = torch.empty_strided((N, N), (1, N), dtype=torch.float64, device="cuda")
+        ozfp4.dgemm(Ad, Bd, 19, out=C19)
+        oms, ost = time_call(ozfp4, torch, lambda: ozfp4.dgemm_ozi(Ad, Bd, 15, out=C),
+                             max(3, args.steps // 4), 1)
+        flops_ozi = 225 * 2.0 * N ** 3
+        result["ozi"] = {
+            "workload": f"dgemm m=n=k={N}, phi=0.5, scheme I, 15 limbs", "ms": oms,
+            "tflops": 2.0 * N ** 3 / oms / 1e9, "products_per_element": 225,
+            "stages_ms": dict(zip(["scale", "encode_A", "encode_B", "limb_gemm", "reduce"], ost)),
+            "fp4_tflops_gemm": flops_ozi / ost[3] / 1e9,
+            "fp4_frac": flops_ozi / ost[3] / 1e9 / FP4_PEAK_TFLOPS,
+            "c_bitwise_equal_to_scheme2_19_moduli": bool(torch.equal(C.view(torch.int64),
+                                                                     C19.view(torch.int64)))}
+        log(json.dumps(result["ozi"]))
+        del C19
+        torch.cuda.empty_cache()
 
     if not args.no_int8:
         log("timing ozfp4_igemm_s8 8192^3")

@@ -219,16 +219,83 @@ int ozfp4_residues(int64_t m, int64_t n, int64_t k,
                    const double* A, int64_t lda, const double* B, int64_t ldb,
                    int n_moduli, uint8_t* R, int64_t ldr);
 
+/* ---- Ozaki scheme I on the same limbs ---------------------------------- */
+
+/* Largest limb count p of ozfp4_dgemm_ozi: 15 limbs hold the 53-bit FP64
+ * significand (Sec. IV-A). */
+#define OZFP4_OZI_MAX_LIMBS 15
+
+/*
+ * ozfp4_dgemm_ozi -- C = fl(A B) for FP64 A, B by Ozaki scheme I on FP4 limbs
+ * (Sec. IV): each converted value is written with p greedy base-13 limbs in
+ * S (Lemma 1), the p x p limb products <a_i, b_j> run on the FP4 matrix
+ * cores, products are summed along the anti-diagonals i + j and combined by
+ * one exact weighted sum (Eq. (expand)), then rounded once.
+ *
+ * Computes, for every (i, j),
+ *     C_ij = RN( (sum_k A~_ik B~_kj) * 2^-(s_i + t_j) )
+ * with the conversion of ozfp4_dgemm (round half to even, one shift per row
+ * of A and per column of B, all-zero lines shift 0) at the capacity
+ * c = floor(log2 min(X_p, 2^53)) for both operands, X_p = (13^p - 1) / 3
+ * (Sec. IV-B): c = 53 for p = 15. Where ozfp4_dgemm runs with
+ * c_A = c_B = 53 (19 moduli and k <= 76549, the paper's configuration),
+ * both entry points convert the inputs identically and compute the same
+ * exact integer product, so their C agree bit for bit (Sec. VII-A).
+ *
+ * n_limbs: p = 1..OZFP4_OZI_MAX_LIMBS (OZFP4_EINVAL otherwise). The
+ *   library runs limbs in blocks of three, 9 ceil(p/3)^2 limb products per
+ *   k (225 for p = 15); limbs at or above p are zero.
+ * Returns OZFP4_EKBOUND for k > OZFP4_MAX_K, OZFP4_ENONFINITE if A or B
+ * holds NaN/Inf. k == 0 writes zeros to C; m == 0 or n == 0 does nothing.
+ * Workspace: besides the limb planes, 2 ceil(p/3) - 1 int64 partial-sum
+ * planes of the padded m x n output (18 GiB for p = 15 at m = n = 16384).
+ * Synchronizes the stream before returning (it reads the non-finite flag).
+ */
+int ozfp4_dgemm_ozi(int64_t m, int64_t n, int64_t k,
+                    const double* A, int64_t lda, const double* B, int64_t ldb,
+                    double* C, int64_t ldc, int n_limbs);
+
+/* Configuration of ozfp4_dgemm_ozi for p = n_limbs (HOST outputs, each may
+ * be null): the capacity c in bits, the number of limb planes per operand
+ * (3 ceil(p/3)) and the number of partial-sum planes (2 ceil(p/3) - 1).
+ * OZFP4_EINVAL for p outside [1, OZFP4_OZI_MAX_LIMBS]. */
+int ozfp4_ozi_config(int n_limbs, int32_t* capacity, int32_t* n_planes, int32_t* n_groups);
+
+/*
+ * ozfp4_ozi_limb_planes -- the packed E2M1 limb planes ozfp4_dgemm_ozi
+ * builds (Lemma 1): plane i holds limb a_i of every converted value, in the
+ * layout of ozfp4_limb_planes (sizes from ozfp4_plane_layout), n_planes of
+ * ozfp4_ozi_config planes per operand. DEVICE outputs. Synchronizes.
+ */
+int ozfp4_ozi_limb_planes(int64_t m, int64_t n, int64_t k,
+                          const double* A, int64_t lda, const double* B, int64_t ldb,
+                          int n_limbs, uint8_t* planes_a, uint8_t* planes_b);
+
+/*
+ * ozfp4_ozi_partials -- the exact partial sums the limb GEMM writes, one
+ * plane per block anti-diagonal h < n_groups (blocks of three limbs,
+ * I + J = h):
+ *     H_h = sum_{I + J = h} sum_{i', j' < 3} 13^(i' + j') <a_{3I+i'}, b_{3J+j'}>
+ * so that sum_h 2197^h H_h is the integer product of the converted
+ * operands. DEVICE int64 output H[h * ldh * n + i + j * ldh], ldh >= m.
+ * Synchronizes.
+ */
+int ozfp4_ozi_partials(int64_t m, int64_t n, int64_t k,
+                       const double* A, int64_t lda, const double* B, int64_t ldb,
+                       int n_limbs, int64_t* H, int64_t ldh);
+
 /* ---- stage timing ------------------------------------------------------ */
 
 /* Enable (1) or disable (0) HIP-event timing of the stages of the next
- * ozfp4_dgemm / ozfp4_igemm_s8 calls, recorded on the library's stream. */
+ * ozfp4_dgemm / ozfp4_dgemm_ozi / ozfp4_igemm_s8 calls, recorded on the
+ * library's stream. */
 int ozfp4_profile(int enable);
 
 /* Milliseconds of each stage of the last profiled call, written to the HOST
  * array ms[max]; returns the stage count (>= 0) or an error. dgemm stages:
- * 0 scale, 1 encode A, 2 encode B, 3 residue GEMM, 4 CRT. igemm_s8 stages:
- * 0 encode A, 1 encode B, 2 GEMM. Synchronizes. */
+ * 0 scale, 1 encode A, 2 encode B, 3 residue GEMM, 4 CRT. dgemm_ozi stages:
+ * 0 scale, 1 encode A, 2 encode B, 3 limb GEMM, 4 reduction. igemm_s8
+ * stages: 0 encode A, 1 encode B, 2 GEMM. Synchronizes. */
 int ozfp4_stage_times(double* ms, int max, int* n_stages);
 
 #ifdef __cplusplus

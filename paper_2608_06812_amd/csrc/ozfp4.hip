@@ -10,6 +10,7 @@
 
 #include "karatsuba.hpp"
 #include "kernels.hpp"
+#include "ozaki1.hpp"
 #include "ozfp4.h"
 #include "tables.hpp"
 
@@ -268,6 +269,113 @@ int run_dgemm(const DgemmPlan& p, DeviceState* d, const double* A, int64_t lda, 
   return OZFP4_OK;
 }
 
+// ------------------------------------------------------- Ozaki scheme I
+
+// c = floor(log2 min(X_p, 2^53)) with X_p = (13^p - 1) / 3 (Sec. IV-B)
+int ozi_capacity_bits(int p) {
+  uint64_t x = 1;
+  for (int i = 0; i < p; ++i) x *= 13;
+  x = std::min<uint64_t>((x - 1) / 3, uint64_t(1) << 53);
+  return 63 - __builtin_clzll(x);
+}
+
+struct OziPlan {
+  int64_t m, n, k;
+  int p, nblk, nplanes, nh, cap;
+  int64_t m_pad, n_pad, k_pad, kblocks;
+  int64_t plane_a, plane_b;
+  size_t off_amax_a, off_amax_b, off_flag, off_pa, off_pb, off_h, total;
+};
+
+int check_ozi_args(int64_t m, int64_t n, int64_t k, const void* A, int64_t lda, const void* B,
+                   int64_t ldb, int n_limbs) {
+  if (m < 0 || n < 0 || k < 0) return OZFP4_EINVAL;
+  if (lda < std::max<int64_t>(1, m) || ldb < std::max<int64_t>(1, k)) return OZFP4_EINVAL;
+  if (n_limbs < 1 || n_limbs > OZFP4_OZI_MAX_LIMBS) return OZFP4_EINVAL;
+  if (m > 0 && n > 0 && k > 0) {
+    if (!A || !B) return OZFP4_EINVAL;
+    if (k > OZFP4_MAX_K) return OZFP4_EKBOUND;
+  }
+  return OZFP4_OK;
+}
+
+void make_ozi_plan(int64_t m, int64_t n, int64_t k, int p, OziPlan* o) {
+  o->m = m; o->n = n; o->k = k; o->p = p;
+  o->nblk = (p + 2) / 3;
+  o->nplanes = 3 * o->nblk;
+  o->nh = 2 * o->nblk - 1;
+  o->cap = ozi_capacity_bits(p);
+  o->m_pad = round_up(m, kTile);
+  o->n_pad = round_up(n, kTile);
+  o->k_pad = plane_k_pad(k);
+  o->kblocks = o->k_pad / kFragK;
+  o->plane_a = o->m_pad * o->k_pad / 2;
+  o->plane_b = o->n_pad * o->k_pad / 2;
+  size_t off = 0;
+  o->off_amax_a = off; off = align256(off + sizeof(uint64_t) * o->m_pad);
+  o->off_amax_b = off; off = align256(off + sizeof(uint64_t) * o->n_pad);
+  o->off_flag = off;   off = align256(off + 256);
+  o->off_pa = off;     off = align256(off + (size_t)o->plane_a * o->nplanes);
+  o->off_pb = off;     off = align256(off + (size_t)o->plane_b * o->nplanes);
+  o->off_h = off;      off = align256(off + sizeof(int64_t) * (size_t)o->m_pad * o->n_pad * o->nh);
+  o->total = off;
+}
+
+// Stages, stopping after `last`: 0 scale, 1 encode A, 2 encode B, 3 limb
+// GEMM into the partial-sum planes, 4 reduction into C.
+int run_ozi(const OziPlan& p, DeviceState* d, const double* A, int64_t lda, const double* B,
+            int64_t ldb, double* C, int64_t ldc, int last, uint8_t* planes_a_out,
+            uint8_t* planes_b_out) {
+  uint8_t* ws = d->ws;
+  uint64_t* amax_a = reinterpret_cast<uint64_t*>(ws + p.off_amax_a);
+  uint64_t* amax_b = reinterpret_cast<uint64_t*>(ws + p.off_amax_b);
+  int* flag = reinterpret_cast<int*>(ws + p.off_flag);
+  uint8_t* pa = planes_a_out ? planes_a_out : ws + p.off_pa;
+  uint8_t* pb = planes_b_out ? planes_b_out : ws + p.off_pb;
+  int64_t* H = reinterpret_cast<int64_t*>(ws + p.off_h);
+
+  record(d, 0);
+  const int64_t nzero = (int64_t)((p.off_flag + 256 - p.off_amax_a) / sizeof(uint64_t));
+  hipLaunchKernelGGL(k_fill_u64, dim3(blocks_for(nzero, 256)), dim3(256), 0, g_stream,
+                     amax_a, nzero, (uint64_t)0);
+  hipLaunchKernelGGL(k_amax_adjacent_lines, dim3(blocks_for(p.m, 256), blocks_for(p.k, kAmaxChunk)),
+                     dim3(256), 0, g_stream, A, lda, p.m, p.k,
+                     reinterpret_cast<unsigned long long*>(amax_a), flag);
+  hipLaunchKernelGGL(k_amax_contig_lines, dim3(blocks_for(p.n, 4), blocks_for(p.k, kAmaxContigChunk)),
+                     dim3(256), 0, g_stream, B, ldb, p.n, p.k,
+                     reinterpret_cast<unsigned long long*>(amax_b), flag);
+  HIP_TRY(hipGetLastError());
+  record(d, 1);
+  if (last < 1) return OZFP4_OK;
+
+  const int64_t nfa = (p.m_pad / kFragLines) * p.kblocks;
+  const int64_t nfb = (p.n_pad / kFragLines) * p.kblocks;
+  HIP_TRY(launch_encode_ozi((unsigned)encode_grid(nfa), g_stream, A, (int64_t)1, lda, p.m, p.k,
+                            amax_a, p.cap, pa, p.plane_a, nfa, p.kblocks, p.nplanes));
+  record(d, 2);
+  HIP_TRY(launch_encode_ozi((unsigned)encode_grid(nfb), g_stream, B, ldb, (int64_t)1, p.n, p.k,
+                            amax_b, p.cap, pb, p.plane_b, nfb, p.kblocks, p.nplanes));
+  record(d, 3);
+  if (last < 3) return OZFP4_OK;
+
+  HIP_TRY(launch_gemm_ozi(g_stream, pa, pb, H, p.plane_a, p.plane_b, p.kblocks, p.m_pad, p.n_pad,
+                          p.nblk));
+  record(d, 4);
+  if (last < 4) return OZFP4_OK;
+
+  HIP_TRY(launch_ozi_reduce(g_stream, H, p.m_pad, p.m_pad * p.n_pad, p.nh, p.m, p.n, amax_a,
+                            amax_b, p.cap, C, ldc));
+  record(d, 5);
+  return OZFP4_OK;
+}
+
+int prepare_ozi(int64_t m, int64_t n, int64_t k, int n_limbs, OziPlan* p, DeviceState** d) {
+  make_ozi_plan(m, n, k, n_limbs, p);
+  int rc = device_state(d);
+  if (rc) return rc;
+  return ensure_workspace(*d, p->total);
+}
+
 int finish_with_flag(DeviceState* d, const int* dflag, int nstages) {
   HIP_TRY(hipMemcpyAsync(d->h_flag, dflag, sizeof(int), hipMemcpyDeviceToHost, g_stream));
   HIP_TRY(hipStreamSynchronize(g_stream));
@@ -366,6 +474,77 @@ int ozfp4_igemm_s8(int64_t m, int64_t n, int64_t k, const int8_t* A, int64_t lda
     HIP_TRY(hipGetDevice(&g_pending_device));
   }
   return OZFP4_OK;
+}
+
+int ozfp4_dgemm_ozi(int64_t m, int64_t n, int64_t k, const double* A, int64_t lda,
+                    const double* B, int64_t ldb, double* C, int64_t ldc, int n_limbs) {
+  int rc = check_ozi_args(m, n, k, A, lda, B, ldb, n_limbs);
+  if (rc) return rc;
+  if (ldc < std::max<int64_t>(1, m)) return OZFP4_EINVAL;
+  if (m == 0 || n == 0) return OZFP4_OK;
+  if (!C) return OZFP4_EINVAL;
+  if (k == 0) {
+    DeviceState* d;
+    rc = device_state(&d);
+    if (rc) return rc;
+    hipLaunchKernelGGL(k_fill_f64_matrix, dim3(blocks_for(m * n, 256)), dim3(256), 0, g_stream, C,
+                       m, n, ldc);
+    HIP_TRY(hipGetLastError());
+    return OZFP4_OK;
+  }
+  OziPlan p;
+  DeviceState* d;
+  rc = prepare_ozi(m, n, k, n_limbs, &p, &d);
+  if (rc) return rc;
+  rc = run_ozi(p, d, A, lda, B, ldb, C, ldc, 4, nullptr, nullptr);
+  if (rc) return rc;
+  return finish_with_flag(d, reinterpret_cast<int*>(d->ws + p.off_flag), 5);
+}
+
+int ozfp4_ozi_config(int n_limbs, int32_t* capacity, int32_t* n_planes, int32_t* n_groups) {
+  if (n_limbs < 1 || n_limbs > OZFP4_OZI_MAX_LIMBS) return OZFP4_EINVAL;
+  const int nblk = (n_limbs + 2) / 3;
+  if (capacity) *capacity = ozi_capacity_bits(n_limbs);
+  if (n_planes) *n_planes = 3 * nblk;
+  if (n_groups) *n_groups = 2 * nblk - 1;
+  return OZFP4_OK;
+}
+
+int ozfp4_ozi_limb_planes(int64_t m, int64_t n, int64_t k, const double* A, int64_t lda,
+                          const double* B, int64_t ldb, int n_limbs, uint8_t* planes_a,
+                          uint8_t* planes_b) {
+  int rc = check_ozi_args(m, n, k, A, lda, B, ldb, n_limbs);
+  if (rc) return rc;
+  if (m == 0 || n == 0 || k == 0) return OZFP4_EINVAL;
+  if (!planes_a || !planes_b) return OZFP4_EINVAL;
+  OziPlan p;
+  DeviceState* d;
+  rc = prepare_ozi(m, n, k, n_limbs, &p, &d);
+  if (rc) return rc;
+  rc = run_ozi(p, d, A, lda, B, ldb, nullptr, 0, 2, planes_a, planes_b);
+  if (rc) return rc;
+  return finish_with_flag(d, reinterpret_cast<int*>(d->ws + p.off_flag), 0);
+}
+
+int ozfp4_ozi_partials(int64_t m, int64_t n, int64_t k, const double* A, int64_t lda,
+                       const double* B, int64_t ldb, int n_limbs, int64_t* H, int64_t ldh) {
+  int rc = check_ozi_args(m, n, k, A, lda, B, ldb, n_limbs);
+  if (rc) return rc;
+  if (m == 0 || n == 0 || k == 0) return OZFP4_EINVAL;
+  if (!H || ldh < m) return OZFP4_EINVAL;
+  OziPlan p;
+  DeviceState* d;
+  rc = prepare_ozi(m, n, k, n_limbs, &p, &d);
+  if (rc) return rc;
+  rc = run_ozi(p, d, A, lda, B, ldb, nullptr, 0, 3, nullptr, nullptr);
+  if (rc) return rc;
+  for (int h = 0; h < p.nh; ++h) {
+    HIP_TRY(hipMemcpy2DAsync(H + (size_t)h * ldh * n, (size_t)ldh * sizeof(int64_t),
+                             d->ws + p.off_h + (size_t)h * p.m_pad * p.n_pad * sizeof(int64_t),
+                             (size_t)p.m_pad * sizeof(int64_t), (size_t)m * sizeof(int64_t),
+                             (size_t)n, hipMemcpyDeviceToDevice, g_stream));
+  }
+  return finish_with_flag(d, reinterpret_cast<int*>(d->ws + p.off_flag), 0);
 }
 
 int ozfp4_set_stream(void* stream) {

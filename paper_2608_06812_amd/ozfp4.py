@@ -31,6 +31,7 @@ OZFP4_MIN_MODULI = 2
 OZFP4_MAX_MODULI = 27
 OZFP4_MAX_K = 131072
 OZFP4_MAX_K_S8 = 87381
+OZFP4_OZI_MAX_LIMBS = 15
 
 _lib = None
 
@@ -52,6 +53,10 @@ _SIGNATURES = {
     "ozfp4_scales": (_int, [_i64, _i64, _i64, _p, _i64, _p, _i64, _int, _p, _p]),
     "ozfp4_limb_planes": (_int, [_i64, _i64, _i64, _p, _i64, _p, _i64, _int, _p, _p]),
     "ozfp4_residues": (_int, [_i64, _i64, _i64, _p, _i64, _p, _i64, _int, _p, _i64]),
+    "ozfp4_dgemm_ozi": (_int, [_i64, _i64, _i64, _p, _i64, _p, _i64, _p, _i64, _int]),
+    "ozfp4_ozi_config": (_int, [_int, _p, _p, _p]),
+    "ozfp4_ozi_limb_planes": (_int, [_i64, _i64, _i64, _p, _i64, _p, _i64, _int, _p, _p]),
+    "ozfp4_ozi_partials": (_int, [_i64, _i64, _i64, _p, _i64, _p, _i64, _int, _p, _i64]),
     "ozfp4_profile": (_int, [_int]),
     "ozfp4_stage_times": (_int, [_p, _int, _p]),
 }
@@ -158,6 +163,25 @@ def ozfp4_limb_planes(m, n, k, A, lda, B, ldb, n_moduli, planes_a, planes_b) -> 
 
 def ozfp4_residues(m, n, k, A, lda, B, ldb, n_moduli, R, ldr) -> int:
     return load().ozfp4_residues(m, n, k, A, lda, B, ldb, n_moduli, R, ldr)
+
+
+def ozfp4_dgemm_ozi(m, n, k, A, lda, B, ldb, C, ldc, n_limbs) -> int:
+    return load().ozfp4_dgemm_ozi(m, n, k, A, lda, B, ldb, C, ldc, n_limbs)
+
+
+def ozfp4_ozi_config(n_limbs: int) -> tuple[int, int, int]:
+    c, npl, ng = ctypes.c_int32(), ctypes.c_int32(), ctypes.c_int32()
+    _check(load().ozfp4_ozi_config(n_limbs, ctypes.byref(c), ctypes.byref(npl), ctypes.byref(ng)),
+           "ozfp4_ozi_config")
+    return c.value, npl.value, ng.value
+
+
+def ozfp4_ozi_limb_planes(m, n, k, A, lda, B, ldb, n_limbs, planes_a, planes_b) -> int:
+    return load().ozfp4_ozi_limb_planes(m, n, k, A, lda, B, ldb, n_limbs, planes_a, planes_b)
+
+
+def ozfp4_ozi_partials(m, n, k, A, lda, B, ldb, n_limbs, H, ldh) -> int:
+    return load().ozfp4_ozi_partials(m, n, k, A, lda, B, ldb, n_limbs, H, ldh)
 
 
 def ozfp4_profile(enable: bool) -> int:
@@ -295,3 +319,59 @@ def residues(A, B, n_moduli: int = 19):
     _check(ozfp4_residues(m, n, k, A.data_ptr(), lda, B.data_ptr(), ldb, n_moduli, R.data_ptr(), m),
            "ozfp4_residues")
     return R
+
+
+def dgemm_ozi(A, B, n_limbs: int = OZFP4_OZI_MAX_LIMBS, out=None):
+    """C = fl(A B) for float64 device tensors A (m x k), B (k x n) by Ozaki
+    scheme I on FP4 limbs with n_limbs limbs per operand; returns C (m x n),
+    column-major."""
+    import torch
+    A, lda = _cm(A, torch.float64, "A")
+    B, ldb = _cm(B, torch.float64, "B")
+    m, k = A.shape
+    k2, n = B.shape
+    if k != k2:
+        raise ValueError("inner dimensions differ")
+    C = _empty_cm(m, n, torch.float64, A.device) if out is None else out
+    if C.shape != (m, n) or C.dtype != torch.float64 or (C.stride(0) != 1 and m > 1):
+        raise ValueError("out must be a column-major float64 (m x n) tensor")
+    ldc = max(1, C.stride(1) if n > 1 else m)
+    _use_torch_stream(A.device)
+    _check(ozfp4_dgemm_ozi(m, n, k, A.data_ptr(), lda, B.data_ptr(), ldb, C.data_ptr(), ldc,
+                           n_limbs), "ozfp4_dgemm_ozi")
+    return C
+
+
+def ozi_limb_planes(A, B, n_limbs: int = OZFP4_OZI_MAX_LIMBS):
+    """Scheme-I limb planes of A and B (uint8 device tensors of shape
+    (n_planes, bytes_per_plane)) in the layout of ozfp4_limb_planes."""
+    import torch
+    A, lda = _cm(A, torch.float64, "A")
+    B, ldb = _cm(B, torch.float64, "B")
+    m, k = A.shape
+    n = B.shape[1]
+    _, _, bpa = ozfp4_plane_layout(m, k)
+    _, _, bpb = ozfp4_plane_layout(n, k)
+    _, nplanes, _ = ozfp4_ozi_config(n_limbs)
+    pa = torch.empty((nplanes, bpa), dtype=torch.uint8, device=A.device)
+    pb = torch.empty((nplanes, bpb), dtype=torch.uint8, device=A.device)
+    _use_torch_stream(A.device)
+    _check(ozfp4_ozi_limb_planes(m, n, k, A.data_ptr(), lda, B.data_ptr(), ldb, n_limbs,
+                                 pa.data_ptr(), pb.data_ptr()), "ozfp4_ozi_limb_planes")
+    return pa, pb
+
+
+def ozi_partials(A, B, n_limbs: int = OZFP4_OZI_MAX_LIMBS):
+    """Partial sums of the scheme-I limb GEMM as an int64 device tensor of
+    shape (n_groups, n, m): H[h, j, i] = partial sum h of element (i, j)."""
+    import torch
+    A, lda = _cm(A, torch.float64, "A")
+    B, ldb = _cm(B, torch.float64, "B")
+    m, k = A.shape
+    n = B.shape[1]
+    _, _, ng = ozfp4_ozi_config(n_limbs)
+    H = torch.empty((ng, n, m), dtype=torch.int64, device=A.device)
+    _use_torch_stream(A.device)
+    _check(ozfp4_ozi_partials(m, n, k, A.data_ptr(), lda, B.data_ptr(), ldb, n_limbs,
+                              H.data_ptr(), m), "ozfp4_ozi_partials")
+    return H

@@ -36,7 +36,7 @@ def asm(tmp_path_factory):
         pytest.skip("no hipcc")
     out = {}
     d = tmp_path_factory.mktemp("asm")
-    for tu in ("ozfp4.hip", "karatsuba.hip"):
+    for tu in ("ozfp4.hip", "karatsuba.hip", "ozaki1.hip"):
         path = str(d / (tu + ".s"))
         subprocess.run([hipcc, *FLAGS, os.path.join(CSRC, tu), "-o", path], check=True,
                        capture_output=True)
@@ -104,6 +104,7 @@ def test_no_kernel_spills(asm):
     ("ozfp4.hip", "_ZN5ozfp410k_gemm_res", 32, 16, 6),          # residue GEMM, k = 128 stage
     ("ozfp4.hip", "_ZN5ozfp49k_gemm_s8", 36, 18, 6),            # INT8 GEMM, k = 128 stage
     ("karatsuba.hip", "_ZN5ozfp414k_gemm_res_kar", 12, 12, 6),  # Karatsuba tile, k = 64 stage
+    ("ozaki1.hip", "_ZN5ozfp410k_gemm_ozi", 36, 18, 6),         # scheme-I GEMM, k = 128 stage
 ])
 def test_gemm_steady_loop(asm, tu, prefix, mfma, reads, dma):
     body = _function(asm[tu], prefix)

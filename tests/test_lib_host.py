@@ -35,7 +35,8 @@ def test_header_declares_the_boundary():
     for required in ("ozfp4_dgemm", "ozfp4_igemm_s8", "ozfp4_set_stream", "ozfp4_finalize",
                      "ozfp4_strerror", "ozfp4_scales", "ozfp4_limb_planes", "ozfp4_residues",
                      "ozfp4_sum_limb_table", "ozfp4_plane_count", "ozfp4_set_karatsuba",
-                     "ozfp4_set_max_capacity"):
+                     "ozfp4_set_max_capacity", "ozfp4_dgemm_ozi", "ozfp4_ozi_config",
+                     "ozfp4_ozi_limb_planes", "ozfp4_ozi_partials"):
         assert required in names
 
 
@@ -166,6 +167,42 @@ def test_hook_argument_errors_on_host(lib):
     assert ozfp4.ozfp4_residues(4, 4, 4, 1, 4, 1, 4, 19, 1, 3) == ozfp4.OZFP4_EINVAL   # ldr < m
     assert ozfp4.ozfp4_scales(4, 4, 4, 1, 4, 1, 4, 19, 0, 1) == ozfp4.OZFP4_EINVAL     # null s
     assert ozfp4.ozfp4_limb_planes(4, 4, 4, 1, 4, 1, 4, 19, 1, 0) == ozfp4.OZFP4_EINVAL
+
+
+def test_ozi_config_matches_oracle(lib, paper):
+    for p in range(1, 16):
+        c, nplanes, ngroups = ozfp4.ozfp4_ozi_config(p)
+        assert c == o.ozi_capacity(p)
+        nblk = -(-p // 3)
+        assert (nplanes, ngroups) == (3 * nblk, 2 * nblk - 1)
+    assert ozfp4.ozfp4_ozi_config(paper["limb_counts"]["fp64"])[0] == 53
+    for bad in (0, 16, -1):
+        with pytest.raises(ozfp4.OzFP4Error):
+            ozfp4.ozfp4_ozi_config(bad)
+
+
+@pytest.mark.parametrize("args,code", [
+    ((-1, 4, 4, 1, 4, 1, 4, 1, 4, 15), ozfp4.OZFP4_EINVAL),
+    ((4, 4, 4, 1, 3, 1, 4, 1, 4, 15), ozfp4.OZFP4_EINVAL),           # lda < m
+    ((4, 4, 4, 1, 4, 1, 3, 1, 4, 15), ozfp4.OZFP4_EINVAL),           # ldb < k
+    ((4, 4, 4, 1, 4, 1, 4, 1, 3, 15), ozfp4.OZFP4_EINVAL),           # ldc < m
+    ((4, 4, 4, 0, 4, 1, 4, 1, 4, 15), ozfp4.OZFP4_EINVAL),           # null A
+    ((4, 4, 4, 1, 4, 1, 4, 0, 4, 15), ozfp4.OZFP4_EINVAL),           # null C
+    ((4, 4, 4, 1, 4, 1, 4, 1, 4, 0), ozfp4.OZFP4_EINVAL),            # no limbs
+    ((4, 4, 4, 1, 4, 1, 4, 1, 4, 16), ozfp4.OZFP4_EINVAL),           # too many limbs
+    ((4, 4, 131073, 1, 4, 1, 131073, 1, 4, 15), ozfp4.OZFP4_EKBOUND),
+    ((0, 5, 5, 0, 1, 0, 5, 0, 1, 15), ozfp4.OZFP4_OK),               # empty: no-op
+    ((5, 0, 5, 0, 5, 0, 5, 0, 5, 15), ozfp4.OZFP4_OK),
+])
+def test_dgemm_ozi_argument_errors_on_host(lib, args, code):
+    assert ozfp4.ozfp4_dgemm_ozi(*args) == code
+
+
+def test_ozi_hook_argument_errors_on_host(lib):
+    assert ozfp4.ozfp4_ozi_partials(4, 4, 4, 1, 4, 1, 4, 15, 1, 3) == ozfp4.OZFP4_EINVAL  # ldh < m
+    assert ozfp4.ozfp4_ozi_partials(4, 4, 4, 1, 4, 1, 4, 15, 0, 4) == ozfp4.OZFP4_EINVAL  # null H
+    assert ozfp4.ozfp4_ozi_limb_planes(4, 4, 4, 1, 4, 1, 4, 15, 1, 0) == ozfp4.OZFP4_EINVAL
+    assert ozfp4.ozfp4_ozi_limb_planes(4, 4, 0, 1, 4, 1, 1, 15, 1, 1) == ozfp4.OZFP4_EINVAL  # k == 0
 
 
 def test_binding_refuses_missing_library(monkeypatch, tmp_path):
