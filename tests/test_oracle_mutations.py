@@ -227,3 +227,46 @@ def test_scheme1_missing_minus5_substitution_is_caught(monkeypatch):
         return out
     monkeypatch.setattr(mod1, "ozi_limbs", bad)
     assert _ozi_mismatch()
+
+
+# ---------------------------------------------------------------- FP32 emulation
+
+from fractions import Fraction  # noqa: E402
+
+from oracle import sgemm_fp4 as mod32  # noqa: E402
+
+
+def _f32_mismatch():
+    """True when the FP32-emulation oracle breaks a pin: the single binary32
+    rounding (a double-rounding case, a tie at the subnormal end) or the
+    residue route against the exact definition."""
+    x = ((2 ** 24 + 1) << 30) + 1
+    if o.round_scaled_f32(x, 30) != np.float32(2 ** 24 + 2):
+        return True
+    if o.round_scaled_f32(3, 150) != np.float32(2.0 ** -148):
+        return True
+    rng = np.random.default_rng(5)
+    A = ((rng.random((3, 5)) - 0.5) * np.exp2(rng.integers(-30, 30, size=(3, 5)))).astype(np.float32)
+    B = ((rng.random((5, 2)) - 0.5) * np.exp2(rng.integers(-30, 30, size=(5, 2)))).astype(np.float32)
+    try:
+        got = o.sgemm(A, B, 10)["C"]
+    except (AssertionError, ValueError):
+        return True
+    return not np.array_equal(got.view(np.uint32), o.sgemm_definition(A, B, 10).view(np.uint32))
+
+
+def test_unmutated_fp32_passes():
+    assert not _f32_mismatch()
+
+
+def test_fp32_double_rounding_is_caught(monkeypatch):
+    def bad(x, shift):
+        return np.float32(float(Fraction(int(x)) / Fraction(2) ** int(shift)))
+    monkeypatch.setattr(mod32, "round_scaled_f32", bad)
+    monkeypatch.setattr(o, "round_scaled_f32", bad)
+    assert _f32_mismatch()
+
+
+def test_fp32_capacity_53_is_caught(monkeypatch):
+    monkeypatch.setattr(mod32, "FP32_CAPACITY", 53)
+    assert _f32_mismatch() or o.capacity_bits_fp32(16384, o.select_moduli(10)) != (24, 24)
