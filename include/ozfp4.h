@@ -219,6 +219,40 @@ int ozfp4_residues(int64_t m, int64_t n, int64_t k,
                    const double* A, int64_t lda, const double* B, int64_t ldb,
                    int n_moduli, uint8_t* R, int64_t ldr);
 
+/* ---- FP32 emulation (SGEMM) --------------------------------------------- */
+
+/*
+ * ozfp4_sgemm -- C = fl32(A B) for FP32 A, B by Ozaki scheme II on FP4 limbs:
+ * the method of ozfp4_dgemm with an FP32 significand's 24 bits as the
+ * capacity cap (the paper's FP64 method applied to the FP32 significand,
+ * which Sec. IV-A sizes at 7 base-13 limbs).
+ *
+ * Computes, for every (i, j),
+ *     C_ij = RN32( (sum_k A~_ik B~_kj) * 2^-(s_i + t_j) )
+ * with A~_ik = round_half_even(A_ik 2^s_i) (the FP32 value taken exactly),
+ * one shift per row of A and per column of B (all-zero lines shift 0),
+ * capacities c_A = min(24, ceil(b/2)), c_B = min(24, b - c_A) with b the
+ * largest integer with 2 k 2^b < P (Eq. (crt)). The integer product is
+ * exact and rounded once to binary32 (never through an FP64 intermediate),
+ * subnormal results and overflow to +-inf included. 10 moduli give 24-bit
+ * capacities for k <= 16384 (39 FP4 limb products per k).
+ *
+ * n_moduli: 2..27, the moduli of ozfp4_dgemm. The residue GEMM always takes
+ *   the four-product route (ozfp4_set_karatsuba does not apply) and the
+ *   capacity cap is 24 whatever ozfp4_set_max_capacity set.
+ * Returns OZFP4_EMODULI when the moduli cannot hold k (b < 2), OZFP4_EKBOUND
+ * for k > OZFP4_MAX_K, OZFP4_ENONFINITE if A or B holds NaN/Inf.
+ * k == 0 writes zeros to C; m == 0 or n == 0 does nothing.
+ * Synchronizes the stream before returning (it reads the non-finite flag).
+ */
+int ozfp4_sgemm(int64_t m, int64_t n, int64_t k,
+                const float* A, int64_t lda, const float* B, int64_t ldb,
+                float* C, int64_t ldc, int n_moduli);
+
+/* The capacities (c_A, c_B) ozfp4_sgemm uses for this k and number of
+ * moduli (HOST outputs); OZFP4_EMODULI if the moduli cannot hold k. */
+int ozfp4_sgemm_capacity(int64_t k, int n_moduli, int32_t* c_a, int32_t* c_b);
+
 /* ---- Ozaki scheme I on the same limbs ---------------------------------- */
 
 /* Largest limb count p of ozfp4_dgemm_ozi: 15 limbs hold the 53-bit FP64
@@ -287,12 +321,13 @@ int ozfp4_ozi_partials(int64_t m, int64_t n, int64_t k,
 /* ---- stage timing ------------------------------------------------------ */
 
 /* Enable (1) or disable (0) HIP-event timing of the stages of the next
- * ozfp4_dgemm / ozfp4_dgemm_ozi / ozfp4_igemm_s8 calls, recorded on the
- * library's stream. */
+ * ozfp4_dgemm / ozfp4_sgemm / ozfp4_dgemm_ozi / ozfp4_igemm_s8 calls,
+ * recorded on the library's stream. */
 int ozfp4_profile(int enable);
 
 /* Milliseconds of each stage of the last profiled call, written to the HOST
- * array ms[max]; returns the stage count (>= 0) or an error. dgemm stages:
+ * array ms[max]; returns the stage count (>= 0) or an error. dgemm and sgemm
+ * stages:
  * 0 scale, 1 encode A, 2 encode B, 3 residue GEMM, 4 CRT. dgemm_ozi stages:
  * 0 scale, 1 encode A, 2 encode B, 3 limb GEMM, 4 reduction. igemm_s8
  * stages: 0 encode A, 1 encode B, 2 GEMM. Synchronizes. */

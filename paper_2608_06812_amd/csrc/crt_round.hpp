@@ -75,11 +75,12 @@ OZFP4_HD double round_scaled(uint64_t w0, uint64_t w1, uint64_t w2, int e2,
 
 // Exact path. x' = S - q P is assembled from the 42-bit chunk differences
 // v_c = sig_c - q P_c (exact integers below 2^53 in magnitude) as a 192-bit
-// two's-complement integer. It is mapped into the symmetric range
-// (-P/2, P/2] and RN(x 2^e2) is taken, including subnormal results and
-// overflow to infinity. s3 = 0 when three chunks are in use (then P_3 = 0).
-OZFP4_HD double crt_exact(double s0, double s1, double s2, double s3, double q,
-                                            const CrtConst* __restrict__ cc, int e2) {
+// two's-complement integer and mapped into the symmetric range (-P/2, P/2];
+// crt_symmetric returns |x| in (w0, w1, w2) and whether x < 0. s3 = 0 when
+// three chunks are in use (then P_3 = 0).
+OZFP4_HD bool crt_symmetric(double s0, double s1, double s2, double s3, double q,
+                            const CrtConst* __restrict__ cc, uint64_t* o0, uint64_t* o1,
+                            uint64_t* o2) {
   const int64_t v0 = (int64_t)__builtin_fma(-q, cc->Pc[0], s0);
   const int64_t v1 = (int64_t)__builtin_fma(-q, cc->Pc[1], s1);
   const int64_t v2 = (int64_t)__builtin_fma(-q, cc->Pc[2], s2);
@@ -117,6 +118,18 @@ OZFP4_HD double crt_exact(double s0, double s1, double s2, double s3, double q,
     w0 = n0; w1 = n1; w2 = n2;
     neg = !neg;
   }
+  *o0 = w0;
+  *o1 = w1;
+  *o2 = w2;
+  return neg;
+}
+
+// RN(x 2^e2) of the exact symmetric x, including subnormal results and
+// overflow to infinity.
+OZFP4_HD double crt_exact(double s0, double s1, double s2, double s3, double q,
+                          const CrtConst* __restrict__ cc, int e2) {
+  uint64_t w0, w1, w2;
+  const bool neg = crt_symmetric(s0, s1, s2, s3, q, cc, &w0, &w1, &w2);
   return round_scaled(w0, w1, w2, e2, neg);
 }
 

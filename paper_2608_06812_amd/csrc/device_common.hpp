@@ -58,7 +58,7 @@ __device__ __forceinline__ int line_shift(uint64_t amax_bits, int cap) {
 
 // ------------------------------------------------------------ Sec. V-A / VI-B
 // Fused integer conversion, residues for every modulus, two-limb split and
-// E2M1 packing. One wave per fragment (32 lines x 64 k); lane
+// E2M1 packing, for FP64 (or FP32, taken exactly as FP64) inputs. One wave per fragment (32 lines x 64 k); lane
 // (line % 32, k half) converts its 32 values once, then for each modulus
 // reduces them, looks the codes up in an LDS table and stores 16 bytes to
 // each plane of that modulus: c0 (plane 2l), c1 (plane 2l + 1) and, in the
@@ -83,9 +83,9 @@ __device__ __forceinline__ uint32_t lut_lookup(double y) {
   return *reinterpret_cast<__attribute__((address_space(3))) const T*>((size_t)addr);
 }
 
-template <bool kKar, bool kWide>
+template <bool kKar, bool kWide, typename TIn = double>
 __global__ __launch_bounds__(256) void k_encode_dgemm(
-    const double* __restrict__ X, int64_t rs, int64_t ks, int64_t lines, int64_t k,
+    const TIn* __restrict__ X, int64_t rs, int64_t ks, int64_t lines, int64_t k,
     const uint64_t* __restrict__ amax, int cap, uint8_t* __restrict__ planes,
     int64_t plane_bytes, int64_t nfrag, int64_t kblocks, int L,
     const ModConst* __restrict__ mc, const void* __restrict__ lut, int lut_entries) {
@@ -107,17 +107,17 @@ __global__ __launch_bounds__(256) void k_encode_dgemm(
     const bool live = line < lines;
     const int s = live ? line_shift(amax[line], cap) : 0;
     double xe[32];
-    const double* src = X + (live ? line : 0) * rs + kbase * ks;
+    const TIn* src = X + (live ? line : 0) * rs + kbase * ks;
     if (live && kbase + 32 <= k) {
 #pragma unroll
       for (int e = 0; e < 32; ++e) {
-        xe[e] = *src;
+        xe[e] = (double)*src;
         src += ks;
       }
     } else {
 #pragma unroll
       for (int e = 0; e < 32; ++e) {
-        xe[e] = (live && kbase + e < k) ? *src : 0.0;
+        xe[e] = (live && kbase + e < k) ? (double)*src : 0.0;
         src += ks;
       }
     }

@@ -11,6 +11,7 @@
 #include "karatsuba.hpp"
 #include "kernels.hpp"
 #include "ozaki1.hpp"
+#include "sgemm.hpp"
 #include "ozfp4.h"
 #include "tables.hpp"
 
@@ -117,6 +118,7 @@ struct DgemmPlan {
   int64_t m_pad, n_pad, k_pad, kblocks;
   int64_t plane_a, plane_b;  // bytes per plane
   bool kar;                  // Karatsuba mode
+  bool f32;                  // FP32 inputs and output (capacity cap 24)
   int nplanes;               // planes per operand: 2L, plus the sum planes in the Karatsuba mode
   // workspace offsets
   size_t off_amax_a, off_amax_b, off_flag, off_pa, off_pb, off_r, total;
@@ -136,18 +138,23 @@ int check_dgemm_args(int64_t m, int64_t n, int64_t k, const void* A, int64_t lda
   return OZFP4_OK;
 }
 
-int make_dgemm_plan(int64_t m, int64_t n, int64_t k, int L, DgemmPlan* p) {
+// FP32 emulation: an FP32 significand's 24 bits in place of FP64's 53
+constexpr int kFp32Capacity = 24;
+
+int make_dgemm_plan(int64_t m, int64_t n, int64_t k, int L, DgemmPlan* p, bool f32 = false) {
   const HostTables* T = tables();
   if (!T) return OZFP4_EHIP;
   p->m = m; p->n = n; p->k = k; p->L = L;
-  if (!capacity_split(T->P[L], k, g_cmax, &p->cA, &p->cB)) return OZFP4_EMODULI;
+  p->f32 = f32;
+  if (!capacity_split(T->P[L], k, f32 ? kFp32Capacity : g_cmax, &p->cA, &p->cB))
+    return OZFP4_EMODULI;
   p->m_pad = round_up(m, kTile);
   p->n_pad = round_up(n, kTile);
   p->k_pad = plane_k_pad(k);
   p->kblocks = p->k_pad / kFragK;
   p->plane_a = p->m_pad * p->k_pad / 2;
   p->plane_b = p->n_pad * p->k_pad / 2;
-  p->kar = g_karatsuba;
+  p->kar = g_karatsuba && !f32;
   p->nplanes = 2 * L + (p->kar ? T->nk[L] : 0);
   size_t off = 0;
   p->off_amax_a = off; off = align256(off + sizeof(uint64_t) * p->m_pad);
@@ -174,9 +181,14 @@ int encode_grid(int64_t nfrag) {
 
 // Stages of the dgemm pipeline, stopping after `last`:
 // 0 scale, 1 encode A, 2 encode B, 3 residue GEMM, 4 CRT.
-int run_dgemm(const DgemmPlan& p, DeviceState* d, const double* A, int64_t lda, const double* B,
-              int64_t ldb, double* C, int64_t ldc, int last, uint8_t* planes_a_out,
+// A, B and C are double, or float when p.f32.
+int run_dgemm(const DgemmPlan& p, DeviceState* d, const void* Av, int64_t lda, const void* Bv,
+              int64_t ldb, void* Cv, int64_t ldc, int last, uint8_t* planes_a_out,
               uint8_t* planes_b_out) {
+  const double* A = static_cast<const double*>(Av);
+  const double* B = static_cast<const double*>(Bv);
+  const float* Af = static_cast<const float*>(Av);
+  const float* Bf = static_cast<const float*>(Bv);
   const HostTables* T = tables();
   uint8_t* ws = d->ws;
   uint64_t* amax_a = reinterpret_cast<uint64_t*>(ws + p.off_amax_a);
@@ -192,12 +204,16 @@ int run_dgemm(const DgemmPlan& p, DeviceState* d, const double* A, int64_t lda, 
   const int64_t nzero = (int64_t)((p.off_flag + 256 - p.off_amax_a) / sizeof(uint64_t));
   hipLaunchKernelGGL(k_fill_u64, dim3(blocks_for(nzero, 256)), dim3(256), 0, g_stream,
                      amax_a, nzero, (uint64_t)0);
-  hipLaunchKernelGGL(k_amax_adjacent_lines, dim3(blocks_for(p.m, 256), blocks_for(p.k, kAmaxChunk)),
-                     dim3(256), 0, g_stream, A, lda, p.m, p.k,
-                     reinterpret_cast<unsigned long long*>(amax_a), flag);
-  hipLaunchKernelGGL(k_amax_contig_lines, dim3(blocks_for(p.n, 4), blocks_for(p.k, kAmaxContigChunk)),
-                     dim3(256), 0, g_stream, B, ldb, p.n, p.k,
-                     reinterpret_cast<unsigned long long*>(amax_b), flag);
+  if (p.f32) {
+    HIP_TRY(launch_amax_f32(g_stream, Af, lda, Bf, ldb, p.m, p.n, p.k, amax_a, amax_b, flag));
+  } else {
+    hipLaunchKernelGGL(k_amax_adjacent_lines, dim3(blocks_for(p.m, 256), blocks_for(p.k, kAmaxChunk)),
+                       dim3(256), 0, g_stream, A, lda, p.m, p.k,
+                       reinterpret_cast<unsigned long long*>(amax_a), flag);
+    hipLaunchKernelGGL(k_amax_contig_lines, dim3(blocks_for(p.n, 4), blocks_for(p.k, kAmaxContigChunk)),
+                       dim3(256), 0, g_stream, B, ldb, p.n, p.k,
+                       reinterpret_cast<unsigned long long*>(amax_b), flag);
+  }
   HIP_TRY(hipGetLastError());
   record(d, 1);
   if (last < 1) return OZFP4_OK;
@@ -210,7 +226,11 @@ int run_dgemm(const DgemmPlan& p, DeviceState* d, const double* A, int64_t lda, 
   const int64_t nfb = (p.n_pad / kFragLines) * p.kblocks;
   // an operand whose capacity exceeds 53 bits takes the wide encoder; the
   // Karatsuba mode's encoder lives in its own translation unit
-  if (p.kar) {
+  if (p.f32) {
+    HIP_TRY(launch_encode_f32((unsigned)encode_grid(nfa), lut_bytes, g_stream, Af, (int64_t)1, lda,
+                              p.m, p.k, amax_a, p.cA, pa, p.plane_a, nfa, p.kblocks, L, d->d_mod,
+                              lut, lut_entries));
+  } else if (p.kar) {
     HIP_TRY(launch_encode_kar(p.cA > 53, (unsigned)encode_grid(nfa), lut_bytes, g_stream, A,
                               (int64_t)1, lda, p.m, p.k, amax_a, p.cA, pa, p.plane_a, nfa,
                               p.kblocks, L, d->d_mod, lut, lut_entries));
@@ -223,7 +243,11 @@ int run_dgemm(const DgemmPlan& p, DeviceState* d, const double* A, int64_t lda, 
   }
   HIP_TRY(hipGetLastError());
   record(d, 2);
-  if (p.kar) {
+  if (p.f32) {
+    HIP_TRY(launch_encode_f32((unsigned)encode_grid(nfb), lut_bytes, g_stream, Bf, ldb, (int64_t)1,
+                              p.n, p.k, amax_b, p.cB, pb, p.plane_b, nfb, p.kblocks, L, d->d_mod,
+                              lut, lut_entries));
+  } else if (p.kar) {
     HIP_TRY(launch_encode_kar(p.cB > 53, (unsigned)encode_grid(nfb), lut_bytes, g_stream, B, ldb,
                               (int64_t)1, p.n, p.k, amax_b, p.cB, pb, p.plane_b, nfb, p.kblocks,
                               L, d->d_mod, lut, lut_entries));
@@ -256,6 +280,14 @@ int run_dgemm(const DgemmPlan& p, DeviceState* d, const double* A, int64_t lda, 
 
   // stage 4: CRT reconstruction and inverse scaling
   const int64_t nthreads = ((p.m + 3) / 4) * p.n;
+  if (p.f32) {
+    HIP_TRY(launch_crt_f32(g_stream, crt_chunks(L), R, p.m_pad, p.m_pad * p.n_pad, p.m, p.n,
+                           amax_a, amax_b, p.cA, p.cB, d->d_crt + L, static_cast<float*>(Cv),
+                           ldc));
+    record(d, 5);
+    return OZFP4_OK;
+  }
+  double* C = static_cast<double*>(Cv);
   if (crt_chunks(L) == 3)
     hipLaunchKernelGGL(k_crt<3>, dim3(blocks_for(nthreads, 256)), dim3(256), 0, g_stream, R,
                        p.m_pad, p.m_pad * p.n_pad, p.m, p.n, amax_a, amax_b, p.cA, p.cB,
@@ -391,8 +423,9 @@ int finish_with_flag(DeviceState* d, const int* dflag, int nstages) {
   return *d->h_flag ? OZFP4_ENONFINITE : OZFP4_OK;
 }
 
-int prepare(int64_t m, int64_t n, int64_t k, int L, DgemmPlan* p, DeviceState** d) {
-  int rc = make_dgemm_plan(m, n, k, L, p);
+int prepare(int64_t m, int64_t n, int64_t k, int L, DgemmPlan* p, DeviceState** d,
+            bool f32 = false) {
+  int rc = make_dgemm_plan(m, n, k, L, p, f32);
   if (rc) return rc;
   rc = device_state(d);
   if (rc) return rc;
@@ -473,6 +506,44 @@ int ozfp4_igemm_s8(int64_t m, int64_t n, int64_t k, const int8_t* A, int64_t lda
     g_pending_stages = 3;
     HIP_TRY(hipGetDevice(&g_pending_device));
   }
+  return OZFP4_OK;
+}
+
+int ozfp4_sgemm(int64_t m, int64_t n, int64_t k, const float* A, int64_t lda, const float* B,
+                int64_t ldb, float* C, int64_t ldc, int n_moduli) {
+  int rc = check_dgemm_args(m, n, k, A, lda, B, ldb, n_moduli);
+  if (rc) return rc;
+  if (ldc < std::max<int64_t>(1, m)) return OZFP4_EINVAL;
+  if (m == 0 || n == 0) return OZFP4_OK;
+  if (!C) return OZFP4_EINVAL;
+  if (k == 0) {
+    DeviceState* d;
+    rc = device_state(&d);
+    if (rc) return rc;
+    // +0.0f has the bit pattern of the int32 zero
+    hipLaunchKernelGGL(k_fill_i32_matrix, dim3(blocks_for(m * n, 256)), dim3(256), 0, g_stream,
+                       reinterpret_cast<int32_t*>(C), m, n, ldc);
+    HIP_TRY(hipGetLastError());
+    return OZFP4_OK;
+  }
+  DgemmPlan p;
+  DeviceState* d;
+  rc = prepare(m, n, k, n_moduli, &p, &d, true);
+  if (rc) return rc;
+  rc = run_dgemm(p, d, A, lda, B, ldb, C, ldc, 4, nullptr, nullptr);
+  if (rc) return rc;
+  return finish_with_flag(d, reinterpret_cast<int*>(d->ws + p.off_flag), 5);
+}
+
+int ozfp4_sgemm_capacity(int64_t k, int n_moduli, int32_t* c_a, int32_t* c_b) {
+  if (k < 1 || !c_a || !c_b) return OZFP4_EINVAL;
+  if (n_moduli < OZFP4_MIN_MODULI || n_moduli > OZFP4_MAX_MODULI) return OZFP4_EMODULI;
+  const HostTables* T = tables();
+  if (!T) return OZFP4_EHIP;
+  int a, b;
+  if (!capacity_split(T->P[n_moduli], k, kFp32Capacity, &a, &b)) return OZFP4_EMODULI;
+  *c_a = a;
+  *c_b = b;
   return OZFP4_OK;
 }
 

@@ -53,6 +53,8 @@ _SIGNATURES = {
     "ozfp4_scales": (_int, [_i64, _i64, _i64, _p, _i64, _p, _i64, _int, _p, _p]),
     "ozfp4_limb_planes": (_int, [_i64, _i64, _i64, _p, _i64, _p, _i64, _int, _p, _p]),
     "ozfp4_residues": (_int, [_i64, _i64, _i64, _p, _i64, _p, _i64, _int, _p, _i64]),
+    "ozfp4_sgemm": (_int, [_i64, _i64, _i64, _p, _i64, _p, _i64, _p, _i64, _int]),
+    "ozfp4_sgemm_capacity": (_int, [_i64, _int, _p, _p]),
     "ozfp4_dgemm_ozi": (_int, [_i64, _i64, _i64, _p, _i64, _p, _i64, _p, _i64, _int]),
     "ozfp4_ozi_config": (_int, [_int, _p, _p, _p]),
     "ozfp4_ozi_limb_planes": (_int, [_i64, _i64, _i64, _p, _i64, _p, _i64, _int, _p, _p]),
@@ -163,6 +165,17 @@ def ozfp4_limb_planes(m, n, k, A, lda, B, ldb, n_moduli, planes_a, planes_b) -> 
 
 def ozfp4_residues(m, n, k, A, lda, B, ldb, n_moduli, R, ldr) -> int:
     return load().ozfp4_residues(m, n, k, A, lda, B, ldb, n_moduli, R, ldr)
+
+
+def ozfp4_sgemm(m, n, k, A, lda, B, ldb, C, ldc, n_moduli) -> int:
+    return load().ozfp4_sgemm(m, n, k, A, lda, B, ldb, C, ldc, n_moduli)
+
+
+def ozfp4_sgemm_capacity(k: int, n_moduli: int) -> tuple[int, int]:
+    a, b = ctypes.c_int32(), ctypes.c_int32()
+    _check(load().ozfp4_sgemm_capacity(k, n_moduli, ctypes.byref(a), ctypes.byref(b)),
+           "ozfp4_sgemm_capacity")
+    return a.value, b.value
 
 
 def ozfp4_dgemm_ozi(m, n, k, A, lda, B, ldb, C, ldc, n_limbs) -> int:
@@ -375,3 +388,38 @@ def ozi_partials(A, B, n_limbs: int = OZFP4_OZI_MAX_LIMBS):
     _check(ozfp4_ozi_partials(m, n, k, A.data_ptr(), lda, B.data_ptr(), ldb, n_limbs,
                               H.data_ptr(), m), "ozfp4_ozi_partials")
     return H
+
+
+def sgemm_moduli(k: int) -> int:
+    """The fewest moduli that give ozfp4_sgemm 24-bit capacities for this k
+    (27 if none does)."""
+    for L in range(OZFP4_MIN_MODULI, OZFP4_MAX_MODULI + 1):
+        try:
+            if ozfp4_sgemm_capacity(k, L) == (24, 24):
+                return L
+        except OzFP4Error:
+            continue
+    return OZFP4_MAX_MODULI
+
+
+def sgemm(A, B, n_moduli: int | None = None, out=None):
+    """C = fl32(A B) for float32 device tensors A (m x k), B (k x n) by Ozaki
+    scheme II on FP4 limbs; n_moduli defaults to the fewest moduli with
+    24-bit capacities for this k. Returns C (m x n), column-major."""
+    import torch
+    A, lda = _cm(A, torch.float32, "A")
+    B, ldb = _cm(B, torch.float32, "B")
+    m, k = A.shape
+    k2, n = B.shape
+    if k != k2:
+        raise ValueError("inner dimensions differ")
+    if n_moduli is None:
+        n_moduli = sgemm_moduli(max(1, k))
+    C = _empty_cm(m, n, torch.float32, A.device) if out is None else out
+    if C.shape != (m, n) or C.dtype != torch.float32 or (C.stride(0) != 1 and m > 1):
+        raise ValueError("out must be a column-major float32 (m x n) tensor")
+    ldc = max(1, C.stride(1) if n > 1 else m)
+    _use_torch_stream(A.device)
+    _check(ozfp4_sgemm(m, n, k, A.data_ptr(), lda, B.data_ptr(), ldb, C.data_ptr(), ldc, n_moduli),
+           "ozfp4_sgemm")
+    return C

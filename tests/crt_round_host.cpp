@@ -2,13 +2,14 @@
 // library (crt_round.hpp), for tests/test_crt_round_host.py.
 // stdin: lines "L e2 r_0 ... r_{L-1}" (residues in [0, m_l)).
 // stdout per line: "<fast-or-exact result bits> <exact-path bits> <1 if the
-// fast path decided>", both as 16 hex digits.
+// fast path decided> <binary32 result bits>", 16, 16 and 8 hex digits.
 #include <cstdio>
 #include <cstring>
 #include <vector>
 
 #define OZFP4_HD inline
 #include "crt_round.hpp"
+#include "crt_round_f32.hpp"
 
 using namespace ozfp4;
 
@@ -37,8 +38,9 @@ int main() {
     if (NC == 3) fast = crt_fast3(sig[0], sig[1], sig[2], q, cc, e2, &out);
     const double ex = crt_exact(sig[0], sig[1], sig[2], NC == 4 ? sig[3] : 0.0, q, cc, e2);
     if (!fast) out = ex;
-    std::printf("%016llx %016llx %d\n", (unsigned long long)bits_of(out),
-                (unsigned long long)bits_of(ex), fast ? 1 : 0);
+    const float f = crt_exact_f32(sig[0], sig[1], sig[2], NC == 4 ? sig[3] : 0.0, q, cc, e2);
+    std::printf("%016llx %016llx %d %08x\n", (unsigned long long)bits_of(out),
+                (unsigned long long)bits_of(ex), fast ? 1 : 0, __builtin_bit_cast(uint32_t, f));
   }
   return 0;
 }

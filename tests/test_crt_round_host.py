@@ -5,7 +5,9 @@ arithmetic). Both the FP64 fast path and the exact 192-bit path are
 checked on every case. The cases cover uniform residues, small values, the
 boundaries of the fast path's two branches (|t| = 2, 3 at chunk 2^84),
 exact ties and near-ties of the final rounding, +-P/2, and scale factors
-that give subnormal results, underflow to zero and overflow to infinity."""
+that give subnormal results, underflow to zero and overflow to infinity.
+The binary32 rounding of the FP32 emulation (crt_round_f32.hpp) is checked
+on the same cases against the oracle's exact binary32 rounding."""
 
 import math
 import os
@@ -59,9 +61,17 @@ def _cases(L, rng):
             x *= rng.choice((-1, 1))
             if lo <= x <= half:
                 xs.append((x, rng.randint(-30, 30)))
+    for _ in range(400):   # near-ties of the binary32 rounding
+        E = rng.randint(25, max(25, P.bit_length() - 2))
+        mant = rng.randint(1 << 23, (1 << 24) - 1)
+        x = ((2 * mant + 1) << (E - 24)) + rng.choice((0, 0, 1, -1, 2, -2))
+        x *= rng.choice((-1, 1))
+        if lo <= x <= half:
+            xs.append((x, rng.randint(-30, 30)))
     for x in (half, lo, half - 1, lo + 1, 0, 1, -1, (1 << 53) - 1, 1 << 53, (1 << 53) + 1):
         if lo <= x <= half:
-            for e2 in (0, -1204, -1100, -1082, -1140, 900, 1000, 923, -2000, 2000):
+            for e2 in (0, -1204, -1100, -1082, -1140, 900, 1000, 923, -2000, 2000,
+                       -149, -150, -172, -180, 104, 127, 128):
                 xs.append((x, e2))
     for _ in range(150):
         x = rng.randint(lo, half)
@@ -79,10 +89,11 @@ def test_crt_round_matches_exact_rational(crt_bin, L):
     lines = res.stdout.split("\n")
     fast_count = 0
     for (x, e2, r), line in zip(cases, lines):
-        got, exact, fast = line.split()
+        got, exact, fast, f32 = line.split()
         want = struct.unpack("<Q", struct.pack("<d", o.round_scaled(x, -e2)))[0]
         assert int(exact, 16) == want, (L, x, e2, "exact path")
         assert int(got, 16) == want, (L, x, e2, "fast path" if fast == "1" else "exact path")
+        assert int(f32, 16) == int(o.round_scaled_f32(x, -e2).view("uint32")), (L, x, e2, "binary32")
         fast_count += int(fast)
     assert len(lines) >= len(cases)
     if L <= 19:   # three chunks: most elements take the fast path

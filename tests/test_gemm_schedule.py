@@ -36,7 +36,7 @@ def asm(tmp_path_factory):
         pytest.skip("no hipcc")
     out = {}
     d = tmp_path_factory.mktemp("asm")
-    for tu in ("ozfp4.hip", "karatsuba.hip", "ozaki1.hip"):
+    for tu in ("ozfp4.hip", "karatsuba.hip", "ozaki1.hip", "sgemm.hip"):
         path = str(d / (tu + ".s"))
         subprocess.run([hipcc, *FLAGS, os.path.join(CSRC, tu), "-o", path], check=True,
                        capture_output=True)

@@ -36,7 +36,8 @@ def test_header_declares_the_boundary():
                      "ozfp4_strerror", "ozfp4_scales", "ozfp4_limb_planes", "ozfp4_residues",
                      "ozfp4_sum_limb_table", "ozfp4_plane_count", "ozfp4_set_karatsuba",
                      "ozfp4_set_max_capacity", "ozfp4_dgemm_ozi", "ozfp4_ozi_config",
-                     "ozfp4_ozi_limb_planes", "ozfp4_ozi_partials"):
+                     "ozfp4_ozi_limb_planes", "ozfp4_ozi_partials", "ozfp4_sgemm",
+                     "ozfp4_sgemm_capacity"):
         assert required in names
 
 
@@ -167,6 +168,39 @@ def test_hook_argument_errors_on_host(lib):
     assert ozfp4.ozfp4_residues(4, 4, 4, 1, 4, 1, 4, 19, 1, 3) == ozfp4.OZFP4_EINVAL   # ldr < m
     assert ozfp4.ozfp4_scales(4, 4, 4, 1, 4, 1, 4, 19, 0, 1) == ozfp4.OZFP4_EINVAL     # null s
     assert ozfp4.ozfp4_limb_planes(4, 4, 4, 1, 4, 1, 4, 19, 1, 0) == ozfp4.OZFP4_EINVAL
+
+
+def test_sgemm_capacity_matches_oracle(lib):
+    for L in range(2, 28):
+        for k in (1, 100, 16384, 131072):
+            try:
+                want = o.capacity_bits_fp32(k, o.select_moduli(L))
+            except ValueError:
+                with pytest.raises(ozfp4.OzFP4Error):
+                    ozfp4.ozfp4_sgemm_capacity(k, L)
+                continue
+            assert ozfp4.ozfp4_sgemm_capacity(k, L) == want
+    assert ozfp4.sgemm_moduli(16384) == 10
+    # the FP32 cap ignores the FP64 path's capacity setting
+    try:
+        assert ozfp4.ozfp4_set_max_capacity(63) == ozfp4.OZFP4_OK
+        assert ozfp4.ozfp4_sgemm_capacity(16384, 19) == (24, 24)
+    finally:
+        ozfp4.ozfp4_set_max_capacity(53)
+
+
+@pytest.mark.parametrize("args,code", [
+    ((4, 4, 4, 1, 3, 1, 4, 1, 4, 10), ozfp4.OZFP4_EINVAL),           # lda < m
+    ((4, 4, 4, 1, 4, 1, 4, 1, 3, 10), ozfp4.OZFP4_EINVAL),           # ldc < m
+    ((4, 4, 4, 1, 4, 1, 4, 0, 4, 10), ozfp4.OZFP4_EINVAL),           # null C
+    ((4, 4, 4, 1, 4, 1, 4, 1, 4, 1), ozfp4.OZFP4_EMODULI),
+    ((4, 4, 4, 1, 4, 1, 4, 1, 4, 28), ozfp4.OZFP4_EMODULI),
+    ((4, 4, 131073, 1, 4, 1, 131073, 1, 4, 10), ozfp4.OZFP4_EKBOUND),
+    ((4, 4, 65536, 1, 4, 1, 65536, 1, 4, 2), ozfp4.OZFP4_EMODULI),   # P too small for k
+    ((0, 5, 5, 0, 1, 0, 5, 0, 1, 10), ozfp4.OZFP4_OK),
+])
+def test_sgemm_argument_errors_on_host(lib, args, code):
+    assert ozfp4.ozfp4_sgemm(*args) == code
 
 
 def test_ozi_config_matches_oracle(lib, paper):
