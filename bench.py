@@ -9,11 +9,12 @@ reconstruction. The printed JSON line carries the emulated-DGEMM rate
 measured with HIP events on the library's stream over the timed steps), the
 CPU oracle timed on a bounded sample, a per-stage breakdown, native FP64
 matrix product on the same GPU, Ozaki scheme I on the same limbs (checked
-bit for bit against scheme II) and the INT8-on-FP4 path as context.
+bit for bit against scheme II), the FP32 emulation beside native FP32 and
+the INT8-on-FP4 path as context.
 
 Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--moduli L]
                        [--size N] [--sweep] [--no-cpu-baseline] [--no-native] [--no-karatsuba]
-                       [--no-phi4] [--no-ozi]
+                       [--no-phi4] [--no-ozi] [--no-sgemm]
 """
 
 from __future__ import annotations
@@ -175,6 +176,8 @@ def main() -> int:
                     help="skip timing the three-product Karatsuba mode (comparison only)")
     ap.add_argument("--no-ozi", action="store_true",
                     help="skip Ozaki scheme I (15 limbs) and its bitwise check against scheme II")
+    ap.add_argument("--no-sgemm", action="store_true",
+                    help="skip the FP32 emulation (ozfp4_sgemm) and native FP32 on FP32 copies of the inputs")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="also run a plain 1 GiB device copy (reference for HBM byte counters)")
     args = ap.parse_args()
@@ -352,6 +355,45 @@ def main() -> int:
                                                                      C19.view(torch.int64)))}
         log(json.dumps(result["ozi"]))
         del C19
+        torch.cuda.empty_cache()
+
+    if not args.no_sgemm:
+        # FP32 emulation on FP32 copies of the same inputs, with the fewest
+        # moduli that give 24-bit capacities, beside native FP32 matmul
+        L32 = ozfp4.sgemm_moduli(N)
+        log(f"timing ozfp4_sgemm, {L32} moduli, and native FP32 torch.matmul")
+        A32 = A.astype(np.float32)
+        B32 = B.astype(np.float32)
+        A32d, B32d = dev_cm(A32, torch), dev_cm(B32, torch)
+        C32 = torch.empty_strided((N, N), (1, N), dtype=torch.float32, device="cuda")
+        sms, sst = time_call(ozfp4, torch, lambda: ozfp4.sgemm(A32d, B32d, L32, out=C32),
+                             max(3, args.steps // 2), 1)
+        rows32 = np.arange(0, N, N // 64)[:64]
+        ref32 = exact_reference(A32.astype(np.float64), B32.astype(np.float64), rows32, rows32)
+        bits32, worst32 = accuracy_bits(block_of(C32, rows32, rows32, torch).astype(np.float64), ref32)
+        Ar32, Br32 = torch.from_numpy(A32).to("cuda"), torch.from_numpy(B32).to("cuda")
+        Cn32 = torch.matmul(Ar32, Br32)
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        for _ in range(5):
+            torch.matmul(Ar32, Br32, out=Cn32)
+        torch.cuda.synchronize()
+        nms32 = (time.perf_counter() - t0) * 1e3 / 5
+        nbits32, nworst32 = accuracy_bits(block_of(Cn32, rows32, rows32, torch).astype(np.float64), ref32)
+        flops32 = (4 * L32 - 1) * 2.0 * N ** 3
+        result["sgemm"] = {
+            "workload": f"sgemm m=n=k={N}, phi=0.5 inputs rounded to FP32", "n_moduli": L32,
+            "capacity_bits": list(ozfp4.ozfp4_sgemm_capacity(N, L32)), "ms": sms,
+            "tflops": 2.0 * N ** 3 / sms / 1e9,
+            "stages_ms": dict(zip(stage_names, sst)),
+            "fp4_tflops_gemm": flops32 / sst[3] / 1e9,
+            "error_bits": bits32, "max_normalized_error": worst32,
+            "block": "64x64 (every 256th row and column)",
+            "native_fp32": {"ms": nms32, "tflops": 2.0 * N ** 3 / nms32 / 1e9,
+                            "error_bits": nbits32, "max_normalized_error": nworst32},
+            "speedup_vs_native_fp32": nms32 / sms}
+        log(json.dumps(result["sgemm"]))
+        del A32d, B32d, C32, Ar32, Br32, Cn32
         torch.cuda.empty_cache()
 
     if not args.no_int8:
