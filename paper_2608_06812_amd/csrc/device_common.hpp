@@ -250,6 +250,21 @@ __device__ __forceinline__ void dma16(const uint8_t* gsrc, uint8_t* lds_base) {
   __builtin_amdgcn_global_load_lds(gsrc, (__attribute__((address_space(3))) void*)lds_base, 16, 0, 0);
 }
 
+// Raw 32-bit data format of untyped buffer loads: dword 3 of a buffer
+// descriptor as the gfx9-family ISA defines it.
+constexpr int kBufferWord3 = 0x00020000;
+
+// Buffer-form LDS DMA: each lane copies 16 bytes from byte voffset + soffset
+// of buffer `src` (a wave-uniform descriptor, held in SGPRs) to LDS at
+// lds_base + 16 * lane (buffer_load_dwordx4 ... lds). A copy reads one
+// 32-bit VGPR offset and one SGPR offset instead of a 64-bit address per
+// lane. Completion is tracked by vmcnt.
+__device__ __forceinline__ void dma16_buf(__amdgpu_buffer_rsrc_t src, uint32_t voffset,
+                                          uint32_t soffset, uint8_t* lds_base) {
+  __builtin_amdgcn_raw_ptr_buffer_load_lds(
+      src, (__attribute__((address_space(3))) void*)lds_base, 16, voffset, soffset, 0, 0);
+}
+
 // s_waitcnt vmcnt(N) lgkmcnt(0) (expcnt untouched): this wave's vector
 // loads except the newest N have landed, and its LDS reads are complete.
 template <int N>
@@ -274,8 +289,8 @@ __device__ __forceinline__ void block_sync() {
 // waves share a SIMD and cover each other's LDS and barrier waits). A stage
 // is 48 fragments (A: 2 planes x 8 line blocks x 2 k fragments, then B:
 // 2 planes x 4 line blocks x 2 k fragments), 48 KiB, copied into a 3-slot
-// LDS ring by LDS DMA (6 whole fragments per wave, each 1 KiB contiguous in
-// HBM), up to three stages ahead of the one being multiplied.
+// LDS ring by buffer-form LDS DMA (6 whole fragments per wave, each 1 KiB
+// contiguous in HBM), two stages ahead of the one being multiplied.
 constexpr int kTileM = 256;        // lines of A per block
 constexpr int kTileN = 128;        // lines of B per block
 constexpr int kRing = 3;           // LDS slots
@@ -337,26 +352,29 @@ __device__ __forceinline__ void gemm_res_tile(
   const int wm = wave >> 1, wn = wave & 1;
   const int rbw = 2 * wm, cbw = 2 * wn;   // this wave's first A / B line block
 
-  // fragment f = wave * 6 + j of a stage (LDS offset f KiB): uniform base
-  const uint8_t* gsrc[kDmaPerWave];
+  // fragment f = wave * 6 + j of a stage (LDS offset f KiB): a buffer
+  // descriptor per fragment, based at that fragment of stage 0 (uniform);
+  // stage st adds st * 2 KiB as the SGPR offset
+  const int nst = (int)(kblocks / 2);
+  __amdgpu_buffer_rsrc_t src[kDmaPerWave];
 #pragma unroll
   for (int j = 0; j < kDmaPerWave; ++j) {
     const int f = wave * kDmaPerWave + j;
+    const uint8_t* base;
     if (f < 32) {
       const int kbl = f & 1, rb = (f >> 1) & 7, p = f >> 4;
-      gsrc[j] = PA + (int64_t)(2 * l + p) * plane_a + ((tm * 8 + rb) * kblocks + kbl) * kFragBytes;
+      base = PA + (int64_t)(2 * l + p) * plane_a + ((tm * 8 + rb) * kblocks + kbl) * kFragBytes;
     } else {
       const int g = f - 32, kbl = g & 1, cb = (g >> 1) & 3, p = g >> 3;
-      gsrc[j] = PB + (int64_t)(2 * l + p) * plane_b + ((tn * 4 + cb) * kblocks + kbl) * kFragBytes;
+      base = PB + (int64_t)(2 * l + p) * plane_b + ((tn * 4 + cb) * kblocks + kbl) * kFragBytes;
     }
+    src[j] = __builtin_amdgcn_make_buffer_rsrc((void*)base, (short)0, nst * 2 * kFragBytes,
+                                               kBufferWord3);
   }
   const int lane16 = lane * 16;
-  const int nst = (int)(kblocks / 2);
-  auto issue = [&](int s) {
-    uint8_t* dst = lds + (s % kRing) * kStageBytes + wave * kDmaPerWave * kFragBytes;
-#pragma unroll
-    for (int j = 0; j < kDmaPerWave; ++j)
-      dma16(gsrc[j] + (int64_t)s * 2 * kFragBytes + lane16, dst + j * kFragBytes);
+  auto dma = [&](int st, int j) {
+    dma16_buf(src[j], (uint32_t)lane16, (uint32_t)(st * 2 * kFragBytes),
+              lds + (st % kRing) * kStageBytes + (wave * kDmaPerWave + j) * kFragBytes);
   };
 
   v16f acc[3][2][2];
@@ -369,14 +387,21 @@ __device__ __forceinline__ void gemm_res_tile(
 #pragma unroll
         for (int v = 0; v < 16; ++v) acc[a][i][j][v] = 0.0f;
 
-  // Per stage: k fragment 0 (read, 16 MFMAs), k fragment 1 (read, 12
+  // Per stage s: k fragment 0 (read, 16 MFMAs), k fragment 1 (read, 12
   // MFMAs), then the stage handover: wait until stage s + 1 has landed and
-  // this wave's reads are done, barrier, refill the slot of stage s with
-  // stage s + 3, and only then issue the last 4 MFMAs of stage s, so the
-  // matrix pipe still has queued work while the waves synchronise.
+  // this wave's reads are done, barrier, and only then the last 4 MFMAs of
+  // stage s, so the matrix pipe still has queued work while the waves
+  // synchronise. Stage s + 2 is copied during stage s into the slot of
+  // stage s - 1, which every wave finished reading before the previous
+  // barrier; its six copies per wave go out in pairs between the MFMAs
+  // rather than in one burst after the barrier, so the data path from L2
+  // into LDS never holds up the matrix pipe of every wave at once. At the
+  // handover only those six copies may still be in flight.
 #pragma unroll
-  for (int s = 0; s < kRing; ++s) issue(s);     // nst >= kRing by padding
-  wait_vm_lgkm0<2 * kDmaPerWave>();
+  for (int j = 0; j < kDmaPerWave; ++j) dma(0, j);
+#pragma unroll
+  for (int j = 0; j < kDmaPerWave; ++j) dma(1, j);   // nst >= 2 by padding
+  wait_vm_lgkm0<kDmaPerWave>();   // stage 0 landed
   block_sync();
 
   v4i a[2][2], b[2][2];   // [plane][i] of A, [plane][j] of B
@@ -390,6 +415,7 @@ __device__ __forceinline__ void gemm_res_tile(
       }
   };
   // every product except a1 b1 (acc2), which is issued after the handover
+  // of the stage's second k fragment
   auto mfma_head = [&]() {
 #pragma unroll
     for (int i = 0; i < 2; ++i)
@@ -411,38 +437,47 @@ __device__ __forceinline__ void gemm_res_tile(
         for (int j = 0; j < 2; ++j) acc[2][i][j] = mfma_fp4(a[1][i], b[1][j], acc[2][i][j]);
     }
   };
-  auto stage_body = [&](int s) {   // everything of stage s before the handover
+  // everything of stage s before the handover; with `copy`, the copies of
+  // stage s + 2 interleaved
+  auto stage_body = [&](int s, bool copy) {
     const uint8_t* sb = lds + (s % kRing) * kStageBytes;
     read_frags(sb, 0);
     mfma_head();
+    if (copy) {
+      dma(s + 2, 0);
+      dma(s + 2, 1);
+    }
+    __builtin_amdgcn_sched_barrier(0);
     mfma_tail();
     __builtin_amdgcn_sched_barrier(0);
     read_frags(sb, 1);
+    if (copy) {
+      dma(s + 2, 2);
+      dma(s + 2, 3);
+    }
     mfma_head();
+    if (copy) {
+      dma(s + 2, 4);
+      dma(s + 2, 5);
+    }
     __builtin_amdgcn_sched_barrier(0);
   };
 
   int s = 0;
-  for (; s + kRing < nst; ++s) {   // steady state: the refill is always due
-    stage_body(s);
+  for (; s + 2 < nst; ++s) {       // steady state: stage s + 2 exists
+    stage_body(s, true);
     wait_vm_lgkm0<kDmaPerWave>();  // stage s + 1 landed; reads of stage s done
     block_sync();
-    issue(s + kRing);              // refills the slot of stage s
     mfma_tail();
     __builtin_amdgcn_sched_barrier(0);
   }
-  // the last three stages (k is padded to at least three stages)
-  stage_body(s);
-  wait_vm_lgkm0<kDmaPerWave>();
-  block_sync();
-  mfma_tail();
-  __builtin_amdgcn_sched_barrier(0);
-  stage_body(s + 1);
+  // the last two stages
+  stage_body(s, false);
   wait_vm_lgkm0<0>();
   block_sync();
   mfma_tail();
   __builtin_amdgcn_sched_barrier(0);
-  stage_body(s + 2);
+  stage_body(s + 1, false);
   mfma_tail();
 
   store_residues<4, 52, 676>(acc, l, tm, tn, wm, wn, lane, R, ldr, rplane, mc);

@@ -151,8 +151,9 @@ __global__ __launch_bounds__(512, 1) void k_gemm_res(
 // int32. Block tile 128 x 128, eight waves (two per SIMD) of 64 x 32 (2 x 1
 // MFMA tiles, five accumulator sets = 160 registers). A stage covers k = 128:
 // 48 fragments (A: 3 planes x 4 line blocks x 2 k fragments, then B the
-// same), 48 KiB, streamed into the 3-slot LDS ring by LDS DMA as in the
-// residue GEMM, 6 fragments per wave.
+// same), 48 KiB, streamed into the 3-slot LDS ring by buffer-form LDS DMA
+// as in the residue GEMM (stage s + 2 copied during stage s, in pairs
+// between the MFMAs), 6 fragments per wave.
 constexpr int kTileS8M = 128;
 constexpr int kTileS8N = 128;
 __device__ __forceinline__ constexpr int fragA8(int p, int rb, int kbl) { return ((p * 4 + rb) * 2 + kbl) * kFragBytes; }
@@ -171,22 +172,23 @@ __global__ __launch_bounds__(512, 1) void k_gemm_s8(
   const int wm = wave >> 2, wn = wave & 3;
   const int rbw = 2 * wm;   // this wave's first A line block; its B line block is wn
 
-  const uint8_t* gsrc[kDmaPerWave];
+  const int nst = (int)(kblocks / 2);
+  __amdgpu_buffer_rsrc_t src[kDmaPerWave];   // fragment j of stage 0, uniform
 #pragma unroll
   for (int j = 0; j < kDmaPerWave; ++j) {
     const int f = wave * kDmaPerWave + j;
     const int g = f < 24 ? f : f - 24;
     const int kbl = g & 1, blk = (g >> 1) & 3, p = g >> 3;
-    gsrc[j] = f < 24 ? PA + (int64_t)p * plane_a + ((tm * 4 + blk) * kblocks + kbl) * kFragBytes
-                     : PB + (int64_t)p * plane_b + ((tn * 4 + blk) * kblocks + kbl) * kFragBytes;
+    const uint8_t* base =
+        f < 24 ? PA + (int64_t)p * plane_a + ((tm * 4 + blk) * kblocks + kbl) * kFragBytes
+               : PB + (int64_t)p * plane_b + ((tn * 4 + blk) * kblocks + kbl) * kFragBytes;
+    src[j] = __builtin_amdgcn_make_buffer_rsrc((void*)base, (short)0, nst * 2 * kFragBytes,
+                                               kBufferWord3);
   }
   const int lane16 = lane * 16;
-  const int nst = (int)(kblocks / 2);
-  auto issue = [&](int s) {
-    uint8_t* dst = lds + (s % kRing) * kStageBytes + wave * kDmaPerWave * kFragBytes;
-#pragma unroll
-    for (int j = 0; j < kDmaPerWave; ++j)
-      dma16(gsrc[j] + (int64_t)s * 2 * kFragBytes + lane16, dst + j * kFragBytes);
+  auto dma = [&](int st, int j) {
+    dma16_buf(src[j], (uint32_t)lane16, (uint32_t)(st * 2 * kFragBytes),
+              lds + (st % kRing) * kStageBytes + (wave * kDmaPerWave + j) * kFragBytes);
   };
 
   v16f acc[5][2];
@@ -198,8 +200,10 @@ __global__ __launch_bounds__(512, 1) void k_gemm_s8(
       for (int v = 0; v < 16; ++v) acc[a][i][v] = 0.0f;
 
 #pragma unroll
-  for (int s = 0; s < kRing; ++s) issue(s);     // nst >= kRing by padding
-  wait_vm_lgkm0<2 * kDmaPerWave>();
+  for (int j = 0; j < kDmaPerWave; ++j) dma(0, j);
+#pragma unroll
+  for (int j = 0; j < kDmaPerWave; ++j) dma(1, j);   // nst >= 2 by padding
+  wait_vm_lgkm0<kDmaPerWave>();   // stage 0 landed
   block_sync();
 
   v4i a[3][2], b[3];
@@ -232,37 +236,44 @@ __global__ __launch_bounds__(512, 1) void k_gemm_s8(
       acc[4][i] = mfma_fp4(a[2][i], b[2], acc[4][i]);
     }
   };
-  auto stage_body = [&](int s) {
+  auto stage_body = [&](int s, bool copy) {   // with the copies of stage s + 2
     const uint8_t* sb = lds + (s % kRing) * kStageBytes;
     read_frags(sb, 0);
     mfma_head();
+    if (copy) {
+      dma(s + 2, 0);
+      dma(s + 2, 1);
+    }
+    __builtin_amdgcn_sched_barrier(0);
     mfma_tail();
     __builtin_amdgcn_sched_barrier(0);
     read_frags(sb, 1);
+    if (copy) {
+      dma(s + 2, 2);
+      dma(s + 2, 3);
+    }
     mfma_head();
+    if (copy) {
+      dma(s + 2, 4);
+      dma(s + 2, 5);
+    }
     __builtin_amdgcn_sched_barrier(0);
   };
 
   int s = 0;
-  for (; s + kRing < nst; ++s) {
-    stage_body(s);
+  for (; s + 2 < nst; ++s) {
+    stage_body(s, true);
     wait_vm_lgkm0<kDmaPerWave>();  // stage s + 1 landed; reads of stage s done
     block_sync();
-    issue(s + kRing);
     mfma_tail();
     __builtin_amdgcn_sched_barrier(0);
   }
-  stage_body(s);
-  wait_vm_lgkm0<kDmaPerWave>();
-  block_sync();
-  mfma_tail();
-  __builtin_amdgcn_sched_barrier(0);
-  stage_body(s + 1);
+  stage_body(s, false);
   wait_vm_lgkm0<0>();
   block_sync();
   mfma_tail();
   __builtin_amdgcn_sched_barrier(0);
-  stage_body(s + 2);
+  stage_body(s + 1, false);
   mfma_tail();
 
   // compose every output first (the other four accumulator sets die), then

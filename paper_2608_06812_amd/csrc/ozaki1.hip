@@ -130,7 +130,10 @@ __global__ __launch_bounds__(256) void k_encode_ozi(
 // GEMM: eight waves of 64 x 32 (2 x 1 MFMA tiles, 160 accumulator
 // registers), k in stages of 128, 48 fragments per stage (waves 0-3 copy
 // the three A planes of block I, waves 4-7 the three B planes of block J),
-// three LDS slots filled by LDS DMA.
+// three LDS slots filled by buffer-form LDS DMA, stage s + 2 copied during
+// stage s in pairs between the MFMAs. A copy's descriptor is based at its
+// own 1 KiB fragment, since the limb-block offsets exceed 32 bits for large
+// operands.
 //
 // Exactness: an accumulator set sums at most 5 pairs x 3 products per k,
 // each a multiple of 1/4 of magnitude <= 16 (greedy limbs |c| <= 8), so a
@@ -176,10 +179,11 @@ __global__ __launch_bounds__(512, 1) void k_gemm_ozi(
                      : PB + (int64_t)p * plane_b + ((tn * 4 + blk) * kblocks + kbl) * kFragBytes;
   }
   const int lane16 = lane * 16;
-  auto issue = [&](int slot, int64_t off) {
-    uint8_t* dst = lds + slot * kStageBytes + wave * kDmaPerWave * kFragBytes;
-#pragma unroll
-    for (int j = 0; j < kDmaPerWave; ++j) dma16(gsrc[j] + off + lane16, dst + j * kFragBytes);
+  auto dma = [&](int slot, int64_t off, int j) {
+    const __amdgpu_buffer_rsrc_t src = __builtin_amdgcn_make_buffer_rsrc(
+        (void*)(gsrc[j] + off), (short)0, kFragBytes, kBufferWord3);
+    dma16_buf(src, (uint32_t)lane16, 0u,
+              lds + slot * kStageBytes + (wave * kDmaPerWave + j) * kFragBytes);
   };
 
   v16f acc[5][2];
@@ -211,14 +215,30 @@ __global__ __launch_bounds__(512, 1) void k_gemm_ozi(
       acc[4][i] = mfma_fp4(a[2][i], b[2], acc[4][i]);
     }
   };
-  auto stage_body = [&](int s) {
+  // stage s; with `copy`, the copies of stage s + 2 (at offset off) are
+  // interleaved
+  auto stage_body = [&](int s, bool copy, int64_t off) {
     const uint8_t* sb = lds + (s % kRing) * kStageBytes;
+    const int slot2 = (s + 2) % kRing;
     read_frags(sb, 0);
     mfma_head();
+    if (copy) {
+      dma(slot2, off, 0);
+      dma(slot2, off, 1);
+    }
+    __builtin_amdgcn_sched_barrier(0);
     mfma_tail();
     __builtin_amdgcn_sched_barrier(0);
     read_frags(sb, 1);
+    if (copy) {
+      dma(slot2, off, 2);
+      dma(slot2, off, 3);
+    }
     mfma_head();
+    if (copy) {
+      dma(slot2, off, 4);
+      dma(slot2, off, 5);
+    }
     __builtin_amdgcn_sched_barrier(0);
   };
 
@@ -238,10 +258,9 @@ __global__ __launch_bounds__(512, 1) void k_gemm_ozi(
     auto next_off = [&]() -> int64_t {
       const int blk = copies_a ? I0 + ip : h - I0 - ip;
       const int64_t off = (int64_t)blk * blk_stride + (int64_t)ks * 2 * kFragBytes;
-      if (++ks == st1) {
-        ks = st0;
-        ++ip;
-      }
+      const int wrap = (++ks == st1) ? 1 : 0;   // uniform, branch-free
+      ks = wrap ? st0 : ks;
+      ip += wrap;
       return off;
     };
 #pragma unroll
@@ -255,30 +274,28 @@ __global__ __launch_bounds__(512, 1) void k_gemm_ozi(
       block_sync();
     }
 #pragma unroll
-    for (int s = 0; s < kRing; ++s) issue(s, next_off());
-    wait_vm_lgkm0<2 * kDmaPerWave>();
+    for (int st = 0; st < 2; ++st) {   // total >= 2
+      const int64_t off = next_off();
+#pragma unroll
+      for (int j = 0; j < kDmaPerWave; ++j) dma(st, off, j);
+    }
+    wait_vm_lgkm0<kDmaPerWave>();   // stage 0 landed
     block_sync();
 
     int s = 0;
-    for (; s + kRing < total; ++s) {
-      stage_body(s);
+    for (; s + 2 < total; ++s) {
+      stage_body(s, true, next_off());   // copies stage s + 2 into the slot of stage s - 1
       wait_vm_lgkm0<kDmaPerWave>();  // stage s + 1 landed; reads of stage s done
       block_sync();
-      issue(s % kRing, next_off());  // refills the slot of stage s with stage s + 3
       mfma_tail();
       __builtin_amdgcn_sched_barrier(0);
     }
-    stage_body(s);
-    wait_vm_lgkm0<kDmaPerWave>();
-    block_sync();
-    mfma_tail();
-    __builtin_amdgcn_sched_barrier(0);
-    stage_body(s + 1);
+    stage_body(s, false, 0);
     wait_vm_lgkm0<0>();
     block_sync();
     mfma_tail();
     __builtin_amdgcn_sched_barrier(0);
-    stage_body(s + 2);
+    stage_body(s + 1, false, 0);
     mfma_tail();
     // keeps every MFMA ahead of the flush instead of sunk into its branches
 #pragma unroll

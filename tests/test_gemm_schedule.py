@@ -2,7 +2,8 @@
 this repository's own sources (hipcc -S, no GPU needed).
 
 The streaming design relies on the compiler keeping a schedule: per stage a
-fixed number of MFMAs, LDS reads and LDS-DMA copies, one barrier, no
+fixed number of MFMAs, LDS reads and LDS-DMA copies (global or buffer
+form), one barrier, no
 register spills, and LDS reads issued in batches rather than each one waited
 for before its MFMA. The compiler's schedule can change without any change
 to a kernel's source (a change elsewhere in the translation unit is
@@ -112,7 +113,7 @@ def test_gemm_steady_loop(asm, tu, prefix, mfma, reads, dma):
     assert loops, f"no loop with {mfma} MFMAs in {prefix}"
     loop = loops[0]
     assert _count(loop, r"^ds_read_b128") == reads
-    assert _count(loop, r"^global_load_lds_dwordx4") == dma
+    assert _count(loop, r"^(global_load_lds_dwordx4|buffer_load_dwordx4 .* lds$)") == dma
     assert _count(loop, r"^s_barrier") == 1
     assert _count(loop, r"scratch_") == 0
     # LDS reads go out in batches, several in flight before a wait for all
