@@ -16,7 +16,8 @@ namespace ozfp4 {
 // = -48 P0 + 52 Ps + 624 P2 (mod m). Same block tile and waves as above; k
 // in stages of 64, 36 fragments (A: 3 planes x 8 line blocks, then B: 3
 // planes x 4 line blocks), in a 4-slot ring of 36 KiB that waves 0..5 fill
-// with 6 fragments each, up to four stages ahead.
+// with 6 fragments each by buffer-form LDS DMA, four stages ahead, the six
+// copies spread in pairs through the MFMA stream.
 constexpr int kRingK = 4;
 constexpr int kStageFragsK = 36;
 constexpr int kStageBytesK = kStageFragsK * kFragBytes;
@@ -38,7 +39,8 @@ __device__ __forceinline__ void gemm_res_tile_k(
   const int rbw = 2 * wm, cbw = 2 * wn;
   const int psum = 2 * L + mc->ksum[l];
 
-  // fragment f = wave * 6 + j of a stage (LDS offset f KiB), waves 0..5
+  // fragment f = wave * 6 + j of a stage (LDS offset f KiB), waves 0..5;
+  // each copy source is a buffer descriptor based at its stage-0 fragment
   const uint8_t* gsrc[kDmaPerWave];
 #pragma unroll
   for (int j = 0; j < kDmaPerWave; ++j) {
@@ -70,11 +72,14 @@ __device__ __forceinline__ void gemm_res_tile_k(
   const int slot_step = dma_wave ? kStageBytesK : 0;
   const int lane16 = lane * 16;
   const int nst = (int)kblocks;
-  auto issue = [&](int s) {
-    uint8_t* dst = dst_base + (s & (kRingK - 1)) * slot_step;
+  __amdgpu_buffer_rsrc_t src[kDmaPerWave];
 #pragma unroll
-    for (int j = 0; j < kDmaPerWave; ++j)
-      dma16(gsrc[j] + (int64_t)s * kFragBytes + lane16, dst + j * dst_step);
+  for (int j = 0; j < kDmaPerWave; ++j)
+    src[j] = __builtin_amdgcn_make_buffer_rsrc((void*)gsrc[j], (short)0, nst * kFragBytes,
+                                               kBufferWord3);
+  auto dma = [&](int st, int j) {
+    dma16_buf(src[j], (uint32_t)lane16, (uint32_t)(st * kFragBytes),
+              dst_base + (st & (kRingK - 1)) * slot_step + j * dst_step);
   };
 
   v16f acc[3][2][2];
@@ -88,11 +93,19 @@ __device__ __forceinline__ void gemm_res_tile_k(
         for (int v = 0; v < 16; ++v) acc[a][i][j][v] = 0.0f;
 
   // Per stage: P0 (4 MFMAs), read the sum fragments, P2 (4), the handover
-  // (wait for stage s + 1 and this wave's reads, barrier, refill the slot of
-  // stage s with stage s + 4), Ps (4), read c0 / c1 fragments of stage s + 1.
+  // (wait for stage s + 1 and this wave's reads, barrier), Ps (4), read c0 /
+  // c1 fragments of stage s + 1. The slot of stage s is free after the
+  // handover barrier and takes stage s + 4: two copies right after the
+  // barrier, two after Ps, the last two between P0 and P2 of stage s + 1,
+  // so no burst of copies holds up the matrix pipes. At a handover at most
+  // the copies of stages s + 2 and s + 3 are in flight.
 #pragma unroll
-  for (int s = 0; s < kRingK; ++s) issue(s);   // nst >= 6 > kRingK by padding
-  wait_vm_lgkm0<(kRingK - 1) * kDmaPerWave>();
+  for (int st = 0; st < kRingK - 1; ++st)   // nst >= 6 > kRingK by padding
+#pragma unroll
+    for (int j = 0; j < kDmaPerWave; ++j) dma(st, j);
+#pragma unroll
+  for (int j = 0; j < kDmaPerWave - 2; ++j) dma(kRingK - 1, j);
+  wait_vm_lgkm0<(kRingK - 1) * kDmaPerWave - 2>();   // stage 0 landed
   block_sync();
 
   v4i a0[2], a1[2], b0[2], b1[2], as[2], bs[2];
@@ -131,8 +144,14 @@ __device__ __forceinline__ void gemm_res_tile_k(
 #pragma unroll
       for (int j = 0; j < 2; ++j) acc[1][i][j] = mfma_fp4(as[i], bs[j], acc[1][i][j]);
   };
-  auto head = [&](int s) {   // stage s up to the handover
+  // stage s up to the handover; with `pend`, the last two copies of stage
+  // s + 3 between P0 and P2
+  auto head = [&](int s, bool pend) {
     mfma_p0();
+    if (pend) {
+      dma(s + 3, 4);
+      dma(s + 3, 5);
+    }
     read_sum(slot(s));
     mfma_p2();
     __builtin_amdgcn_sched_barrier(0);
@@ -141,36 +160,40 @@ __device__ __forceinline__ void gemm_res_tile_k(
   read_lo(slot(0));
   int s = 0;
 #pragma unroll 1
-  for (; s + kRingK < nst; ++s) {   // steady state: the refill is always due
-    head(s);
+  for (; s + kRingK < nst; ++s) {   // steady state: stage s + 4 exists
+    head(s, true);
     wait_vm_lgkm0<(kRingK - 2) * kDmaPerWave>();   // stage s + 1 landed; reads done
     block_sync();
-    issue(s + kRingK);
+    dma(s + kRingK, 0);
+    dma(s + kRingK, 1);
     __builtin_amdgcn_sched_barrier(0);
     mfma_ps();
+    __builtin_amdgcn_sched_barrier(0);
+    dma(s + kRingK, 2);
+    dma(s + kRingK, 3);
     read_lo(slot(s + 1));
     __builtin_amdgcn_sched_barrier(0);
   }
   // the last four stages
-  head(s);
+  head(s, true);
   wait_vm_lgkm0<2 * kDmaPerWave>();
   block_sync();
   mfma_ps();
   read_lo(slot(s + 1));
   __builtin_amdgcn_sched_barrier(0);
-  head(s + 1);
+  head(s + 1, false);
   wait_vm_lgkm0<kDmaPerWave>();
   block_sync();
   mfma_ps();
   read_lo(slot(s + 2));
   __builtin_amdgcn_sched_barrier(0);
-  head(s + 2);
+  head(s + 2, false);
   wait_vm_lgkm0<0>();
   block_sync();
   mfma_ps();
   read_lo(slot(s + 3));
   __builtin_amdgcn_sched_barrier(0);
-  head(s + 3);
+  head(s + 3, false);
   mfma_ps();
 
   store_residues<-48, 52, 624>(acc, l, tm, tn, wm, wn, lane, R, ldr, rplane, mc);
