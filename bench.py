@@ -40,7 +40,7 @@ METRIC = "emulated DGEMM TFLOPS at N=16384 + % of FP4 MFMA peak, 1xMI355X"
 # (profiles/k_gemm_res_dgemm_16384_L18.md). Valid only for the GEMM source
 # they were taken on, identified by the hash of its section of kernels.hpp.
 MEASURED_TRAFFIC = {
-    "kernel_source_sha256_16": "5239bf8704811bd7",
+    "kernel_source_sha256_16": "87c72f0392169584",
     "workload": (16384, 16384, 16384, 18),
     "read_GB": 154.6, "write_GB": 4.87,
 }

@@ -226,30 +226,6 @@ __device__ __forceinline__ v16f mfma_fp4(v4i a, v4i b, v16f c) {
   return __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(a8, b8, c, 4, 4, 0, 127, 0, 127);
 }
 
-// Fused limb-product GEMM over a 128 x 128 block tile, k in stages of 128.
-// NP planes per operand; product (i, j) of plane i of A and plane j of B is
-// accumulated into accumulator acc_index(i, j). Four waves, each 64 x 64
-// (2 x 2 MFMA tiles of 32 x 32). LDS holds two stages (double buffer);
-// global -> register -> LDS staging, one stage ahead.
-//   LDS stage layout: [operand][plane][32-line block 0..3][k fragment 0..1]
-//   x 1 KiB.
-template <int NP>
-struct StageLayout {
-  static constexpr int kBytes = 2 * NP * 4 * 2 * kFragBytes;
-  static constexpr int kChunks = kBytes / 16;            // 16-byte pieces
-  static constexpr int kPerThread = kChunks / 256;       // 4 * NP
-  __device__ static constexpr int frag(int op, int p, int rbl, int kbl) {
-    return (((op * NP + p) * 4 + rbl) * 2 + kbl) * kFragBytes;
-  }
-};
-
-// LDS DMA: each lane copies 16 bytes from global memory to LDS at
-// lds_base + 16 * lane (global_load_lds_dwordx4); lds_base must be
-// wave-uniform. Completion is tracked by vmcnt like any vector load.
-__device__ __forceinline__ void dma16(const uint8_t* gsrc, uint8_t* lds_base) {
-  __builtin_amdgcn_global_load_lds(gsrc, (__attribute__((address_space(3))) void*)lds_base, 16, 0, 0);
-}
-
 // Raw 32-bit data format of untyped buffer loads: dword 3 of a buffer
 // descriptor as the gfx9-family ISA defines it.
 constexpr int kBufferWord3 = 0x00020000;
