@@ -108,7 +108,19 @@ __global__ __launch_bounds__(256) void k_encode_dgemm(
     const int s = live ? line_shift(amax[line], cap) : 0;
     double xe[32];
     const TIn* src = X + (live ? line : 0) * rs + kbase * ks;
-    if (live && kbase + 32 <= k) {
+    if (live && kbase + 32 <= k && ks == 1 && (reinterpret_cast<uintptr_t>(src) & 15) == 0) {
+      // the lane's 32 values are contiguous (lines along k, as B's
+      // columns): 16-byte loads
+      constexpr int kPer = 16 / (int)sizeof(TIn);
+      typedef TIn Vec __attribute__((ext_vector_type(kPer)));
+      const Vec* v = reinterpret_cast<const Vec*>(src);
+#pragma unroll
+      for (int e = 0; e < 32 / kPer; ++e) {
+        const Vec x = v[e];
+#pragma unroll
+        for (int q = 0; q < kPer; ++q) xe[e * kPer + q] = (double)x[q];
+      }
+    } else if (live && kbase + 32 <= k) {
 #pragma unroll
       for (int e = 0; e < 32; ++e) {
         xe[e] = (double)*src;
