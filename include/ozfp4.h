@@ -47,9 +47,12 @@ extern "C" {
  * (the cross term holds two products per k) is a multiple of 1/4 of
  * magnitude <= 2^22, exact in FP32, for k <= 131072 (Lemma 2, Lemma 3). */
 #define OZFP4_MAX_K       131072
-/* INT8 path: the deepest limb group holds three products per k, so every
- * prefix stays exact in FP32 for k <= 2^24 / (3 * 64) = 87381. */
-#define OZFP4_MAX_K_S8     87381
+/* INT8 path: the deepest limb group holds three products per k, so an FP32
+ * accumulation stays exact for k <= 2^24 / (3 * 64) = 87381; the library
+ * accumulates k in chunks of at most 81920 and adds the chunks in wrapping
+ * int32, so any k up to this limit (set by 32-bit buffer offsets) is exact
+ * modulo 2^32. */
+#define OZFP4_MAX_K_S8  16777216
 
 /*
  * ozfp4_dgemm -- C = fl(A B) for FP64 A, B by Ozaki scheme II on FP4 limbs
@@ -87,10 +90,10 @@ int ozfp4_dgemm(int64_t m, int64_t n, int64_t k,
  * ozfp4_igemm_s8 -- C = A B for INT8 A, B with INT32 C, bit-exact, on FP4
  * limbs (Sec. III): every int8 splits into three greedy base-13 limbs
  * (X_3 = 732 >= 128), the nine limb products run as FP4 matrix products
- * grouped by i + j with FP32 accumulation (exact by the bound above), and
- * C = sum_g 13^g * 4 * G_g is formed in wrapping int32 arithmetic, i.e. C
- * equals the integer product reduced modulo 2^32 into [-2^31, 2^31) exactly
- * like INT32 accumulation.
+ * grouped by i + j with FP32 accumulation (exact over each k chunk of at
+ * most 81920), and C = sum_g 13^g * 4 * G_g is formed in wrapping int32
+ * arithmetic over the chunks, i.e. C equals the integer product reduced
+ * modulo 2^32 into [-2^31, 2^31) exactly like INT32 accumulation.
  * Returns OZFP4_EKBOUND for k > OZFP4_MAX_K_S8. k == 0 writes zeros.
  * Asynchronous on the set stream.
  */

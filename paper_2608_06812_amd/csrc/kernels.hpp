@@ -154,7 +154,13 @@ __global__ __launch_bounds__(512, 1) void k_gemm_res(
 // same), 48 KiB, streamed into the 3-slot LDS ring by buffer-form LDS DMA
 // as in the residue GEMM (stage s + 2 copied during stage s, in pairs
 // between the MFMAs), 6 fragments per wave.
+// The deepest group sums three products per k, each a multiple of 1/4 of
+// magnitude <= 16, so an FP32 accumulation stays exact for k <= 87381.
+// Longer k runs in balanced chunks of at most 640 stages (k = 81920); after
+// each chunk the composed sums are added into wrapping uint32 registers,
+// which is exact modulo 2^32.
 constexpr int kTileS8M = 128;
+constexpr int kChunkS8Stages = 640;
 constexpr int kTileS8N = 128;
 __device__ __forceinline__ constexpr int fragA8(int p, int rb, int kbl) { return ((p * 4 + rb) * 2 + kbl) * kFragBytes; }
 __device__ __forceinline__ constexpr int fragB8(int p, int cb, int kbl) { return (24 + (p * 4 + cb) * 2 + kbl) * kFragBytes; }
@@ -186,26 +192,19 @@ __global__ __launch_bounds__(512, 1) void k_gemm_s8(
                                                kBufferWord3);
   }
   const int lane16 = lane * 16;
-  auto dma = [&](int st, int j) {
-    dma16_buf(src[j], (uint32_t)lane16, (uint32_t)(st * 2 * kFragBytes),
-              lds + (st % kRing) * kStageBytes + (wave * kDmaPerWave + j) * kFragBytes);
+  int st0 = 0;   // first stage of the current chunk
+  // copy of chunk stage s (LDS slot s % kRing, k stage st0 + s)
+  auto dma = [&](int s, int j) {
+    dma16_buf(src[j], (uint32_t)lane16, (uint32_t)((st0 + s) * 2 * kFragBytes),
+              lds + (s % kRing) * kStageBytes + (wave * kDmaPerWave + j) * kFragBytes);
   };
 
   v16f acc[5][2];
+  uint32_t out[2][16];
 #pragma unroll
-  for (int a = 0; a < 5; ++a)
+  for (int i = 0; i < 2; ++i)
 #pragma unroll
-    for (int i = 0; i < 2; ++i)
-#pragma unroll
-      for (int v = 0; v < 16; ++v) acc[a][i][v] = 0.0f;
-
-#pragma unroll
-  for (int j = 0; j < kDmaPerWave; ++j) dma(0, j);
-#pragma unroll
-  for (int j = 0; j < kDmaPerWave; ++j) dma(1, j);   // nst >= 2 by padding
-  wait_vm_lgkm0<kDmaPerWave>();   // stage 0 landed
-  block_sync();
-
+    for (int v = 0; v < 16; ++v) out[i][v] = 0u;
   v4i a[3][2], b[3];
   auto read_frags = [&](const uint8_t* sb, int kbl) {
 #pragma unroll
@@ -260,39 +259,64 @@ __global__ __launch_bounds__(512, 1) void k_gemm_s8(
     __builtin_amdgcn_sched_barrier(0);
   };
 
-  int s = 0;
-  for (; s + 2 < nst; ++s) {
-    stage_body(s, true);
-    wait_vm_lgkm0<kDmaPerWave>();  // stage s + 1 landed; reads of stage s done
+  const int nch = (nst + kChunkS8Stages - 1) / kChunkS8Stages;
+  const int cbase = nst / nch, crem = nst - cbase * nch;   // chunk lengths
+  for (int c = 0; c < nch; ++c) {
+    const int len = cbase + (c < crem ? 1 : 0);   // >= 3: one chunk, or >= 320
+#pragma unroll
+    for (int e = 0; e < 5; ++e)
+#pragma unroll
+      for (int i = 0; i < 2; ++i)
+#pragma unroll
+        for (int v = 0; v < 16; ++v) acc[e][i][v] = 0.0f;
+    if (c > 0) {   // every wave has finished reading the previous chunk's slots
+      wait_vm_lgkm0<0>();
+      block_sync();
+    }
+#pragma unroll
+    for (int j = 0; j < kDmaPerWave; ++j) dma(0, j);
+#pragma unroll
+    for (int j = 0; j < kDmaPerWave; ++j) dma(1, j);
+    wait_vm_lgkm0<kDmaPerWave>();   // stage 0 landed
+    block_sync();
+
+    int s = 0;
+    for (; s + 2 < len; ++s) {
+      stage_body(s, true);
+      wait_vm_lgkm0<kDmaPerWave>();  // stage s + 1 landed; reads of stage s done
+      block_sync();
+      mfma_tail();
+      __builtin_amdgcn_sched_barrier(0);
+    }
+    stage_body(s, false);
+    wait_vm_lgkm0<0>();
     block_sync();
     mfma_tail();
     __builtin_amdgcn_sched_barrier(0);
-  }
-  stage_body(s, false);
-  wait_vm_lgkm0<0>();
-  block_sync();
-  mfma_tail();
-  __builtin_amdgcn_sched_barrier(0);
-  stage_body(s + 1, false);
-  mfma_tail();
+    stage_body(s + 1, false);
+    mfma_tail();
 
-  // compose every output first (the other four accumulator sets die), then
-  // store with the bounds check
-  uint32_t out[2][16];
+    // add this chunk's sum_g 13^g 4 G_g into the wrapping outputs (each
+    // 4 G_g exact below 2^24)
+#pragma unroll
+    for (int i = 0; i < 2; ++i)
+#pragma unroll
+      for (int v = 0; v < 16; ++v) {
+        uint32_t x = (uint32_t)(int)(4.0f * acc[0][i][v]);
+        x += 13u * (uint32_t)(int)(4.0f * acc[1][i][v]);
+        x += 169u * (uint32_t)(int)(4.0f * acc[2][i][v]);
+        x += 2197u * (uint32_t)(int)(4.0f * acc[3][i][v]);
+        x += 28561u * (uint32_t)(int)(4.0f * acc[4][i][v]);
+        out[i][v] += x;
+      }
+    st0 += len;
+  }
+  // keeps the composition (and the MFMAs it reads) ahead of the guarded
+  // stores below instead of sunk into their branches
 #pragma unroll
   for (int i = 0; i < 2; ++i)
 #pragma unroll
-    for (int v = 0; v < 16; ++v) {
-      uint32_t c = (uint32_t)(int)(4.0f * acc[0][i][v]);
-      c += 13u * (uint32_t)(int)(4.0f * acc[1][i][v]);
-      c += 169u * (uint32_t)(int)(4.0f * acc[2][i][v]);
-      c += 2197u * (uint32_t)(int)(4.0f * acc[3][i][v]);
-      c += 28561u * (uint32_t)(int)(4.0f * acc[4][i][v]);
-      out[i][v] = c;
-      // keeps the composition (and the MFMAs it reads) ahead of the guarded
-      // stores below instead of sunk into their branches
-      asm volatile("" ::"v"(out[i][v]));
-    }
+    for (int v = 0; v < 16; ++v) asm volatile("" ::"v"(out[i][v]));
   const int64_t col = tn * kTileS8N + wn * 32 + (lane & 31);
   const int64_t row0 = tm * kTileS8M + wm * 64 + (lane >> 5) * 4;
 #pragma unroll

@@ -24,9 +24,10 @@ def test_igemm_s8_bit_exact(gpu_lib, m, n, k):
     assert np.array_equal(C, want)
 
 
-def test_igemm_s8_extremes_at_max_k(gpu_lib):
+def test_igemm_s8_extremes_at_the_fp32_limit(gpu_lib):
     """All -128 (the largest limb products) at k = 87381, the FP32-exactness
-    limit of the grouped accumulators; plus mixed signs."""
+    limit of one grouped accumulation (the library runs it as two chunks);
+    plus mixed signs."""
     k = 87381
     A = np.full((128, k), -128, dtype=np.int8)
     B = np.full((k, 64), -128, dtype=np.int8)
@@ -35,6 +36,23 @@ def test_igemm_s8_extremes_at_max_k(gpu_lib):
     A[:, -1] = 1
     want = o.igemm_s8(A, B)
     announce(f"igemm_s8 extremes k={k}")
+    C = to_np(gpu_lib.igemm_s8(dev_cm(A), dev_cm(B)))
+    assert np.array_equal(C, want)
+
+
+def test_igemm_s8_long_k_chunks_and_wraps(gpu_lib):
+    """k = 200000: three accumulation chunks, and with every value -128 the
+    exact products reach 2^31.6, so C must wrap modulo 2^32 like INT32
+    accumulation; mixed signs and a ragged shape around it."""
+    k = 200000
+    A = np.full((70, k), -128, dtype=np.int8)
+    B = np.full((k, 40), -128, dtype=np.int8)
+    A[1::3, :] = 127
+    B[:, 2::5] = 3
+    A[5, ::7] = -1
+    want = o.igemm_s8(A, B)
+    assert np.abs(A[:1].astype(np.int64) @ B[:, :1].astype(np.int64)).max() > 2 ** 31
+    announce(f"igemm_s8 k={k}")
     C = to_np(gpu_lib.igemm_s8(dev_cm(A), dev_cm(B)))
     assert np.array_equal(C, want)
 

@@ -158,7 +158,7 @@ def test_dgemm_empty_is_noop(lib):
 @pytest.mark.parametrize("args,code", [
     ((4, 4, 4, 1, 3, 1, 4, 1, 4), ozfp4.OZFP4_EINVAL),
     ((4, 4, 4, 1, 4, 1, 4, 0, 4), ozfp4.OZFP4_EINVAL),               # null C
-    ((4, 4, 87382, 1, 4, 1, 87382, 1, 4), ozfp4.OZFP4_EKBOUND),
+    ((4, 4, 16777217, 1, 4, 1, 16777217, 1, 4), ozfp4.OZFP4_EKBOUND),
 ])
 def test_igemm_argument_errors_on_host(lib, args, code):
     assert ozfp4.ozfp4_igemm_s8(*args) == code
