@@ -14,7 +14,7 @@ the INT8-on-FP4 path as context.
 
 Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--moduli L]
                        [--size N] [--sweep] [--no-cpu-baseline] [--no-native] [--no-karatsuba]
-                       [--no-phi4] [--no-ozi] [--no-sgemm]
+                       [--no-phi4] [--no-ozi] [--no-sgemm] [--no-table1]
 """
 
 from __future__ import annotations
@@ -45,6 +45,11 @@ MEASURED_TRAFFIC = {
     "read_GB": 154.6, "write_GB": 4.87,
 }
 SEED = 20260806
+
+# The paper's own configuration (19 moduli) as its Table I prints it for
+# OzII-FP4 on an RTX PRO 6000 Blackwell: (compute stage, total) equivalent
+# TFLOP/s per N. Context for the same configuration here, not a target.
+PAPER_TABLE1_TFLOPS = {4096: (16.28, 10.81), 8192: (17.11, 13.52), 16384: (17.31, 15.26)}
 
 
 GEMM_SOURCES = (  # (file, first line of the section, first line after it)
@@ -178,6 +183,8 @@ def main() -> int:
                     help="skip Ozaki scheme I (15 limbs) and its bitwise check against scheme II")
     ap.add_argument("--no-sgemm", action="store_true",
                     help="skip the FP32 emulation (ozfp4_sgemm) and native FP32 on FP32 copies of the inputs")
+    ap.add_argument("--no-table1", action="store_true",
+                    help="skip the paper's configuration (19 moduli) at N = 4096, 8192, 16384")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="also run a plain 1 GiB device copy (reference for HBM byte counters)")
     args = ap.parse_args()
@@ -355,6 +362,34 @@ def main() -> int:
                                                                      C19.view(torch.int64)))}
         log(json.dumps(result["ozi"]))
         del C19
+        torch.cuda.empty_cache()
+
+    if not args.no_table1:
+        # the paper's configuration at its three sizes: "compute" is the
+        # residue GEMM plus the CRT (the paper's compute stage), "total" the
+        # whole call
+        log("paper configuration (19 moduli) at N = 4096, 8192, 16384")
+        rows1 = []
+        for N1 in sorted(PAPER_TABLE1_TFLOPS):
+            if N1 == N:
+                A1d, B1d, C1 = Ad, Bd, C
+            else:
+                A1, B1 = dgemm_inputs(N1, N1, N1, 0.5, SEED + 3)
+                A1d, B1d = dev_cm(A1, torch), dev_cm(B1, torch)
+                C1 = torch.empty_strided((N1, N1), (1, N1), dtype=torch.float64, device="cuda")
+            reps = max(5, int(2000 // (N1 / 1024) ** 3))
+            t1, st1 = time_call(ozfp4, torch, lambda: ozfp4.dgemm(A1d, B1d, 19, out=C1), reps, 2)
+            f1 = 2.0 * N1 ** 3
+            comp, total = PAPER_TABLE1_TFLOPS[N1]
+            rows1.append({"n": N1, "ms": t1, "tflops_total": f1 / t1 / 1e9,
+                          "tflops_compute": f1 / (st1[3] + st1[4]) / 1e9,
+                          "paper_tflops_compute": comp, "paper_tflops_total": total})
+            log(json.dumps(rows1[-1]))
+            if N1 != N:
+                del A1d, B1d, C1
+        result["table1"] = {"workload": "dgemm m=n=k=N, phi=0.5, 19 moduli (the paper's configuration)",
+                            "paper": "Table I, OzII-FP4, RTX PRO 6000 Blackwell (other hardware)",
+                            "runs": rows1}
         torch.cuda.empty_cache()
 
     if not args.no_sgemm:
