@@ -192,7 +192,7 @@ def main() -> int:
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
         print("bench.py measures one GPU: this method has no multi-GPU path "
-              "(the output tiles and moduli would shard without communication; see DESIGN.md)",
+              "(its output tiles and moduli would shard without communication)",
               file=sys.stderr)
         return 2
 
