@@ -79,3 +79,18 @@ def test_igemm_s8_8192_rows_sampled(gpu_lib):
     got_cols = to_np(Cd[:, torch.as_tensor(cols, device="cuda")])
     assert np.array_equal(got_rows, o.igemm_s8(A[rows], B))
     assert np.array_equal(got_cols, o.igemm_s8(A, B[:, cols]))
+
+
+def test_igemm_s8_equals_native_int8_matrix_cores(gpu_lib):
+    """The FP4-limb product equals the GPU's own INT8 matrix product
+    (torch._int_mm, int32 accumulation) bit for bit, including results that
+    wrap modulo 2^32."""
+    import torch
+    A, B = int8_inputs(256, 192, 4096, SEED + 2)
+    A[:3, :] = -128
+    B[:, :2] = -128
+    announce("igemm_s8 against native int8 256x192x4096")
+    C = gpu_lib.igemm_s8(dev_cm(A), dev_cm(B))
+    native = torch._int_mm(torch.from_numpy(A).cuda(), torch.from_numpy(np.ascontiguousarray(B)).cuda())
+    assert torch.equal(C, native)
+    assert np.array_equal(to_np(C), o.igemm_s8(A, B))
