@@ -296,10 +296,12 @@ def main() -> int:
         result["copy_calibration_bytes"] = {"read": src.numel() * 8, "write": dst.numel() * 8}
         del src, dst
 
+    ref_block = None
     if not args.no_accuracy:
         rows = np.arange(0, N, N // 128)[:128]
         cols = np.arange(0, N, N // 128)[:128]
-        bits, worst = accuracy_bits(block_of(C, rows, cols, torch), exact_reference(A, B, rows, cols))
+        ref_block = exact_reference(A, B, rows, cols)
+        bits, worst = accuracy_bits(block_of(C, rows, cols, torch), ref_block)
         result["accuracy"] = {"block": "128x128 (every N/128-th row and column)",
                               "error_bits": bits, "max_normalized_error": worst,
                               "fp64_accurate": worst <= 2.0 ** -50}
@@ -319,6 +321,12 @@ def main() -> int:
         nms = (time.perf_counter() - t0) * 1e3 / reps
         result["native_fp64"] = {"ms": nms, "tflops": 2.0 * N ** 3 / nms / 1e9,
                                  "speedup_of_emulation": nms / ms}
+        if ref_block is not None:
+            # native FP64 accumulates rounding errors along k; same block
+            Cn = torch.matmul(Ar, Br)
+            nbits, nworst = accuracy_bits(block_of(Cn, rows, cols, torch), ref_block)
+            result["native_fp64"].update({"error_bits": nbits, "max_normalized_error": nworst})
+            del Cn
         del Ar, Br
 
     if not args.no_karatsuba:
