@@ -287,6 +287,21 @@ def main() -> int:
         "compute_stage_tflops": 2.0 * N ** 3 / (gemm_ms + stages[4]) / 1e9,
     }
 
+    # the paper's runtime model with measured rates: beta from a plain 1 GiB
+    # device copy (read + write bytes over time), R from the GEMM stage
+    src = torch.empty(1 << 27, dtype=torch.float64, device="cuda").fill_(1.0)
+    dst = torch.empty_like(src)
+    dst.copy_(src)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(5):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    beta = 2.0 * src.numel() * 8 * 5 / (time.perf_counter() - t0) / 1e9
+    result["hbm_copy_GBs"] = beta
+    result["model_ms_measured"] = gemm_ms + D / (beta * 1e9) * 1e3
+    del src, dst
+
     if args.copy_calibration:
         src = torch.empty(1 << 27, dtype=torch.float64, device="cuda").fill_(1.0)
         dst = torch.empty_like(src)

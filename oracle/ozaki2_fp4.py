@@ -49,6 +49,7 @@ __all__ = [
     "round_scaled", "dgemm", "dgemm_definition", "int8_limbs", "igemm_s8",
     "igemm_s8_limbs", "fp32_exact_bound", "fp32_accumulate_emulated",
     "exact_product_entry", "normalized_error", "exact_block", "normalized_errors_block",
+    "quantization_error_bound",
     "MAX_K_FP32",
 ]
 
@@ -719,6 +720,38 @@ def exact_block(A: np.ndarray, B: np.ndarray, rows, cols):
             out_p[i, j] = Fraction(int(prod[i, j])) * scale
             out_a[i, j] = Fraction(int(absum[i, j])) * scale
     return out_p, out_a
+
+
+def quantization_error_bound(A: np.ndarray, B: np.ndarray, s, t, x, rows, cols) -> np.ndarray:
+    """A-priori bound on |C_ij - (AB)_ij| for the block (rows, cols), from
+    the shared-exponent conversion (Sec. IV-B) and the final rounding.
+
+    With A = A~ 2^-s + dA and B = B~ 2^-t + dB, |dA_ik| <= 2^(-s_i - 1) and
+    |dB_kj| <= 2^(-t_j - 1) (round to nearest integer at the line's scale),
+    AB - A~ B~ 2^-(s+t) = dA B + (A~ 2^-s) dB, so
+      |C - AB| <= u |x 2^-(s_i+t_j)| + 2^(-s_i-1) sum_k |B_kj|
+                  + 2^(-t_j-1) sum_k |A_ik| + k 2^(-s_i-t_j-2),
+    u = 2^-53, plus 2^-1075 for a subnormal result. `s`, `t` and `x` (the
+    exact integer product) are those of the block, as ``dgemm`` returns
+    them. Sums of |A|, |B| are correctly rounded (math.fsum) and the bound
+    is inflated by 2^-40 relative, so it is a safe upper bound in FP64."""
+    A = np.asarray(A, dtype=np.float64)
+    B = np.asarray(B, dtype=np.float64)
+    k = A.shape[1]
+    rows = np.asarray(rows)
+    cols = np.asarray(cols)
+    sa = [math.fsum(np.abs(A[i, :])) for i in rows]
+    sb = [math.fsum(np.abs(B[:, j])) for j in cols]
+    out = np.empty((len(rows), len(cols)), dtype=np.float64)
+    for a in range(len(rows)):
+        for b in range(len(cols)):
+            si, tj = int(s[a]), int(t[b])
+            val = abs(Fraction(int(x[a, b])) / Fraction(2) ** (si + tj))
+            bound = (Fraction(1, 2 ** 53) * val + Fraction(sb[b]) / Fraction(2) ** (si + 1)
+                     + Fraction(sa[a]) / Fraction(2) ** (tj + 1)
+                     + Fraction(k) / Fraction(2) ** (si + tj + 2) + Fraction(1, 2 ** 1075))
+            out[a, b] = float(bound * (1 + Fraction(1, 2 ** 40)))
+    return out
 
 
 def normalized_errors_block(C_block: np.ndarray, A: np.ndarray, B: np.ndarray, rows, cols) -> np.ndarray:

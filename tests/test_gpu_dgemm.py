@@ -247,3 +247,11 @@ def test_dgemm_wide_range_sampled(gpu_lib):
     rows = np.sort(rng.choice(8192, 8, replace=False))
     cols = np.sort(rng.choice(8192, 8, replace=False))
     _sampled_check(gpu_lib, A, B, 19, rows, cols)
+    want = o.dgemm(A, B, 19, rows=rows, cols=cols)
+    bound = o.quantization_error_bound(A, B, want["s"], want["t"], want["x"], rows, cols)
+    exact, _ = o.exact_block(A, B, rows, cols)
+    from fractions import Fraction
+    for i in range(len(rows)):
+        for j in range(len(cols)):
+            err = abs(Fraction(float(want["C"][i, j])) - exact[i, j])
+            assert err <= Fraction(float(bound[i, j])), (i, j)

@@ -627,3 +627,35 @@ def test_normalized_errors_block_matches_single_entry():
     for i in range(3):
         for j in range(3):
             assert got[i, j] == o.normalized_error(C[i, j], A, B, i, j)
+
+
+# ---------------------------------------------------------------- Sec. IV-B error bound
+
+@pytest.mark.parametrize("phi,seed", [(4.0, 1), (8.0, 2), (0.5, 3)])
+def test_quantization_bound_holds_exactly(phi, seed):
+    """|C - AB| against the exact product stays within the a-priori bound of
+    the shared-exponent conversion on every element (wide exponent spread)."""
+    from paper_2608_06812_amd.workloads import dgemm_inputs
+    A, B = dgemm_inputs(12, 10, 300, phi, seed)
+    res = o.dgemm(A, B, 19)
+    rows, cols = np.arange(12), np.arange(10)
+    bound = o.quantization_error_bound(A, B, res["s"], res["t"], res["x"], rows, cols)
+    exact, _ = o.exact_block(A, B, rows, cols)
+    for i in range(12):
+        for j in range(10):
+            err = abs(Fraction(float(res["C"][i, j])) - exact[i, j])
+            assert err <= Fraction(float(bound[i, j]))
+
+
+def test_quantization_bound_is_attained_by_a_half_unit_loss():
+    """A row whose small element sits exactly half a unit of the row's
+    scale below an integer loses exactly that half unit (ties to even):
+    the bound's A term is reached up to the other terms."""
+    k = 4
+    A = np.array([[1.0, 2.0 ** -53, 0.0, 0.0]])          # s = 52: 2^-53 -> 0.5 -> rounds to 0
+    B = np.array([[0.0], [1.0], [0.0], [0.0]])
+    res = o.dgemm(A, B, 19)
+    assert int(res["s"][0]) == 52 and int(res["Ai"][0, 1]) == 0
+    err = abs(float(res["C"][0, 0]) - 2.0 ** -53)
+    bound = o.quantization_error_bound(A, B, res["s"], res["t"], res["x"], [0], [0])[0, 0]
+    assert err == 2.0 ** -53 and err <= bound <= 4 * err
