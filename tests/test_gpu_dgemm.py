@@ -255,3 +255,20 @@ def test_dgemm_wide_range_sampled(gpu_lib):
         for j in range(len(cols)):
             err = abs(Fraction(float(want["C"][i, j])) - exact[i, j])
             assert err <= Fraction(float(bound[i, j])), (i, j)
+
+
+@pytest.mark.slow
+@pytest.mark.parametrize("phi,key", [(0, "accuracy_bits_phi0"), (32, "accuracy_bits_phi32")])
+def test_paper_accuracy_experiment(gpu_lib, paper, phi, key):
+    """Sec. VII-A: the paper's input law at K = 8192, a whole 128 x 128
+    output, 19 moduli; the maximum normalized error over all 16384 outputs
+    (exact reference) is within 0.75 bit of the printed value."""
+    import math
+    A, B = paper_law_inputs(128, 128, 8192, phi, SEED + 60 + phi)
+    announce(f"dgemm paper accuracy phi={phi}")
+    C = to_np(gpu_lib.dgemm(dev_cm(A), dev_cm(B), 19))
+    assert bits_equal(C[:4, :4], o.dgemm(A, B, 19, rows=np.arange(4), cols=np.arange(4))["C"])
+    err = o.normalized_errors_block(C, A, B, np.arange(128), np.arange(128)).max()
+    bits = -math.log2(err)
+    announce(f"phi={phi}: {bits:.2f} bits (paper {paper[key]})")
+    assert abs(bits - paper[key]) <= 0.75
