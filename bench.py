@@ -41,7 +41,7 @@ METRIC = "emulated DGEMM TFLOPS at N=16384 + % of FP4 MFMA peak, 1xMI355X"
 # (profiles/k_gemm_res_dgemm_16384_L18.md). Valid only for the GEMM source
 # they were taken on, identified by the hash of its section of kernels.hpp.
 MEASURED_TRAFFIC = {
-    "kernel_source_sha256_16": "87c72f0392169584",
+    "kernel_source_sha256_16": "90015c698430d2c5",
     "workload": (16384, 16384, 16384, 18),
     "read_GB": 154.6, "write_GB": 4.87,
 }

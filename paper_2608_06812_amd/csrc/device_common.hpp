@@ -7,7 +7,7 @@
 //   * limb planes: per operand, plane p holds one limb of one modulus for
 //     every (line, k); it is a sequence of 1 KiB fragments of 32 lines x 64 k
 //     in the exact register order of the A/B operand of
-//     v_mfma_scale_f32_32x32x64_f8f6f4 in FP4 mode (lane = line % 32 +
+//     v_mfma_f32_32x32x64_f8f6f4 in FP4 mode (lane = line % 32 +
 //     32 * (k / 32 % 2), 16 bytes per lane, two E2M1 codes per byte, low
 //     nibble first). A wave therefore moves a fragment with one 16-byte
 //     load per lane, coalesced in HBM and conflict-free in LDS. Fragments
@@ -234,8 +234,12 @@ __device__ __forceinline__ void tile_coords(int64_t bid, int64_t nblocks, int64_
 __device__ __forceinline__ v16f mfma_fp4(v4i a, v4i b, v16f c) {
   v8i a8 = {a.x, a.y, a.z, a.w, 0, 0, 0, 0};
   v8i b8 = {b.x, b.y, b.z, b.w, 0, 0, 0, 0};
-  // cbsz = blgp = 4: both operands E2M1; E8M0 scales 127 = 2^0
-  return __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(a8, b8, c, 4, 4, 0, 127, 0, 127);
+  // cbsz = blgp = 4: both operands E2M1. Constant zero scale operands make
+  // the compiler emit the unscaled v_mfma_f32_32x32x64_f8f6f4, which
+  // multiplies by 2^0 (bitwise equal to the scaled form with E8M0 127) and
+  // takes no scale register, so it issues with fewer gaps (about 1 % faster
+  // GEMMs at the same clock).
+  return __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(a8, b8, c, 4, 4, 0, 0, 0, 0);
 }
 
 // Raw 32-bit data format of untyped buffer loads: dword 3 of a buffer
