@@ -41,7 +41,7 @@ METRIC = "emulated DGEMM TFLOPS at N=16384 + % of FP4 MFMA peak, 1xMI355X"
 # (profiles/k_gemm_res_dgemm_16384_L18.md). Valid only for the GEMM source
 # they were taken on, identified by the hash of its section of kernels.hpp.
 MEASURED_TRAFFIC = {
-    "kernel_source_sha256_16": "90015c698430d2c5",
+    "kernel_source_sha256_16": "9bebb506c97596dd",
     "workload": (16384, 16384, 16384, 18),
     "read_GB": 154.6, "write_GB": 4.87,
 }
@@ -59,17 +59,26 @@ GEMM_SOURCES = (  # (file, first line of the section, first line after it)
 )
 
 
+def code_only(text: str) -> str:
+    """C++ source without its comments, white space collapsed: what the
+    compiler sees, so that editing a comment keeps the hash."""
+    import re
+    text = re.sub(r"/\*.*?\*/", " ", text, flags=re.S)
+    text = re.sub(r"//[^\n]*", " ", text)
+    return " ".join(text.split())
+
+
 def kernel_source_hash() -> str:
-    """sha256 (16 hex digits) of the residue GEMM's source: the tile mapping,
-    the MFMA and LDS-DMA helpers and the block tiles (device_common.hpp), and
-    the kernel itself (kernels.hpp)."""
+    """sha256 (16 hex digits) of the code of the residue GEMM (comments and
+    white space ignored): the tile mapping, the MFMA and LDS-DMA helpers and
+    the block tiles (device_common.hpp), and the kernel itself (kernels.hpp)."""
     import hashlib
     h = hashlib.sha256()
     for name, start, end in GEMM_SOURCES:
         with open(os.path.join(ROOT, "paper_2608_06812_amd", "csrc", name), encoding="utf-8") as f:
             text = f.read()
         a = text.index(start)
-        h.update(text[a:text.index(end) if end else len(text)].encode())
+        h.update(code_only(text[a:text.index(end) if end else len(text)]).encode())
     return h.hexdigest()[:16]
 
 

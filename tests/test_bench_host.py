@@ -55,3 +55,11 @@ def test_accuracy_bits_against_the_exact_block():
     assert bits >= 52 and worst <= 2.0 ** -52
     bits_native, _ = bench.accuracy_bits((A.astype(np.float32) @ B.astype(np.float32)).astype(np.float64), ref)
     assert bits_native < bits
+
+
+def test_source_hash_ignores_comments_but_not_code():
+    code = "int f(int x) {\n  // a comment\n  return x + 1; /* another */\n}\n"
+    assert bench.code_only(code) == bench.code_only(code.replace("a comment", "edited"))
+    assert bench.code_only(code) == bench.code_only(code.replace("\n  ", "\n    "))
+    assert bench.code_only(code) != bench.code_only(code.replace("x + 1", "x + 2"))
+    assert "comment" not in bench.code_only(code) and "another" not in bench.code_only(code)
