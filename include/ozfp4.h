@@ -22,6 +22,9 @@
  *     that workspace.
  *   - Every entry point returns OZFP4_OK (0) or a negative error code; argument
  *     errors are detected on the host before any GPU work is issued.
+ *   - Each product of two of m, n, k is at most OZFP4_MAX_ELEMENTS (else
+ *     OZFP4_EINVAL): no larger matrix fits in device memory, and the bound
+ *     keeps every size the library computes within 64 bits.
  */
 #ifndef OZFP4_H
 #define OZFP4_H
@@ -53,6 +56,8 @@ extern "C" {
  * int32, so any k up to this limit (set by 32-bit buffer offsets) is exact
  * modulo 2^32. */
 #define OZFP4_MAX_K_S8  16777216
+/* Largest product of two of m, n, k (2^48). */
+#define OZFP4_MAX_ELEMENTS ((int64_t)1 << 48)
 
 /*
  * ozfp4_dgemm -- C = fl(A B) for FP64 A, B by Ozaki scheme II on FP4 limbs

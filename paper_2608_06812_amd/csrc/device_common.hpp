@@ -40,6 +40,17 @@ constexpr int kMinKPad = 384;    // k is padded to at least three stages
 constexpr uint64_t kAbsMask = 0x7fffffffffffffffull;
 constexpr uint64_t kNonFinite = 0x7ff0000000000000ull;
 
+// One launch holds fewer than 2^32 work-items. Kernels with one thread per
+// item take their first item as an argument and the host splits larger
+// counts into launches of kLaunchThreads threads; grid-stride kernels take
+// at most kLaunchThreads / 256 blocks of 256.
+constexpr int64_t kLaunchThreads = int64_t(1) << 30;
+inline unsigned stride_blocks(int64_t items, int64_t per) {
+  const int64_t b = items / per + (items % per != 0);
+  const int64_t cap = kLaunchThreads / 256;
+  return (unsigned)(b < cap ? b : cap);
+}
+
 // ------------------------------------------------------------ Sec. IV-B
 // floor(log2 |x|) from the bit pattern of the line maximum |x| (finite,
 // nonzero), subnormals included; shift c - 1 - e, or 0 for a zero line.

@@ -14,14 +14,18 @@ __global__ void k_fill_u64(uint64_t* __restrict__ p, int64_t n, uint64_t v) {
   if (i < n) p[i] = v;
 }
 
+// Matrix fills stride over the grid, so a bounded grid covers any m x n
+// (one launch holds fewer than 2^32 work-items).
 __global__ void k_fill_f64_matrix(double* __restrict__ C, int64_t m, int64_t n, int64_t ldc) {
-  int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (t < m * n) C[(t % m) + (t / m) * ldc] = 0.0;
+  const int64_t total = m * n, stride = (int64_t)gridDim.x * blockDim.x;
+  for (int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; t < total; t += stride)
+    C[(t % m) + (t / m) * ldc] = 0.0;
 }
 
 __global__ void k_fill_i32_matrix(int32_t* __restrict__ C, int64_t m, int64_t n, int64_t ldc) {
-  int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (t < m * n) C[(t % m) + (t / m) * ldc] = 0;
+  const int64_t total = m * n, stride = (int64_t)gridDim.x * blockDim.x;
+  for (int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; t < total; t += stride)
+    C[(t % m) + (t / m) * ldc] = 0;
 }
 
 // Row maxima of |X| for lines that are adjacent in memory (X[line + kk*ld]):
@@ -54,8 +58,8 @@ __global__ __launch_bounds__(256) void k_amax_adjacent_lines(
 constexpr int kAmaxContigChunk = 4096;
 __global__ __launch_bounds__(256) void k_amax_contig_lines(
     const double* __restrict__ X, int64_t ld, int64_t lines, int64_t k,
-    unsigned long long* __restrict__ amax, int* __restrict__ flag) {
-  int64_t line = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+    unsigned long long* __restrict__ amax, int* __restrict__ flag, int64_t line0) {
+  int64_t line = line0 + (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
   int lane = threadIdx.x & 63;
   if (line >= lines) return;
   int64_t k0 = (int64_t)blockIdx.y * kAmaxContigChunk;
@@ -332,14 +336,15 @@ __global__ __launch_bounds__(512, 1) void k_gemm_s8(
 // modulus and accumulates the exact chunk sums sig_c = sum_l r_l w_l,c
 // (Sec. V-B). The quotient q = rint(S / P) comes from the chunk sums,
 // then every element is reconstructed and rounded once. NC = number of
-// 42-bit chunks (3 for up to 19 moduli, 4 for 20).
+// 42-bit chunks (3 for up to 19 moduli, 4 for 20). t0 is the first thread
+// index of the launch (large outputs take several launches).
 template <int NC>
 __global__ __launch_bounds__(256) void k_crt(
     const uint8_t* __restrict__ R, int64_t ldr, int64_t rplane, int64_t m, int64_t n,
     const uint64_t* __restrict__ amaxA, const uint64_t* __restrict__ amaxB, int cA, int cB,
-    const CrtConst* __restrict__ cc, double* __restrict__ C, int64_t ldc) {
+    const CrtConst* __restrict__ cc, double* __restrict__ C, int64_t ldc, int64_t t0) {
   const int64_t rows4 = (m + 3) >> 2;
-  const int64_t t = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  const int64_t t = t0 + (int64_t)blockIdx.x * 256 + threadIdx.x;
   if (t >= rows4 * n) return;
   const int64_t j = t / rows4;
   const int64_t i0 = (t - j * rows4) * 4;

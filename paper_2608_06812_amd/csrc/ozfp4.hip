@@ -66,6 +66,37 @@ inline int64_t plane_k_pad(int64_t k) {
     if ((expr) != hipSuccess) return OZFP4_EHIP;       \
   } while (0)
 
+// Frees whatever the state holds (with its device current) and resets it.
+void release_device(DeviceState& d) {
+  (void)hipFree(d.ws);
+  (void)hipFree(d.d_mod);
+  (void)hipFree(d.d_crt);
+  (void)hipFree(d.d_lut);
+  (void)hipFree(d.d_lut_k);
+  (void)hipFree(d.d_lut8);
+  if (d.h_flag) (void)hipHostFree(d.h_flag);
+  for (int e = 0; e <= kMaxStages; ++e)
+    if (d.ev[e]) (void)hipEventDestroy(d.ev[e]);
+  d = DeviceState();
+}
+
+int init_device(DeviceState& d, const HostTables* T) {
+  HIP_TRY(hipMalloc(&d.d_mod, sizeof(ModConst)));
+  HIP_TRY(hipMalloc(&d.d_crt, sizeof(CrtConst) * (kMaxModuli + 1)));
+  HIP_TRY(hipMalloc(&d.d_lut, T->lut.size() * sizeof(uint16_t)));
+  HIP_TRY(hipMalloc(&d.d_lut_k, T->lut_k.size() * sizeof(uint32_t)));
+  HIP_TRY(hipMalloc(&d.d_lut8, sizeof(T->lut8)));
+  HIP_TRY(hipMemcpy(d.d_mod, &T->mod, sizeof(ModConst), hipMemcpyHostToDevice));
+  HIP_TRY(hipMemcpy(d.d_crt, T->crt, sizeof(CrtConst) * (kMaxModuli + 1), hipMemcpyHostToDevice));
+  HIP_TRY(hipMemcpy(d.d_lut, T->lut.data(), T->lut.size() * sizeof(uint16_t), hipMemcpyHostToDevice));
+  HIP_TRY(hipMemcpy(d.d_lut_k, T->lut_k.data(), T->lut_k.size() * sizeof(uint32_t),
+                    hipMemcpyHostToDevice));
+  HIP_TRY(hipMemcpy(d.d_lut8, T->lut8, sizeof(T->lut8), hipMemcpyHostToDevice));
+  HIP_TRY(hipHostMalloc(reinterpret_cast<void**>(&d.h_flag), sizeof(int), hipHostMallocDefault));
+  for (int i = 0; i <= kMaxStages; ++i) HIP_TRY(hipEventCreate(&d.ev[i]));
+  return OZFP4_OK;
+}
+
 int device_state(DeviceState** out) {
   const HostTables* T = tables();
   if (!T) return OZFP4_EHIP;
@@ -74,19 +105,11 @@ int device_state(DeviceState** out) {
   if (dev < 0 || dev >= kMaxDevices) return OZFP4_EHIP;
   DeviceState& d = g_dev[dev];
   if (!d.ready) {
-    HIP_TRY(hipMalloc(&d.d_mod, sizeof(ModConst)));
-    HIP_TRY(hipMalloc(&d.d_crt, sizeof(CrtConst) * (kMaxModuli + 1)));
-    HIP_TRY(hipMalloc(&d.d_lut, T->lut.size() * sizeof(uint16_t)));
-    HIP_TRY(hipMalloc(&d.d_lut_k, T->lut_k.size() * sizeof(uint32_t)));
-    HIP_TRY(hipMalloc(&d.d_lut8, sizeof(T->lut8)));
-    HIP_TRY(hipMemcpy(d.d_mod, &T->mod, sizeof(ModConst), hipMemcpyHostToDevice));
-    HIP_TRY(hipMemcpy(d.d_crt, T->crt, sizeof(CrtConst) * (kMaxModuli + 1), hipMemcpyHostToDevice));
-    HIP_TRY(hipMemcpy(d.d_lut, T->lut.data(), T->lut.size() * sizeof(uint16_t), hipMemcpyHostToDevice));
-    HIP_TRY(hipMemcpy(d.d_lut_k, T->lut_k.data(), T->lut_k.size() * sizeof(uint32_t),
-                      hipMemcpyHostToDevice));
-    HIP_TRY(hipMemcpy(d.d_lut8, T->lut8, sizeof(T->lut8), hipMemcpyHostToDevice));
-    HIP_TRY(hipHostMalloc(reinterpret_cast<void**>(&d.h_flag), sizeof(int), hipHostMallocDefault));
-    for (int i = 0; i <= kMaxStages; ++i) HIP_TRY(hipEventCreate(&d.ev[i]));
+    if (init_device(d, T) != OZFP4_OK) {  // leave nothing half-made behind
+      (void)hipGetLastError();
+      release_device(d);
+      return OZFP4_EHIP;
+    }
     d.ready = true;
   }
   *out = &d;
@@ -126,9 +149,17 @@ struct DgemmPlan {
 
 size_t align256(size_t v) { return (v + 255) & ~size_t(255); }
 
+// Each product of two dimensions at most OZFP4_MAX_ELEMENTS: then every
+// padded size, plane, residue and partial-sum buffer fits in 64 bits.
+bool dims_ok(int64_t m, int64_t n, int64_t k) {
+  if (m < 0 || n < 0 || k < 0) return false;
+  auto ok = [](int64_t a, int64_t b) { return a == 0 || b <= OZFP4_MAX_ELEMENTS / a; };
+  return ok(m, n) && ok(m, k) && ok(n, k);
+}
+
 int check_dgemm_args(int64_t m, int64_t n, int64_t k, const void* A, int64_t lda, const void* B,
                      int64_t ldb, int n_moduli) {
-  if (m < 0 || n < 0 || k < 0) return OZFP4_EINVAL;
+  if (!dims_ok(m, n, k)) return OZFP4_EINVAL;
   if (lda < std::max<int64_t>(1, m) || ldb < std::max<int64_t>(1, k)) return OZFP4_EINVAL;
   if (n_moduli < OZFP4_MIN_MODULI || n_moduli > OZFP4_MAX_MODULI) return OZFP4_EMODULI;
   if (m > 0 && n > 0 && k > 0) {
@@ -179,6 +210,22 @@ int encode_grid(int64_t nfrag) {
   return (int)std::min<int64_t>(want, 256 * 16);
 }
 
+// Line maxima of the FP64 operands: rows of A (adjacent in memory) and
+// columns of B (contiguous), one wave per column of B in launches of at
+// most kLaunchThreads threads.
+void launch_amax_f64(const double* A, int64_t lda, const double* B, int64_t ldb, int64_t m,
+                     int64_t n, int64_t k, uint64_t* amax_a, uint64_t* amax_b, int* flag) {
+  hipLaunchKernelGGL(k_amax_adjacent_lines, dim3(blocks_for(m, 256), blocks_for(k, kAmaxChunk)),
+                     dim3(256), 0, g_stream, A, lda, m, k,
+                     reinterpret_cast<unsigned long long*>(amax_a), flag);
+  constexpr int64_t kLines = kLaunchThreads / 64;
+  for (int64_t l0 = 0; l0 < n; l0 += kLines)
+    hipLaunchKernelGGL(k_amax_contig_lines,
+                       dim3(blocks_for(std::min(n - l0, kLines), 4), blocks_for(k, kAmaxContigChunk)),
+                       dim3(256), 0, g_stream, B, ldb, n, k,
+                       reinterpret_cast<unsigned long long*>(amax_b), flag, l0);
+}
+
 // Stages of the dgemm pipeline, stopping after `last`:
 // 0 scale, 1 encode A, 2 encode B, 3 residue GEMM, 4 CRT.
 // A, B and C are double, or float when p.f32.
@@ -207,12 +254,7 @@ int run_dgemm(const DgemmPlan& p, DeviceState* d, const void* Av, int64_t lda, c
   if (p.f32) {
     HIP_TRY(launch_amax_f32(g_stream, Af, lda, Bf, ldb, p.m, p.n, p.k, amax_a, amax_b, flag));
   } else {
-    hipLaunchKernelGGL(k_amax_adjacent_lines, dim3(blocks_for(p.m, 256), blocks_for(p.k, kAmaxChunk)),
-                       dim3(256), 0, g_stream, A, lda, p.m, p.k,
-                       reinterpret_cast<unsigned long long*>(amax_a), flag);
-    hipLaunchKernelGGL(k_amax_contig_lines, dim3(blocks_for(p.n, 4), blocks_for(p.k, kAmaxContigChunk)),
-                       dim3(256), 0, g_stream, B, ldb, p.n, p.k,
-                       reinterpret_cast<unsigned long long*>(amax_b), flag);
+    launch_amax_f64(A, lda, B, ldb, p.m, p.n, p.k, amax_a, amax_b, flag);
   }
   HIP_TRY(hipGetLastError());
   record(d, 1);
@@ -288,14 +330,17 @@ int run_dgemm(const DgemmPlan& p, DeviceState* d, const void* Av, int64_t lda, c
     return OZFP4_OK;
   }
   double* C = static_cast<double*>(Cv);
-  if (crt_chunks(L) == 3)
-    hipLaunchKernelGGL(k_crt<3>, dim3(blocks_for(nthreads, 256)), dim3(256), 0, g_stream, R,
-                       p.m_pad, p.m_pad * p.n_pad, p.m, p.n, amax_a, amax_b, p.cA, p.cB,
-                       d->d_crt + L, C, ldc);
-  else
-    hipLaunchKernelGGL(k_crt<4>, dim3(blocks_for(nthreads, 256)), dim3(256), 0, g_stream, R,
-                       p.m_pad, p.m_pad * p.n_pad, p.m, p.n, amax_a, amax_b, p.cA, p.cB,
-                       d->d_crt + L, C, ldc);
+  for (int64_t t0 = 0; t0 < nthreads; t0 += kLaunchThreads) {
+    const unsigned grid = blocks_for(std::min(nthreads - t0, kLaunchThreads), 256);
+    if (crt_chunks(L) == 3)
+      hipLaunchKernelGGL(k_crt<3>, dim3(grid), dim3(256), 0, g_stream, R, p.m_pad,
+                         p.m_pad * p.n_pad, p.m, p.n, amax_a, amax_b, p.cA, p.cB, d->d_crt + L, C,
+                         ldc, t0);
+    else
+      hipLaunchKernelGGL(k_crt<4>, dim3(grid), dim3(256), 0, g_stream, R, p.m_pad,
+                         p.m_pad * p.n_pad, p.m, p.n, amax_a, amax_b, p.cA, p.cB, d->d_crt + L, C,
+                         ldc, t0);
+  }
   HIP_TRY(hipGetLastError());
   record(d, 5);
   return OZFP4_OK;
@@ -321,7 +366,7 @@ struct OziPlan {
 
 int check_ozi_args(int64_t m, int64_t n, int64_t k, const void* A, int64_t lda, const void* B,
                    int64_t ldb, int n_limbs) {
-  if (m < 0 || n < 0 || k < 0) return OZFP4_EINVAL;
+  if (!dims_ok(m, n, k)) return OZFP4_EINVAL;
   if (lda < std::max<int64_t>(1, m) || ldb < std::max<int64_t>(1, k)) return OZFP4_EINVAL;
   if (n_limbs < 1 || n_limbs > OZFP4_OZI_MAX_LIMBS) return OZFP4_EINVAL;
   if (m > 0 && n > 0 && k > 0) {
@@ -370,12 +415,7 @@ int run_ozi(const OziPlan& p, DeviceState* d, const double* A, int64_t lda, cons
   const int64_t nzero = (int64_t)((p.off_flag + 256 - p.off_amax_a) / sizeof(uint64_t));
   hipLaunchKernelGGL(k_fill_u64, dim3(blocks_for(nzero, 256)), dim3(256), 0, g_stream,
                      amax_a, nzero, (uint64_t)0);
-  hipLaunchKernelGGL(k_amax_adjacent_lines, dim3(blocks_for(p.m, 256), blocks_for(p.k, kAmaxChunk)),
-                     dim3(256), 0, g_stream, A, lda, p.m, p.k,
-                     reinterpret_cast<unsigned long long*>(amax_a), flag);
-  hipLaunchKernelGGL(k_amax_contig_lines, dim3(blocks_for(p.n, 4), blocks_for(p.k, kAmaxContigChunk)),
-                     dim3(256), 0, g_stream, B, ldb, p.n, p.k,
-                     reinterpret_cast<unsigned long long*>(amax_b), flag);
+  launch_amax_f64(A, lda, B, ldb, p.m, p.n, p.k, amax_a, amax_b, flag);
   HIP_TRY(hipGetLastError());
   record(d, 1);
   if (last < 1) return OZFP4_OK;
@@ -447,7 +487,7 @@ int ozfp4_dgemm(int64_t m, int64_t n, int64_t k, const double* A, int64_t lda, c
     DeviceState* d;
     rc = device_state(&d);
     if (rc) return rc;
-    hipLaunchKernelGGL(k_fill_f64_matrix, dim3(blocks_for(m * n, 256)), dim3(256), 0, g_stream, C,
+    hipLaunchKernelGGL(k_fill_f64_matrix, dim3(stride_blocks(m * n, 256)), dim3(256), 0, g_stream, C,
                        m, n, ldc);
     HIP_TRY(hipGetLastError());
     return OZFP4_OK;
@@ -463,7 +503,7 @@ int ozfp4_dgemm(int64_t m, int64_t n, int64_t k, const double* A, int64_t lda, c
 
 int ozfp4_igemm_s8(int64_t m, int64_t n, int64_t k, const int8_t* A, int64_t lda, const int8_t* B,
                    int64_t ldb, int32_t* C, int64_t ldc) {
-  if (m < 0 || n < 0 || k < 0) return OZFP4_EINVAL;
+  if (!dims_ok(m, n, k)) return OZFP4_EINVAL;
   if (lda < std::max<int64_t>(1, m) || ldb < std::max<int64_t>(1, k) ||
       ldc < std::max<int64_t>(1, m))
     return OZFP4_EINVAL;
@@ -474,7 +514,7 @@ int ozfp4_igemm_s8(int64_t m, int64_t n, int64_t k, const int8_t* A, int64_t lda
   int rc = device_state(&d);
   if (rc) return rc;
   if (k == 0) {
-    hipLaunchKernelGGL(k_fill_i32_matrix, dim3(blocks_for(m * n, 256)), dim3(256), 0, g_stream, C,
+    hipLaunchKernelGGL(k_fill_i32_matrix, dim3(stride_blocks(m * n, 256)), dim3(256), 0, g_stream, C,
                        m, n, ldc);
     HIP_TRY(hipGetLastError());
     return OZFP4_OK;
@@ -521,7 +561,7 @@ int ozfp4_sgemm(int64_t m, int64_t n, int64_t k, const float* A, int64_t lda, co
     rc = device_state(&d);
     if (rc) return rc;
     // +0.0f has the bit pattern of the int32 zero
-    hipLaunchKernelGGL(k_fill_i32_matrix, dim3(blocks_for(m * n, 256)), dim3(256), 0, g_stream,
+    hipLaunchKernelGGL(k_fill_i32_matrix, dim3(stride_blocks(m * n, 256)), dim3(256), 0, g_stream,
                        reinterpret_cast<int32_t*>(C), m, n, ldc);
     HIP_TRY(hipGetLastError());
     return OZFP4_OK;
@@ -558,7 +598,7 @@ int ozfp4_dgemm_ozi(int64_t m, int64_t n, int64_t k, const double* A, int64_t ld
     DeviceState* d;
     rc = device_state(&d);
     if (rc) return rc;
-    hipLaunchKernelGGL(k_fill_f64_matrix, dim3(blocks_for(m * n, 256)), dim3(256), 0, g_stream, C,
+    hipLaunchKernelGGL(k_fill_f64_matrix, dim3(stride_blocks(m * n, 256)), dim3(256), 0, g_stream, C,
                        m, n, ldc);
     HIP_TRY(hipGetLastError());
     return OZFP4_OK;
@@ -631,15 +671,7 @@ int ozfp4_finalize(void) {
     if (!d.ready) continue;
     if (hipSetDevice(i) != hipSuccess) continue;
     (void)hipDeviceSynchronize();
-    (void)hipFree(d.ws);
-    (void)hipFree(d.d_mod);
-    (void)hipFree(d.d_crt);
-    (void)hipFree(d.d_lut);
-    (void)hipFree(d.d_lut_k);
-    (void)hipFree(d.d_lut8);
-    (void)hipHostFree(d.h_flag);
-    for (int e = 0; e <= kMaxStages; ++e) (void)hipEventDestroy(d.ev[e]);
-    d = DeviceState();
+    release_device(d);
   }
   if (cur >= 0) (void)hipSetDevice(cur);
   return OZFP4_OK;
@@ -649,7 +681,7 @@ const char* ozfp4_strerror(int code) {
   switch (code) {
     case OZFP4_OK: return "success";
     case OZFP4_EINVAL: return "invalid size, leading dimension or null pointer";
-    case OZFP4_EMODULI: return "n_moduli outside [2, 20] or too few moduli for this k";
+    case OZFP4_EMODULI: return "n_moduli outside [2, 27] or too few moduli for this k";
     case OZFP4_EKBOUND: return "k above the FP32-exactness bound";
     case OZFP4_ENONFINITE: return "NaN or Inf in an input matrix";
     case OZFP4_ENOMEM: return "device workspace allocation failed";
@@ -732,7 +764,7 @@ int ozfp4_plane_count(int n_moduli, int32_t* n_planes, int32_t* sum_plane) {
 
 int ozfp4_plane_layout(int64_t lines, int64_t k, int64_t* rows_pad, int64_t* k_pad,
                        int64_t* bytes_per_plane) {
-  if (lines < 0 || k < 0 || !rows_pad || !k_pad || !bytes_per_plane) return OZFP4_EINVAL;
+  if (!dims_ok(lines, 0, k) || !rows_pad || !k_pad || !bytes_per_plane) return OZFP4_EINVAL;
   *rows_pad = round_up(lines, kTile);
   *k_pad = plane_k_pad(k);
   *bytes_per_plane = *rows_pad * *k_pad / 2;

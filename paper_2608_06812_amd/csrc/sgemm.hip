@@ -45,8 +45,8 @@ __global__ __launch_bounds__(256) void k_amax_adjacent_lines_f32(
 constexpr int kAmaxContigChunk32 = 4096;
 __global__ __launch_bounds__(256) void k_amax_contig_lines_f32(
     const float* __restrict__ X, int64_t ld, int64_t lines, int64_t k,
-    unsigned long long* __restrict__ amax, int* __restrict__ flag) {
-  const int64_t line = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+    unsigned long long* __restrict__ amax, int* __restrict__ flag, int64_t line0) {
+  const int64_t line = line0 + (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
   const int lane = threadIdx.x & 63;
   if (line >= lines) return;
   const int64_t k0 = (int64_t)blockIdx.y * kAmaxContigChunk32;
@@ -75,9 +75,9 @@ template <int NC>
 __global__ __launch_bounds__(256) void k_crt_f32(
     const uint8_t* __restrict__ R, int64_t ldr, int64_t rplane, int64_t m, int64_t n,
     const uint64_t* __restrict__ amaxA, const uint64_t* __restrict__ amaxB, int cA, int cB,
-    const CrtConst* __restrict__ cc, float* __restrict__ C, int64_t ldc) {
+    const CrtConst* __restrict__ cc, float* __restrict__ C, int64_t ldc, int64_t t0) {
   const int64_t rows4 = (m + 3) >> 2;
-  const int64_t t = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  const int64_t t = t0 + (int64_t)blockIdx.x * 256 + threadIdx.x;
   if (t >= rows4 * n) return;
   const int64_t j = t / rows4;
   const int64_t i0 = (t - j * rows4) * 4;
@@ -132,9 +132,13 @@ hipError_t launch_amax_f32(hipStream_t stream, const float* A, int64_t lda, cons
   hipLaunchKernelGGL(k_amax_adjacent_lines_f32, dim3(blocks_of(m, 256), blocks_of(k, kAmaxChunk32)),
                      dim3(256), 0, stream, A, lda, m, k,
                      reinterpret_cast<unsigned long long*>(amax_a), flag);
-  hipLaunchKernelGGL(k_amax_contig_lines_f32, dim3(blocks_of(n, 4), blocks_of(k, kAmaxContigChunk32)),
-                     dim3(256), 0, stream, B, ldb, n, k,
-                     reinterpret_cast<unsigned long long*>(amax_b), flag);
+  constexpr int64_t kLines = kLaunchThreads / 64;   // one wave per line
+  for (int64_t l0 = 0; l0 < n; l0 += kLines)
+    hipLaunchKernelGGL(k_amax_contig_lines_f32,
+                       dim3(blocks_of(n - l0 < kLines ? n - l0 : kLines, 4),
+                            blocks_of(k, kAmaxContigChunk32)),
+                       dim3(256), 0, stream, B, ldb, n, k,
+                       reinterpret_cast<unsigned long long*>(amax_b), flag, l0);
   return hipGetLastError();
 }
 
@@ -153,13 +157,17 @@ hipError_t launch_crt_f32(hipStream_t stream, int nc, const uint8_t* R, int64_t 
                           int64_t rplane, int64_t m, int64_t n, const uint64_t* amaxA,
                           const uint64_t* amaxB, int cA, int cB, const CrtConst* cc, float* C,
                           int64_t ldc) {
-  const unsigned grid = blocks_of(((m + 3) / 4) * n, 256);
-  if (nc == 3)
-    hipLaunchKernelGGL(k_crt_f32<3>, dim3(grid), dim3(256), 0, stream, R, ldr, rplane, m, n,
-                       amaxA, amaxB, cA, cB, cc, C, ldc);
-  else
-    hipLaunchKernelGGL(k_crt_f32<4>, dim3(grid), dim3(256), 0, stream, R, ldr, rplane, m, n,
-                       amaxA, amaxB, cA, cB, cc, C, ldc);
+  const int64_t nthreads = ((m + 3) / 4) * n;
+  for (int64_t t0 = 0; t0 < nthreads; t0 += kLaunchThreads) {
+    const int64_t cnt = nthreads - t0 < kLaunchThreads ? nthreads - t0 : kLaunchThreads;
+    const unsigned grid = blocks_of(cnt, 256);
+    if (nc == 3)
+      hipLaunchKernelGGL(k_crt_f32<3>, dim3(grid), dim3(256), 0, stream, R, ldr, rplane, m, n,
+                         amaxA, amaxB, cA, cB, cc, C, ldc, t0);
+    else
+      hipLaunchKernelGGL(k_crt_f32<4>, dim3(grid), dim3(256), 0, stream, R, ldr, rplane, m, n,
+                         amaxA, amaxB, cA, cB, cc, C, ldc, t0);
+  }
   return hipGetLastError();
 }
 

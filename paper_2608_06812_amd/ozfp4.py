@@ -31,6 +31,7 @@ OZFP4_MIN_MODULI = 2
 OZFP4_MAX_MODULI = 27
 OZFP4_MAX_K = 131072
 OZFP4_MAX_K_S8 = 16777216
+OZFP4_MAX_ELEMENTS = 1 << 48
 OZFP4_OZI_MAX_LIMBS = 15
 
 _lib = None

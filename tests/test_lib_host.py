@@ -41,6 +41,15 @@ def test_header_declares_the_boundary():
         assert required in names
 
 
+def test_binding_mirrors_the_header_constants():
+    text = open(HEADER).read()
+    for name, value in re.findall(r"#define (OZFP4_[A-Z0-9_]+)[ \t]+(\S.*?)\s*(?:/\*|$)", text, re.M):
+        if name == "OZFP4_H":
+            continue
+        value = value.replace("((int64_t)1 << 48)", str(1 << 48))
+        assert getattr(ozfp4, name) == int(value, 0), name
+
+
 def test_library_exports_every_declared_symbol(lib):
     for name in _declared_symbols():
         assert hasattr(lib, name), name
@@ -125,6 +134,8 @@ def test_plane_layout(lib):
     assert ozfp4.ozfp4_plane_layout(256, 256) == (256, 384, 256 * 192)
     assert ozfp4.ozfp4_plane_layout(300, 129) == (512, 384, 512 * 192)
     assert ozfp4.ozfp4_plane_layout(300, 1000) == (512, 1024, 512 * 512)
+    with pytest.raises(ozfp4.OzFP4Error):
+        ozfp4.ozfp4_plane_layout(2 ** 40, 2 ** 17)   # lines k > 2^48
 
 
 def test_strerror(lib):
@@ -132,6 +143,9 @@ def test_strerror(lib):
     for code in range(-6, 0):
         assert ozfp4.ozfp4_strerror(code) != "unknown error code"
     assert ozfp4.ozfp4_strerror(-99) == "unknown error code"
+    # the message states the same moduli range as the header
+    assert "[%d, %d]" % (ozfp4.OZFP4_MIN_MODULI, ozfp4.OZFP4_MAX_MODULI) in \
+        ozfp4.ozfp4_strerror(ozfp4.OZFP4_EMODULI)
 
 
 @pytest.mark.parametrize("args,code", [
@@ -145,6 +159,11 @@ def test_strerror(lib):
     ((4, 4, 4, 1, 4, 1, 4, 1, 4, 28), ozfp4.OZFP4_EMODULI),          # too many moduli
     ((4, 4, 131073, 1, 4, 1, 131073, 1, 4, 19), ozfp4.OZFP4_EKBOUND),
     ((4, 4, 65536, 1, 4, 1, 65536, 1, 4, 2), ozfp4.OZFP4_EMODULI),   # P too small for k
+    # a product of two dimensions above OZFP4_MAX_ELEMENTS (2^48)
+    ((2 ** 25, 2 ** 25, 4, 1, 2 ** 25, 1, 4, 1, 2 ** 25, 19), ozfp4.OZFP4_EINVAL),   # m n
+    ((2 ** 32, 4, 131072, 1, 2 ** 32, 1, 131072, 1, 2 ** 32, 19), ozfp4.OZFP4_EINVAL),  # m k
+    ((4, 2 ** 32, 131072, 1, 4, 1, 131072, 1, 4, 19), ozfp4.OZFP4_EINVAL),  # n k
+    ((2 ** 62, 0, 4, 1, 2 ** 62, 1, 4, 1, 2 ** 62, 19), ozfp4.OZFP4_EINVAL),  # m k, n = 0
 ])
 def test_dgemm_argument_errors_on_host(lib, args, code):
     assert ozfp4.ozfp4_dgemm(*args) == code
@@ -159,6 +178,7 @@ def test_dgemm_empty_is_noop(lib):
     ((4, 4, 4, 1, 3, 1, 4, 1, 4), ozfp4.OZFP4_EINVAL),
     ((4, 4, 4, 1, 4, 1, 4, 0, 4), ozfp4.OZFP4_EINVAL),               # null C
     ((4, 4, 16777217, 1, 4, 1, 16777217, 1, 4), ozfp4.OZFP4_EKBOUND),
+    ((2 ** 25, 4, 2 ** 24, 1, 2 ** 25, 1, 2 ** 24, 1, 2 ** 25), ozfp4.OZFP4_EINVAL),  # m k > 2^48
 ])
 def test_igemm_argument_errors_on_host(lib, args, code):
     assert ozfp4.ozfp4_igemm_s8(*args) == code
@@ -198,6 +218,7 @@ def test_sgemm_capacity_matches_oracle(lib):
     ((4, 4, 131073, 1, 4, 1, 131073, 1, 4, 10), ozfp4.OZFP4_EKBOUND),
     ((4, 4, 65536, 1, 4, 1, 65536, 1, 4, 2), ozfp4.OZFP4_EMODULI),   # P too small for k
     ((0, 5, 5, 0, 1, 0, 5, 0, 1, 10), ozfp4.OZFP4_OK),
+    ((2 ** 25, 2 ** 25, 4, 1, 2 ** 25, 1, 4, 1, 2 ** 25, 10), ozfp4.OZFP4_EINVAL),   # m n > 2^48
 ])
 def test_sgemm_argument_errors_on_host(lib, args, code):
     assert ozfp4.ozfp4_sgemm(*args) == code
@@ -227,6 +248,7 @@ def test_ozi_config_matches_oracle(lib, paper):
     ((4, 4, 131073, 1, 4, 1, 131073, 1, 4, 15), ozfp4.OZFP4_EKBOUND),
     ((0, 5, 5, 0, 1, 0, 5, 0, 1, 15), ozfp4.OZFP4_OK),               # empty: no-op
     ((5, 0, 5, 0, 5, 0, 5, 0, 5, 15), ozfp4.OZFP4_OK),
+    ((2 ** 25, 2 ** 25, 4, 1, 2 ** 25, 1, 4, 1, 2 ** 25, 15), ozfp4.OZFP4_EINVAL),   # m n > 2^48
 ])
 def test_dgemm_ozi_argument_errors_on_host(lib, args, code):
     assert ozfp4.ozfp4_dgemm_ozi(*args) == code
