@@ -14,6 +14,7 @@ is accepted when X.stride(0) == 1, with leading dimension X.stride(1).
 
 from __future__ import annotations
 
+import contextlib
 import ctypes
 import os
 
@@ -235,9 +236,18 @@ def _cm(X, dtype, name):
     return X, ld
 
 
-def _use_torch_stream(device):
+@contextlib.contextmanager
+def _on(device, *tensors):
+    """Runs the library call on `device`: every tensor must live there; the
+    device is made current (the library works on the current device) and
+    its current torch stream becomes the library stream."""
     import torch
-    ozfp4_set_stream(torch.cuda.current_stream(device).cuda_stream)
+    for T in tensors:
+        if T.device != device:
+            raise ValueError(f"tensors on {T.device} and {device}: all must share one device")
+    with torch.cuda.device(device):
+        ozfp4_set_stream(torch.cuda.current_stream(device).cuda_stream)
+        yield
 
 
 def _empty_cm(rows, cols, dtype, device):
@@ -259,9 +269,9 @@ def dgemm(A, B, n_moduli: int = 19, out=None):
     if C.shape != (m, n) or C.dtype != torch.float64 or (C.stride(0) != 1 and m > 1):
         raise ValueError("out must be a column-major float64 (m x n) tensor")
     ldc = max(1, C.stride(1) if n > 1 else m)
-    _use_torch_stream(A.device)
-    _check(ozfp4_dgemm(m, n, k, A.data_ptr(), lda, B.data_ptr(), ldb, C.data_ptr(), ldc, n_moduli),
-           "ozfp4_dgemm")
+    with _on(A.device, B, C):
+        _check(ozfp4_dgemm(m, n, k, A.data_ptr(), lda, B.data_ptr(), ldb, C.data_ptr(), ldc, n_moduli),
+               "ozfp4_dgemm")
     return C
 
 
@@ -279,9 +289,9 @@ def igemm_s8(A, B, out=None):
     if C.shape != (m, n) or C.dtype != torch.int32 or (C.stride(0) != 1 and m > 1):
         raise ValueError("out must be a column-major int32 (m x n) tensor")
     ldc = max(1, C.stride(1) if n > 1 else m)
-    _use_torch_stream(A.device)
-    _check(ozfp4_igemm_s8(m, n, k, A.data_ptr(), lda, B.data_ptr(), ldb, C.data_ptr(), ldc),
-           "ozfp4_igemm_s8")
+    with _on(A.device, B, C):
+        _check(ozfp4_igemm_s8(m, n, k, A.data_ptr(), lda, B.data_ptr(), ldb, C.data_ptr(), ldc),
+               "ozfp4_igemm_s8")
     return C
 
 
@@ -294,9 +304,9 @@ def scales(A, B, n_moduli: int = 19):
     n = B.shape[1]
     s = torch.empty(m, dtype=torch.int32, device=A.device)
     t = torch.empty(n, dtype=torch.int32, device=A.device)
-    _use_torch_stream(A.device)
-    _check(ozfp4_scales(m, n, k, A.data_ptr(), lda, B.data_ptr(), ldb, n_moduli, s.data_ptr(),
-                        t.data_ptr()), "ozfp4_scales")
+    with _on(A.device, B, s, t):
+        _check(ozfp4_scales(m, n, k, A.data_ptr(), lda, B.data_ptr(), ldb, n_moduli, s.data_ptr(),
+                            t.data_ptr()), "ozfp4_scales")
     return s, t
 
 
@@ -314,9 +324,9 @@ def limb_planes(A, B, n_moduli: int = 19):
     nplanes, _ = ozfp4_plane_count(n_moduli)
     pa = torch.empty((nplanes, bpa), dtype=torch.uint8, device=A.device)
     pb = torch.empty((nplanes, bpb), dtype=torch.uint8, device=A.device)
-    _use_torch_stream(A.device)
-    _check(ozfp4_limb_planes(m, n, k, A.data_ptr(), lda, B.data_ptr(), ldb, n_moduli, pa.data_ptr(),
-                             pb.data_ptr()), "ozfp4_limb_planes")
+    with _on(A.device, B, pa, pb):
+        _check(ozfp4_limb_planes(m, n, k, A.data_ptr(), lda, B.data_ptr(), ldb, n_moduli, pa.data_ptr(),
+                                 pb.data_ptr()), "ozfp4_limb_planes")
     return pa, pb
 
 
@@ -329,9 +339,9 @@ def residues(A, B, n_moduli: int = 19):
     m, k = A.shape
     n = B.shape[1]
     R = torch.empty((n_moduli, n, m), dtype=torch.uint8, device=A.device)
-    _use_torch_stream(A.device)
-    _check(ozfp4_residues(m, n, k, A.data_ptr(), lda, B.data_ptr(), ldb, n_moduli, R.data_ptr(), m),
-           "ozfp4_residues")
+    with _on(A.device, B, R):
+        _check(ozfp4_residues(m, n, k, A.data_ptr(), lda, B.data_ptr(), ldb, n_moduli, R.data_ptr(), m),
+               "ozfp4_residues")
     return R
 
 
@@ -350,9 +360,9 @@ def dgemm_ozi(A, B, n_limbs: int = OZFP4_OZI_MAX_LIMBS, out=None):
     if C.shape != (m, n) or C.dtype != torch.float64 or (C.stride(0) != 1 and m > 1):
         raise ValueError("out must be a column-major float64 (m x n) tensor")
     ldc = max(1, C.stride(1) if n > 1 else m)
-    _use_torch_stream(A.device)
-    _check(ozfp4_dgemm_ozi(m, n, k, A.data_ptr(), lda, B.data_ptr(), ldb, C.data_ptr(), ldc,
-                           n_limbs), "ozfp4_dgemm_ozi")
+    with _on(A.device, B, C):
+        _check(ozfp4_dgemm_ozi(m, n, k, A.data_ptr(), lda, B.data_ptr(), ldb, C.data_ptr(), ldc,
+                               n_limbs), "ozfp4_dgemm_ozi")
     return C
 
 
@@ -369,9 +379,9 @@ def ozi_limb_planes(A, B, n_limbs: int = OZFP4_OZI_MAX_LIMBS):
     _, nplanes, _ = ozfp4_ozi_config(n_limbs)
     pa = torch.empty((nplanes, bpa), dtype=torch.uint8, device=A.device)
     pb = torch.empty((nplanes, bpb), dtype=torch.uint8, device=A.device)
-    _use_torch_stream(A.device)
-    _check(ozfp4_ozi_limb_planes(m, n, k, A.data_ptr(), lda, B.data_ptr(), ldb, n_limbs,
-                                 pa.data_ptr(), pb.data_ptr()), "ozfp4_ozi_limb_planes")
+    with _on(A.device, B, pa, pb):
+        _check(ozfp4_ozi_limb_planes(m, n, k, A.data_ptr(), lda, B.data_ptr(), ldb, n_limbs,
+                                     pa.data_ptr(), pb.data_ptr()), "ozfp4_ozi_limb_planes")
     return pa, pb
 
 
@@ -385,9 +395,9 @@ def ozi_partials(A, B, n_limbs: int = OZFP4_OZI_MAX_LIMBS):
     n = B.shape[1]
     _, _, ng = ozfp4_ozi_config(n_limbs)
     H = torch.empty((ng, n, m), dtype=torch.int64, device=A.device)
-    _use_torch_stream(A.device)
-    _check(ozfp4_ozi_partials(m, n, k, A.data_ptr(), lda, B.data_ptr(), ldb, n_limbs,
-                              H.data_ptr(), m), "ozfp4_ozi_partials")
+    with _on(A.device, B, H):
+        _check(ozfp4_ozi_partials(m, n, k, A.data_ptr(), lda, B.data_ptr(), ldb, n_limbs,
+                                  H.data_ptr(), m), "ozfp4_ozi_partials")
     return H
 
 
@@ -420,7 +430,7 @@ def sgemm(A, B, n_moduli: int | None = None, out=None):
     if C.shape != (m, n) or C.dtype != torch.float32 or (C.stride(0) != 1 and m > 1):
         raise ValueError("out must be a column-major float32 (m x n) tensor")
     ldc = max(1, C.stride(1) if n > 1 else m)
-    _use_torch_stream(A.device)
-    _check(ozfp4_sgemm(m, n, k, A.data_ptr(), lda, B.data_ptr(), ldb, C.data_ptr(), ldc, n_moduli),
-           "ozfp4_sgemm")
+    with _on(A.device, B, C):
+        _check(ozfp4_sgemm(m, n, k, A.data_ptr(), lda, B.data_ptr(), ldb, C.data_ptr(), ldc, n_moduli),
+               "ozfp4_sgemm")
     return C

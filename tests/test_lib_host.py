@@ -266,3 +266,12 @@ def test_binding_refuses_missing_library(monkeypatch, tmp_path):
     monkeypatch.setattr(ozfp4, "LIB_PATH", str(tmp_path / "missing.so"))
     with pytest.raises(RuntimeError):
         ozfp4.load()
+
+
+def test_binding_refuses_tensors_on_different_devices():
+    """The helpers run the library on the first operand's device; an operand
+    or output elsewhere is refused before any library or device call."""
+    import torch
+    with pytest.raises(ValueError, match="share one device"):
+        with ozfp4._on(torch.device("cpu"), torch.empty(1, device="meta")):
+            pass
