@@ -144,7 +144,9 @@ def cpu_baseline(A, B, L, k, budget_s=10.0):
     return {"value": tflops, "unit": "TFLOP/s (emulated DGEMM)", "cores": blas_threads,
             "kind": "oracle",
             "sample": f"{side}x{side} output block of the {A.shape[0]}x{B.shape[1]}x{k} workload at full k, "
-                      f"{L} moduli, {elapsed:.2f} s (calibration 64x64: {t64:.2f} s)"}
+                      f"{L} moduli, {elapsed:.2f} s (calibration 64x64: {t64:.2f} s); limb products "
+                      f"in FP64 BLAS on {blas_threads} threads, exact CRT and rounding in "
+                      f"single-threaded Python"}
 
 
 def exact_reference(A, B, rows, cols):
@@ -283,7 +285,8 @@ def main() -> int:
         "metric": METRIC, "value": value, "unit": "TFLOP/s", "n_gpus": 1,
         "steps": args.steps, "warmup": args.warmup, "ms_per_step": ms,
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
-        "dtype": "f64 (FP4 E2M1 MFMA, FP32 accumulate, exact integer CRT)",
+        "dtype": "f64",
+        "arithmetic": "FP4 E2M1 MFMA products, FP32 accumulation, exact integer CRT",
         "data": "synthetic: (U(0,1)-0.5)*exp(0.5*N(0,1)), seed %d" % (SEED + 2),
         "config": {"workload": f"dgemm m=n=k={N}, phi=0.5", "m": N, "n": N, "k": N,
                    "n_moduli": L, "parallelism": "single GPU"},
