@@ -1,0 +1,57 @@
+"""The library runs on the caller's stream (ozfp4_set_stream; the torch
+helpers pass torch's current stream): work queued on a side stream before a
+call is complete before the library reads its inputs, and work queued after
+it sees the finished output. A spin kernel delays the producer of the
+input on the side stream, so a call issued on any other stream would read
+the input before it is written."""
+
+import numpy as np
+import pytest
+
+import oracle as o
+from gpu_util import announce, bits_equal, dev_cm, to_np
+from paper_2608_06812_amd.workloads import dgemm_inputs, int8_inputs
+
+pytestmark = pytest.mark.gpu
+
+SEED = 20261203
+SPIN_CYCLES = 20_000_000   # about 10 ms of a spinning kernel
+
+
+def test_dgemm_on_a_side_stream(gpu_lib):
+    import torch
+    m, n, k = 200, 150, 300
+    A, B = dgemm_inputs(m, n, k, 0.5, SEED)
+    want = o.dgemm(A, B, 19)["C"]
+    Ad, Bd = dev_cm(A), dev_cm(B)
+    torch.cuda.synchronize()
+    side = torch.cuda.Stream()
+    announce("dgemm on a side stream after a spin kernel")
+    with torch.cuda.stream(side):
+        torch.cuda._sleep(SPIN_CYCLES)
+        A2 = Ad * 2.0                 # exact; written only after the spin
+        C = gpu_lib.dgemm(A2, Bd, 19)
+        D = C * 0.5                   # exact: fl(2 A B) = 2 fl(A B) here
+    torch.cuda.synchronize()
+    assert bits_equal(to_np(D), want)
+
+
+def test_igemm_s8_on_a_side_stream(gpu_lib):
+    """ozfp4_igemm_s8 is asynchronous: ordering on the side stream is all
+    that makes its inputs ready and its output complete."""
+    import torch
+    m, n, k = 256, 192, 640
+    A, B = int8_inputs(m, n, k, SEED + 1)
+    want = (A.astype(np.int64) @ B.astype(np.int64)).astype(np.int32)
+    Ad = torch.from_numpy(np.ascontiguousarray(A.T)).cuda().t()
+    Bd = torch.from_numpy(np.ascontiguousarray(B.T)).cuda().t()
+    torch.cuda.synchronize()
+    side = torch.cuda.Stream()
+    announce("igemm_s8 on a side stream after a spin kernel")
+    with torch.cuda.stream(side):
+        torch.cuda._sleep(SPIN_CYCLES)
+        A2 = Ad.clone()
+        C = gpu_lib.igemm_s8(A2, Bd)
+        D = C.clone()
+    torch.cuda.synchronize()
+    assert np.array_equal(D.cpu().numpy(), want)
