@@ -17,9 +17,10 @@
  *     stream). Calls that read back a status synchronize that stream and say
  *     so below.
  *   - The library owns a per-device workspace (limb planes, residues,
- *     exponents) that grows on demand and is released by ozfp4_finalize.
- *     Calls are not thread-safe and calls that overlap on one device race on
- *     that workspace.
+ *     exponents) that grows on demand (the device is synchronized before the
+ *     old buffer is freed) and is released by ozfp4_finalize. Calls are not
+ *     thread-safe, and calls that overlap on one device (for example
+ *     asynchronous calls on two streams) race on that workspace.
  *   - Every entry point returns OZFP4_OK (0) or a negative error code; argument
  *     errors are detected on the host before any GPU work is issued.
  *   - Each product of two of m, n, k is at most OZFP4_MAX_ELEMENTS (else

@@ -119,7 +119,9 @@ int device_state(DeviceState** out) {
 int ensure_workspace(DeviceState* d, size_t bytes) {
   if (bytes <= d->ws_bytes) return OZFP4_OK;
   if (d->ws) {
-    HIP_TRY(hipStreamSynchronize(g_stream));
+    // an asynchronous call issued earlier on another stream may still use
+    // the old buffer: wait for the whole device before freeing it
+    HIP_TRY(hipDeviceSynchronize());
     HIP_TRY(hipFree(d->ws));
     d->ws = nullptr;
     d->ws_bytes = 0;
