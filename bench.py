@@ -117,11 +117,12 @@ def time_call(ozfp4, torch, call, steps, warmup, profile=True):
     return (t1 - t0) * 1e3 / steps, stages
 
 
-def cpu_baseline(A, B, L, k, budget_s=10.0):
+def cpu_baseline(A, B, L, k, budget_s=20.0):
     """The oracle, as it stands, on a bounded sample of output elements of
     the same workload (a square block of outputs, whole rows of A and
     columns of B at full k), grown until one timed run takes at least half
-    of `budget_s` seconds."""
+    of `budget_s` seconds (10-30 s of CPU work at the default), or reaches
+    1024 x 1024."""
     import numpy as np
 
     import oracle
