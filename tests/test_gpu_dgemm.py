@@ -275,31 +275,33 @@ def test_paper_accuracy_experiment(gpu_lib, paper, phi, key):
 
 
 @pytest.mark.slow
-def test_residues_16384_full_for_one_modulus(gpu_lib):
+def test_residues_16384_full_for_two_moduli(gpu_lib):
     """The benchmark workload (m = n = k = 16384, L = 18): every one of the
-    2^28 residues of modulus 115 (the modulus with the paper's worked split,
-    -58 = 13 (-4) - 6) equals the definition (A~ B~) mod m, formed from the
-    oracle's converted integers as ((A~ mod m)(B~ mod m)) mod m by one FP64
-    product, exact because every sum is below 114^2 k < 2^53."""
+    2^28 residues of modulus 169 (whose tile skips the a1 b1 products, as
+    13^2 = 0 mod 169) and of modulus 115 (the modulus with the paper's worked
+    split, -58 = 13 (-4) - 6) equals the definition (A~ B~) mod m, formed
+    from the oracle's converted integers as ((A~ mod m)(B~ mod m)) mod m by
+    one FP64 product, exact because every sum is below 168^2 k < 2^53."""
     import torch
-    N, L, index = 16384, 18, 1
+    N, L = 16384, 18
     A, B = dgemm_inputs(N, N, N, 0.5, SEED + 11)
     moduli = o.select_moduli(L)
-    assert moduli[index] == 115
+    assert moduli[:2] == [169, 115]
     cA, cB = o.capacity_bits(N, moduli)
     Ai = o.to_integers(A, o.shift_exponents(A, axis=1, c=cA), axis=1)
     Bi = o.to_integers(B, o.shift_exponents(B, axis=0, c=cB), axis=0)
-    announce("residues 16384^3 L=18, all of modulus 115")
+    announce("residues 16384^3 L=18, all of moduli 169 and 115")
     Ad, Bd = dev_cm(A), dev_cm(B)
     del A, B
     R = gpu_lib.residues(Ad, Bd, L)
-    got = R[index].cpu().numpy().T          # (m, n)
+    got = [R[i].cpu().numpy().T for i in (0, 1)]   # (m, n) each
     del R, Ad, Bd
     torch.cuda.empty_cache()
-    ra = o.residues(Ai, 115).astype(np.float64)
-    rb = o.residues(Bi, 115).astype(np.float64)
-    del Ai, Bi
-    assert 114.0 ** 2 * N < 2.0 ** 53
-    want = np.mod(np.rint(ra @ rb).astype(np.int64), 115)
-    assert got.shape == want.shape
-    assert np.array_equal(got.astype(np.int64), want)
+    assert 168.0 ** 2 * N < 2.0 ** 53
+    for i, m in ((0, 169), (1, 115)):
+        ra = o.residues(Ai, m).astype(np.float64)
+        rb = o.residues(Bi, m).astype(np.float64)
+        want = np.mod(np.rint(ra @ rb).astype(np.int64), m)
+        del ra, rb
+        assert got[i].shape == want.shape
+        assert np.array_equal(got[i].astype(np.int64), want), f"modulus {m}"
