@@ -65,9 +65,11 @@ def test_igemm_s8_k_zero(gpu_lib):
 
 
 @pytest.mark.slow
-def test_igemm_s8_8192_rows_sampled(gpu_lib):
+def test_igemm_s8_8192_full(gpu_lib):
     """The INT8 configuration (8192^3): 48 whole rows and 48 whole columns
-    of C checked exactly (FP64 BLAS is exact here: |sum| <= 2^27)."""
+    of C against the oracle, and every element of C against the definition
+    A B formed by one FP64 product of the int8 inputs, exact here because
+    |sum| <= 128^2 8192 = 2^27 < 2^53 (and below 2^31, so nothing wraps)."""
     A, B = int8_inputs(8192, 8192, 8192, SEED + 1)
     announce("igemm_s8 8192^3")
     Cd = gpu_lib.igemm_s8(dev_cm(A), dev_cm(B))
@@ -79,6 +81,9 @@ def test_igemm_s8_8192_rows_sampled(gpu_lib):
     got_cols = to_np(Cd[:, torch.as_tensor(cols, device="cuda")])
     assert np.array_equal(got_rows, o.igemm_s8(A[rows], B))
     assert np.array_equal(got_cols, o.igemm_s8(A, B[:, cols]))
+    want = np.rint(A.astype(np.float64) @ B.astype(np.float64)).astype(np.int64)
+    assert np.abs(want).max() < 2 ** 31
+    assert np.array_equal(to_np(Cd).astype(np.int64), want)
 
 
 def test_igemm_s8_equals_native_int8_matrix_cores(gpu_lib):
