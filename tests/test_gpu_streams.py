@@ -55,3 +55,23 @@ def test_igemm_s8_on_a_side_stream(gpu_lib):
         D = C.clone()
     torch.cuda.synchronize()
     assert np.array_equal(D.cpu().numpy(), want)
+
+
+def test_finalize_then_reuse(gpu_lib):
+    """ozfp4_finalize releases the workspace and tables of every device; the
+    next call sets them up again and gives the same bits."""
+    import torch
+    m, n, k = 90, 70, 200
+    A, B = dgemm_inputs(m, n, k, 0.5, SEED + 2)
+    A8, B8 = int8_inputs(m, n, k, SEED + 3)
+    Ad, Bd = dev_cm(A), dev_cm(B)
+    A8d = torch.from_numpy(np.ascontiguousarray(A8.T)).cuda().t()
+    B8d = torch.from_numpy(np.ascontiguousarray(B8.T)).cuda().t()
+    announce("dgemm, finalize, dgemm and igemm_s8 again")
+    C1 = to_np(gpu_lib.dgemm(Ad, Bd, 19))
+    assert gpu_lib.ozfp4_finalize() == gpu_lib.OZFP4_OK
+    C2 = to_np(gpu_lib.dgemm(Ad, Bd, 19))
+    assert gpu_lib.ozfp4_finalize() == gpu_lib.OZFP4_OK
+    C3 = gpu_lib.igemm_s8(A8d, B8d).cpu().numpy()
+    assert bits_equal(C1, C2) and bits_equal(C1, o.dgemm(A, B, 19)["C"])
+    assert np.array_equal(C3, o.igemm_s8(A8, B8))
