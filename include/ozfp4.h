@@ -138,7 +138,8 @@ int ozfp4_set_karatsuba(int enable);
  */
 int ozfp4_set_max_capacity(int bits);
 
-/* Releases every device workspace and table of the library. */
+/* Releases every device workspace and table of the library, after waiting
+ * for each device's work. A later call sets them up again. */
 int ozfp4_finalize(void);
 
 /* Static message for an error code. */
@@ -147,11 +148,13 @@ const char* ozfp4_strerror(int code);
 /* ---- host-only queries (no GPU work; usable without a device) ---------- */
 
 /* Writes the first n_moduli moduli (Sec. V-A greedy order) to the HOST array
- * out[n_moduli]. */
+ * out[n_moduli]; n_moduli in 1..OZFP4_MAX_MODULI, else OZFP4_EINVAL. */
 int ozfp4_moduli(int n_moduli, int32_t* out);
 
 /* Capacities (c_A, c_B) used for inner dimension k with n_moduli moduli
- * and the current capacity cap (see ozfp4_dgemm). HOST pointers. */
+ * and the current capacity cap (see ozfp4_dgemm). HOST pointers.
+ * OZFP4_EINVAL for k < 1 or a null pointer, OZFP4_EMODULI when n_moduli is
+ * outside 2..27 or the moduli cannot hold k. */
 int ozfp4_capacity(int64_t k, int n_moduli, int32_t* c_a, int32_t* c_b);
 
 /* Canonical two-limb split of every residue r in [0, m_l) of modulus l
@@ -164,6 +167,8 @@ int ozfp4_capacity(int64_t k, int n_moduli, int32_t* c_a, int32_t* c_b);
  * -58 = 13(-4) - 6). E2M1 codes: magnitudes 0, .5, 1, 1.5, 2, 3, 4, 6 are
  * codes 0..7, sign bit 0x8; a limb c is stored as the value c/2. */
 int ozfp4_two_limb_table(int modulus_index, uint8_t* out, int32_t* m_out);
+/* (modulus_index in 0..OZFP4_MAX_MODULI-1 and HOST *m_out = m_l; OZFP4_EINVAL
+ * otherwise or for a null pointer.) */
 
 /* Limbs of every residue r in [0, m_l) of a Karatsuba modulus l for the
  * Karatsuba mode (ozfp4_set_karatsuba): c0, c1 and c0 + c1 all in S and of
@@ -178,13 +183,15 @@ int ozfp4_sum_limb_table(int modulus_index, uint8_t* out, int32_t* m_out);
  * mode: 2 n_moduli limb planes, plus in the Karatsuba mode one sum plane
  * (c0 + c1) per Karatsuba modulus among them. HOST outputs: *n_planes, and
  * when sum_plane is not NULL the index of the sum plane of each modulus in
- * sum_plane[n_moduli] (-1 for none). */
+ * sum_plane[n_moduli] (-1 for none). OZFP4_EMODULI for n_moduli outside
+ * 2..27, OZFP4_EINVAL for a null n_planes. */
 int ozfp4_plane_count(int n_moduli, int32_t* n_planes, int32_t* sum_plane);
 
 /* Layout of the packed FP4 limb planes (the debug hook below returns them):
  * lines (rows of A, columns of B) are padded to rows_pad (a multiple of 256)
  * and k to k_pad (a multiple of 128, at least 384); one plane holds
- * rows_pad * k_pad / 2 bytes. */
+ * rows_pad * k_pad / 2 bytes. HOST outputs; OZFP4_EINVAL for a negative
+ * size, lines * k above OZFP4_MAX_ELEMENTS or a null pointer. */
 int ozfp4_plane_layout(int64_t lines, int64_t k, int64_t* rows_pad,
                        int64_t* k_pad, int64_t* bytes_per_plane);
 
@@ -334,12 +341,14 @@ int ozfp4_ozi_partials(int64_t m, int64_t n, int64_t k,
  * recorded on the library's stream. */
 int ozfp4_profile(int enable);
 
-/* Milliseconds of each stage of the last profiled call, written to the HOST
- * array ms[max]; returns the stage count (>= 0) or an error. dgemm and sgemm
- * stages:
+/* Milliseconds of each stage of the last profiled call: the first
+ * min(max, stage count) values go to the HOST array ms[max] and the stage
+ * count to the HOST *n_stages (0 if no profiled call ran). Returns OZFP4_OK,
+ * or OZFP4_EINVAL for a null pointer or max < 0. dgemm and sgemm stages:
  * 0 scale, 1 encode A, 2 encode B, 3 residue GEMM, 4 CRT. dgemm_ozi stages:
  * 0 scale, 1 encode A, 2 encode B, 3 limb GEMM, 4 reduction. igemm_s8
- * stages: 0 encode A, 1 encode B, 2 GEMM. Synchronizes. */
+ * stages: 0 encode A, 1 encode B, 2 GEMM (asynchronous: this call waits for
+ * its last event). */
 int ozfp4_stage_times(double* ms, int max, int* n_stages);
 
 #ifdef __cplusplus
