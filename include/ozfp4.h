@@ -165,10 +165,10 @@ int ozfp4_capacity(int64_t k, int n_moduli, int32_t* c_a, int32_t* c_b);
  * replaced by -+8, Lemma 2) and, when that fails (m = 115, r' = +-57),
  * moves r' by one m toward the other sign first (Sec. V-A example
  * -58 = 13(-4) - 6). E2M1 codes: magnitudes 0, .5, 1, 1.5, 2, 3, 4, 6 are
- * codes 0..7, sign bit 0x8; a limb c is stored as the value c/2. */
+ * codes 0..7, sign bit 0x8; a limb c is stored as the value c/2.
+ * modulus_index in 0..OZFP4_MAX_MODULI-1; HOST *m_out = m_l; OZFP4_EINVAL
+ * for another index or a null pointer. */
 int ozfp4_two_limb_table(int modulus_index, uint8_t* out, int32_t* m_out);
-/* (modulus_index in 0..OZFP4_MAX_MODULI-1 and HOST *m_out = m_l; OZFP4_EINVAL
- * otherwise or for a null pointer.) */
 
 /* Limbs of every residue r in [0, m_l) of a Karatsuba modulus l for the
  * Karatsuba mode (ozfp4_set_karatsuba): c0, c1 and c0 + c1 all in S and of
