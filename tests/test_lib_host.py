@@ -275,3 +275,24 @@ def test_binding_refuses_tensors_on_different_devices():
     with pytest.raises(ValueError, match="share one device"):
         with ozfp4._on(torch.device("cpu"), torch.empty(1, device="meta")):
             pass
+
+
+def test_binding_argument_checks_on_host():
+    """The torch helpers check their arguments before any device call: a
+    2-D device tensor of the documented dtype, nothing else."""
+    import torch
+    A = torch.zeros(4, 4, dtype=torch.float64)
+    with pytest.raises(TypeError):
+        ozfp4.dgemm([[1.0]], A)                               # not a tensor
+    with pytest.raises(TypeError):
+        ozfp4.dgemm(torch.zeros(4, dtype=torch.float64), A)   # not 2-D
+    with pytest.raises(TypeError):
+        ozfp4.dgemm(A.float(), A)                              # wrong dtype
+    with pytest.raises(TypeError):
+        ozfp4.sgemm(A, A)                                      # FP64 into the FP32 path
+    with pytest.raises(TypeError):
+        ozfp4.igemm_s8(A, A)                                   # not int8
+    with pytest.raises(ValueError, match="device tensor"):
+        ozfp4.dgemm(A, A)                                      # host memory
+    with pytest.raises(ValueError, match="device tensor"):
+        ozfp4.igemm_s8(A.to(torch.int8), A.to(torch.int8))
