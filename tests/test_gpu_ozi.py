@@ -196,3 +196,27 @@ def test_ozi_16384_sampled_and_equal_to_ozii(gpu_lib):
     del C1, C2
     want = o.dgemm_ozi(A, B, 15, rows=rows, cols=cols)["C"]
     assert bits_equal(sub, want)
+
+
+@pytest.mark.slow
+def test_ozi_at_the_largest_k_with_largest_limbs(gpu_lib):
+    """k = 131072 (OZFP4_MAX_K, eight accumulation chunks of 16384) with
+    every converted value at the largest greedy limbs (fourteen limbs of 8,
+    then 1): the int64 partial sums reach their largest magnitudes, and the
+    partial sums and C stay exact."""
+    x = sum(8 * 13 ** i for i in range(14)) + 13 ** 14
+    m, n, k = 24, 16, gpu_lib.OZFP4_MAX_K
+    A = np.full((m, k), float(x))
+    B = np.full((k, n), float(x))
+    A[1, :] = -float(x)
+    B[:, 2] = -float(x)
+    A[3, 1::2] = -float(x)
+    res = o.dgemm_ozi(A, B, 15)
+    announce(f"ozi partials and dgemm k={k} largest limbs")
+    H = to_np(gpu_lib.ozi_partials(dev_cm(A), dev_cm(B), 15))
+    total = np.zeros((m, n), dtype=object)
+    for h in range(H.shape[0]):
+        total = total + H[h].T.astype(object) * 2197 ** h
+    assert np.all(total == res["x"])
+    C = to_np(gpu_lib.dgemm_ozi(dev_cm(A), dev_cm(B), 15))
+    assert bits_equal(C, res["C"])
