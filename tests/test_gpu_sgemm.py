@@ -134,3 +134,23 @@ def test_sgemm_16384_sampled_and_accuracy(gpu_lib):
     err_n = o.normalized_errors_block(Cn.astype(np.float64), A64, B64, rows, cols)
     announce(f"normalized error: emulated {err.max():.3e}, native {err_n.max():.3e}")
     assert err.max() <= 2.0 ** -22
+
+
+@pytest.mark.slow
+def test_sgemm_at_the_largest_k(gpu_lib):
+    """k = 131072 (OZFP4_MAX_K) with the default moduli for 24-bit
+    capacities, wide exponents and adversarial all-equal lines: C bit for
+    bit against the oracle."""
+    import torch
+    m, n, k = 40, 24, gpu_lib.OZFP4_MAX_K
+    L = gpu_lib.sgemm_moduli(k)
+    A, B = dgemm_inputs(m, n, k, 2.0, SEED + 20)
+    A, B = A.astype(np.float32), B.astype(np.float32)
+    A[0, :] = np.float32(3.0)
+    B[:, 0] = np.float32(-5.0)
+    want = o.sgemm(A, B, L)["C"]
+    announce(f"sgemm k={k} L={L}")
+    Ad = torch.from_numpy(np.ascontiguousarray(A.T)).cuda().t()
+    Bd = torch.from_numpy(np.ascontiguousarray(B.T)).cuda().t()
+    C = gpu_lib.sgemm(Ad, Bd).cpu().numpy()
+    assert np.array_equal(C.view(np.uint32), want.view(np.uint32))
