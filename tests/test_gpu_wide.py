@@ -116,3 +116,23 @@ def test_wide_phi4_8192_sampled_and_more_accurate(gpu_lib):
                          for i in range(len(rows)) for j in range(len(cols)))
     announce(f"normalized error: 53-bit {errs[53]:.3e}, 63-bit {errs[63]:.3e}")
     assert errs[63] * 2 ** 6 <= errs[53]
+
+
+@pytest.mark.slow
+def test_wide_at_the_largest_k(wide):
+    """k = 131072 (OZFP4_MAX_K) with all 27 moduli and 63-bit capacities
+    (four CRT chunks, the exact path for every element): residues and C bit
+    for bit against the oracle, on wide exponents and on lines of equal
+    largest values."""
+    m, n, k, L = 24, 16, wide.OZFP4_MAX_K, 27
+    A, B = dgemm_inputs(m, n, k, 4.0, SEED + 5)
+    A[0, :] = 1.0 - 2.0 ** -53
+    B[:, 0] = -(1.0 - 2.0 ** -53)
+    res = o.dgemm(A, B, L, cmax=63)
+    assert (res["cA"], res["cB"]) == (63, 63)
+    announce(f"wide residues and dgemm k={k} L={L}")
+    R = to_np(wide.residues(dev_cm(A), dev_cm(B), L))
+    for l in range(L):
+        assert np.array_equal(R[l].T.astype(np.int64), res["r"][l]), f"modulus {res['moduli'][l]}"
+    C = to_np(wide.dgemm(dev_cm(A), dev_cm(B), L))
+    assert bits_equal(C, res["C"])
