@@ -375,6 +375,7 @@ __global__ __launch_bounds__(256) void k_crt(
     }
   }
   const int tj = line_shift(amaxB[j], cB);
+  double outv[4] = {0.0, 0.0, 0.0, 0.0};
 #pragma unroll
   for (int e = 0; e < 4; ++e) {
     const int64_t i = i0 + e;
@@ -389,8 +390,19 @@ __global__ __launch_bounds__(256) void k_crt(
       if constexpr (NC == 3) done = crt_fast3(sig[e][0], sig[e][1], sig[e][2], q, cc, e2, &out);
       if (!done)
         out = crt_exact(sig[e][0], sig[e][1], sig[e][2], NC == 4 ? sig[e][NC - 1] : 0.0, q, cc, e2);
-      C[i + j * ldc] = out;
+      outv[e] = out;
     }
+  }
+  // two 16-byte stores for the four rows where the column is aligned
+  double* dst = C + i0 + j * ldc;
+  if (i0 + 3 < m && ((uintptr_t)dst & 15) == 0) {
+    typedef double d2 __attribute__((ext_vector_type(2)));
+    reinterpret_cast<d2*>(dst)[0] = d2{outv[0], outv[1]};
+    reinterpret_cast<d2*>(dst)[1] = d2{outv[2], outv[3]};
+  } else {
+#pragma unroll
+    for (int e = 0; e < 4; ++e)
+      if (i0 + e < m) dst[e] = outv[e];
   }
 }
 

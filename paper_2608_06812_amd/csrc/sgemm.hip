@@ -107,6 +107,7 @@ __global__ __launch_bounds__(256) void k_crt_f32(
     }
   }
   const int tj = line_shift(amaxB[j], cB);
+  float outv[4] = {0.0f, 0.0f, 0.0f, 0.0f};
 #pragma unroll
   for (int e = 0; e < 4; ++e) {
     const int64_t i = i0 + e;
@@ -116,9 +117,19 @@ __global__ __launch_bounds__(256) void k_crt_f32(
 #pragma unroll
       for (int c = NC - 2; c >= 0; --c) Qe = __builtin_fma(sig[e][c], cc->Qc[c], Qe);
       const double q = __builtin_rint(Qe);
-      C[i + j * ldc] =
+      outv[e] =
           crt_exact_f32(sig[e][0], sig[e][1], sig[e][2], NC == 4 ? sig[e][NC - 1] : 0.0, q, cc, e2);
     }
+  }
+  // one 16-byte store for the four rows where the column is aligned
+  float* dst = C + i0 + j * ldc;
+  if (i0 + 3 < m && ((uintptr_t)dst & 15) == 0) {
+    typedef float f4 __attribute__((ext_vector_type(4)));
+    *reinterpret_cast<f4*>(dst) = f4{outv[0], outv[1], outv[2], outv[3]};
+  } else {
+#pragma unroll
+    for (int e = 0; e < 4; ++e)
+      if (i0 + e < m) dst[e] = outv[e];
   }
 }
 
