@@ -75,3 +75,33 @@ def test_finalize_then_reuse(gpu_lib):
     C3 = gpu_lib.igemm_s8(A8d, B8d).cpu().numpy()
     assert bits_equal(C1, C2) and bits_equal(C1, o.dgemm(A, B, 19)["C"])
     assert np.array_equal(C3, o.igemm_s8(A8, B8))
+
+
+def test_workspace_allocation_failure_is_reported_and_recovered(gpu_lib):
+    """Sizes that pass the argument checks but need a workspace far beyond
+    the device's memory return OZFP4_ENOMEM before any kernel runs (the
+    small buffers passed are never read); the next call of normal size
+    allocates again and is exact."""
+    import torch
+    total = torch.cuda.get_device_properties(0).total_memory
+    big, kk = 1 << 20, 1 << 16          # dgemm: m = n = 2^20, k = 1
+    m8 = 1 << 24                        # igemm_s8: m = n = 2^24, k = 2^16
+    dgemm_ws = big * big * 19           # residue bytes alone
+    igemm_ws = 2 * 3 * m8 * kk // 2     # limb planes of A and B
+    if min(dgemm_ws, igemm_ws) < 2 * total:
+        pytest.skip("device memory too large for a certain allocation failure")
+    dummy = torch.zeros(16, dtype=torch.float64, device="cuda")
+    dummy8 = torch.zeros(16, dtype=torch.int8, device="cuda")
+    out32 = torch.zeros(16, dtype=torch.int32, device="cuda")
+    announce("dgemm and igemm_s8 with a workspace beyond the device: ENOMEM")
+    p = dummy.data_ptr()
+    assert gpu_lib.ozfp4_dgemm(big, big, 1, p, big, p, 1, p, big, 19) == gpu_lib.OZFP4_ENOMEM
+    assert gpu_lib.ozfp4_igemm_s8(m8, m8, kk, dummy8.data_ptr(), m8, dummy8.data_ptr(), kk,
+                                  out32.data_ptr(), m8) == gpu_lib.OZFP4_ENOMEM
+    torch.cuda.synchronize()
+    assert float(dummy.abs().sum()) == 0.0 and int(out32.abs().sum()) == 0
+    m, n, k = 60, 50, 100
+    A, B = dgemm_inputs(m, n, k, 0.5, SEED + 4)
+    announce("dgemm of normal size after ENOMEM")
+    C = to_np(gpu_lib.dgemm(dev_cm(A), dev_cm(B), 19))
+    assert bits_equal(C, o.dgemm(A, B, 19)["C"])
