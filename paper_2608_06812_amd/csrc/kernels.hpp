@@ -323,12 +323,23 @@ __global__ __launch_bounds__(512, 1) void k_gemm_s8(
     for (int v = 0; v < 16; ++v) asm volatile("" ::"v"(out[i][v]));
   const int64_t col = tn * kTileS8N + wn * 32 + (lane & 31);
   const int64_t row0 = tm * kTileS8M + wm * 64 + (lane >> 5) * 4;
+  // four consecutive rows per (i, g): one 16-byte store where the column
+  // is aligned and all four rows exist
+  typedef int i4 __attribute__((ext_vector_type(4)));
 #pragma unroll
   for (int i = 0; i < 2; ++i)
 #pragma unroll
-    for (int v = 0; v < 16; ++v) {
-      const int64_t row = row0 + i * 32 + (v >> 2) * 8 + (v & 3);
-      if (row < m && col < n) C[row + col * ldc] = (int32_t)out[i][v];
+    for (int g = 0; g < 4; ++g) {
+      const int64_t r = row0 + i * 32 + g * 8;
+      int32_t* dst = C + r + col * ldc;
+      if (col < n && r + 3 < m && ((uintptr_t)dst & 15) == 0) {
+        *reinterpret_cast<i4*>(dst) = i4{(int)out[i][4 * g], (int)out[i][4 * g + 1],
+                                          (int)out[i][4 * g + 2], (int)out[i][4 * g + 3]};
+        continue;
+      }
+#pragma unroll
+      for (int e = 0; e < 4; ++e)
+        if (r + e < m && col < n) dst[e] = (int32_t)out[i][4 * g + e];
     }
 }
 
