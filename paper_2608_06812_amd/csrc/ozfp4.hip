@@ -675,6 +675,9 @@ int ozfp4_finalize(void) {
     (void)hipDeviceSynchronize();
     release_device(d);
   }
+  // the events of a pending profiled call are gone with the device state
+  g_pending_stages = 0;
+  g_nstages = 0;
   if (cur >= 0) (void)hipSetDevice(cur);
   return OZFP4_OK;
 }

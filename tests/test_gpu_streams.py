@@ -105,3 +105,24 @@ def test_workspace_allocation_failure_is_reported_and_recovered(gpu_lib):
     announce("dgemm of normal size after ENOMEM")
     C = to_np(gpu_lib.dgemm(dev_cm(A), dev_cm(B), 19))
     assert bits_equal(C, o.dgemm(A, B, 19)["C"])
+
+
+def test_stage_times_after_finalize(gpu_lib):
+    """A profiled asynchronous call whose events were released by
+    ozfp4_finalize leaves no stage times behind (and no stale events)."""
+    import torch
+    A8, B8 = int8_inputs(64, 64, 128, SEED + 5)
+    Ad = torch.from_numpy(np.ascontiguousarray(A8.T)).cuda().t()
+    Bd = torch.from_numpy(np.ascontiguousarray(B8.T)).cuda().t()
+    announce("profiled igemm_s8, finalize, stage times")
+    gpu_lib.ozfp4_profile(True)
+    try:
+        gpu_lib.igemm_s8(Ad, Bd)
+        torch.cuda.synchronize()
+        assert gpu_lib.ozfp4_finalize() == gpu_lib.OZFP4_OK
+        assert gpu_lib.ozfp4_stage_times() == []
+        C = gpu_lib.igemm_s8(Ad, Bd).cpu().numpy()
+        assert len(gpu_lib.ozfp4_stage_times()) == 3
+    finally:
+        gpu_lib.ozfp4_profile(False)
+    assert np.array_equal(C, o.igemm_s8(A8, B8))
