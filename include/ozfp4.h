@@ -334,6 +334,39 @@ int ozfp4_ozi_partials(int64_t m, int64_t n, int64_t k,
                        const double* A, int64_t lda, const double* B, int64_t ldb,
                        int n_limbs, int64_t* H, int64_t ldh);
 
+/* ---- reference measurements ---------------------------------------------
+ * Kernels that take part in no product of the library. They give the rates
+ * the residue GEMM is measured against, and a known byte count for memory
+ * counters. All are asynchronous on the library stream; arguments are
+ * checked on the host (OZFP4_EINVAL) before any GPU work. */
+
+/* The FP4 matrix-core rate with no memory traffic: `blocks` blocks of eight
+ * waves, each wave running `iterations` times the 32 FP4 MFMAs of one
+ * k = 128 stage of the residue GEMM, with the GEMM's register tile, on
+ * pseudo-random E2M1 operands (from `seed`) that are changed before every
+ * k fragment. Writes one checksum per thread to the DEVICE array
+ * sink[blocks * 512]. Executed flops: blocks * 8 * iterations * 32 * 131072.
+ * blocks in 1..2^22, iterations >= 1. */
+int ozfp4_calib_mfma(int64_t blocks, int64_t iterations, uint32_t seed, float* sink);
+
+/* A plain single-product FP4 GEMM, the effective FP4 rate R of the runtime
+ * model (Sec. VII-C, Eq. (model)): C = A B in FP32, where A (m x k) and B
+ * (k x n) are single planes of E2M1 codes in the limb-plane fragment layout
+ * (see ozfp4_limb_planes: 32-line blocks of k/64 fragments; A's lines are
+ * its rows, B's lines its columns). C is a DEVICE column-major m x n FP32
+ * matrix with ldc >= m; exact (every sum is a multiple of 1/4 below 2^22).
+ * m and n multiples of 256, k a multiple of 128 in 384..65536. Streams the
+ * planes through the residue GEMM's LDS-DMA ring with a 256 x 256 block
+ * tile. */
+int ozfp4_calib_gemm_fp4(int64_t m, int64_t n, int64_t k, const uint8_t* plane_a,
+                         const uint8_t* plane_b, float* C, int64_t ldc);
+
+/* Reads the DEVICE buffer src[bytes] once through buffer-form LDS DMA (the
+ * residue GEMM's copy path) with `blocks` blocks of four waves, and writes
+ * one XOR checksum per thread to the DEVICE array sink[blocks * 256].
+ * bytes a multiple of 1024, at most 2^31 - 1024; blocks in 1..2^22. */
+int ozfp4_calib_dma_read(const uint8_t* src, int64_t bytes, int64_t blocks, uint32_t* sink);
+
 /* ---- stage timing ------------------------------------------------------ */
 
 /* Enable (1) or disable (0) HIP-event timing of the stages of the next
@@ -348,7 +381,10 @@ int ozfp4_profile(int enable);
  * 0 scale, 1 encode A, 2 encode B, 3 residue GEMM, 4 CRT. dgemm_ozi stages:
  * 0 scale, 1 encode A, 2 encode B, 3 limb GEMM, 4 reduction. igemm_s8
  * stages: 0 encode A, 1 encode B, 2 GEMM (asynchronous: this call waits for
- * its last event). */
+ * its last event, and so does the next call of the library that records
+ * stage events, before it records over them; the parity hooks record events
+ * but are not profiled calls, so they leave these times as they were).
+ * Returns OZFP4_EHIP if an event cannot be read. */
 int ozfp4_stage_times(double* ms, int max, int* n_stages);
 
 #ifdef __cplusplus

@@ -1,0 +1,301 @@
+// Reference kernels for the measurements beside the residue GEMM. They do
+// not take part in any product of the library; they give the rates the GEMM
+// is measured against:
+//   * k_calib_mfma: the FP4 matrix-core rate with no memory traffic, on
+//     operands that change with every k fragment (the attainable rate of
+//     the residue GEMM's own register tile and MFMA order);
+//   * k_calib_gemm_fp4: a plain single-product FP4 GEMM, C = A B in FP32,
+//     streamed through the same LDS-DMA ring as the residue GEMM: the
+//     effective FP4 rate R of the runtime model (Sec. VII-C, Eq. (model));
+//   * k_calib_dma_read: reads a buffer through buffer-form LDS DMA only,
+//     a known byte count for calibrating memory counters on that path.
+// A translation unit of its own, so nothing here can change how the
+// compiler schedules the default kernels.
+#include "calibrate.hpp"
+#include "device_common.hpp"
+
+namespace ozfp4 {
+
+namespace {
+
+__device__ __forceinline__ uint32_t mix32(uint32_t x) {
+  // a 32-bit avalanche finaliser (multiply-xorshift)
+  x ^= x >> 16;
+  x *= 0x7feb352du;
+  x ^= x >> 15;
+  x *= 0x846ca68bu;
+  x ^= x >> 16;
+  return x;
+}
+
+// ------------------------------------------------------- register-only loop
+// Eight waves per block (two per SIMD) with the residue GEMM's register tile:
+// operand registers a[2][2], b[2][2] (plane, 32-line block) and the three
+// accumulator sets acc[3][2][2]. One iteration is one k = 128 stage of the
+// GEMM: two k fragments of 16 products each, in the GEMM's order. Before
+// each k fragment the operand words are XOR-ed with a fresh pseudo-random
+// word (an LCG in a scalar register), so the operands change like streamed
+// data while every lane keeps its own random codes.
+__global__ __launch_bounds__(512, 1) void k_calib_mfma(int64_t iters, uint32_t seed,
+                                                       float* __restrict__ sink) {
+  const uint32_t gid = blockIdx.x * 512u + threadIdx.x;
+  v4i a[2][2], b[2][2];
+#pragma unroll
+  for (int p = 0; p < 2; ++p)
+#pragma unroll
+    for (int i = 0; i < 2; ++i)
+#pragma unroll
+      for (int w = 0; w < 4; ++w) {
+        const uint32_t idx = (uint32_t)((p * 2 + i) * 4 + w);
+        a[p][i][w] = (int)mix32(seed ^ (gid * 0x9e3779b9u) ^ (idx * 0x85ebca6bu));
+        b[p][i][w] = (int)mix32(~seed ^ (gid * 0xc2b2ae35u) ^ (idx * 0x27d4eb2fu));
+      }
+  v16f acc[3][2][2];
+#pragma unroll
+  for (int s = 0; s < 3; ++s)
+#pragma unroll
+    for (int i = 0; i < 2; ++i)
+#pragma unroll
+      for (int j = 0; j < 2; ++j)
+#pragma unroll
+        for (int v = 0; v < 16; ++v) acc[s][i][j][v] = 0.0f;
+  uint32_t r = __builtin_amdgcn_readfirstlane(mix32(seed + blockIdx.x));
+  for (int64_t it = 0; it < iters; ++it) {
+#pragma unroll
+    for (int kf = 0; kf < 2; ++kf) {
+      r = r * 1664525u + 1013904223u;
+#pragma unroll
+      for (int p = 0; p < 2; ++p)
+#pragma unroll
+        for (int i = 0; i < 2; ++i)
+#pragma unroll
+          for (int w = 0; w < 4; ++w) {
+            a[p][i][w] ^= (int)r;
+            b[p][i][w] ^= (int)(r >> 3 | r << 29);
+          }
+#pragma unroll
+      for (int i = 0; i < 2; ++i)
+#pragma unroll
+        for (int j = 0; j < 2; ++j) {
+          acc[0][i][j] = mfma_fp4(a[0][i], b[0][j], acc[0][i][j]);
+          acc[1][i][j] = mfma_fp4(a[0][i], b[1][j], acc[1][i][j]);
+        }
+#pragma unroll
+      for (int i = 0; i < 2; ++i)
+#pragma unroll
+        for (int j = 0; j < 2; ++j) acc[1][i][j] = mfma_fp4(a[1][i], b[0][j], acc[1][i][j]);
+#pragma unroll
+      for (int i = 0; i < 2; ++i)
+#pragma unroll
+        for (int j = 0; j < 2; ++j) acc[2][i][j] = mfma_fp4(a[1][i], b[1][j], acc[2][i][j]);
+    }
+  }
+  float sum = 0.0f;
+#pragma unroll
+  for (int s = 0; s < 3; ++s)
+#pragma unroll
+    for (int i = 0; i < 2; ++i)
+#pragma unroll
+      for (int j = 0; j < 2; ++j)
+#pragma unroll
+        for (int v = 0; v < 16; ++v) sum += acc[s][i][j][v];
+  sink[gid] = sum;
+}
+
+// ------------------------------------------------------------ plain FP4 GEMM
+// C (FP32, column-major, ldc) = A B for one FP4 plane of A (m lines) and one
+// of B (n lines), both in the fragment layout of the limb planes with k
+// fragments per 32-line block. m, n multiples of 256, k a multiple of 128,
+// at least 384. The products are multiples of 1/4 of magnitude <= 36, so C
+// is exact for k <= 2^16 (sums below 2^22).
+//
+// Block tile 256 x 256, eight waves (two per SIMD) of 64 x 128 (2 x 4 MFMA
+// tiles, 128 accumulator registers). A k = 128 stage is 32 fragments (A: 8
+// line blocks x 2 k fragments, then B the same), 32 KiB, streamed into a
+// 3-slot LDS ring by the residue GEMM's buffer-form DMA, two stages ahead,
+// 4 copies per wave in pairs between the MFMAs; the stage handover (wait
+// for the next stage, barrier) sits before the stage's last four MFMAs.
+constexpr int kCalTile = 256;
+constexpr int kCalStageFrags = 32;
+constexpr int kCalStageBytes = kCalStageFrags * kFragBytes;
+constexpr int kCalDma = kCalStageFrags / kWaves;   // 4
+
+__device__ __forceinline__ constexpr int calA(int rb, int kbl) { return (rb * 2 + kbl) * kFragBytes; }
+__device__ __forceinline__ constexpr int calB(int cb, int kbl) { return (16 + cb * 2 + kbl) * kFragBytes; }
+
+__global__ __launch_bounds__(512, 1) void k_calib_gemm_fp4(
+    const uint8_t* __restrict__ PA, const uint8_t* __restrict__ PB, float* __restrict__ C,
+    int64_t ldc, int64_t kblocks, int64_t tiles_m, int64_t tiles_n) {
+  __shared__ __attribute__((aligned(1024))) uint8_t lds[kRing * kCalStageBytes];
+  int l;
+  int64_t tm, tn;
+  tile_coords(blockIdx.x, tiles_m * tiles_n, tiles_m, tiles_n, &l, &tm, &tn);
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int wm = wave >> 1, wn = wave & 1;
+  const int rbw = 2 * wm, cbw = 4 * wn;   // this wave's first A / B line block
+
+  const int nst = (int)(kblocks / 2);
+  __amdgpu_buffer_rsrc_t src[kCalDma];
+#pragma unroll
+  for (int j = 0; j < kCalDma; ++j) {
+    const int f = wave * kCalDma + j;
+    const int g = f & 15, kbl = g & 1, blk = g >> 1;
+    const uint8_t* base = f < 16 ? PA + ((tm * 8 + blk) * kblocks + kbl) * kFragBytes
+                                 : PB + ((tn * 8 + blk) * kblocks + kbl) * kFragBytes;
+    src[j] = __builtin_amdgcn_make_buffer_rsrc((void*)base, (short)0, nst * 2 * kFragBytes,
+                                               kBufferWord3);
+  }
+  const int lane16 = lane * 16;
+  auto dma = [&](int st, int j) {
+    dma16_buf(src[j], (uint32_t)lane16, (uint32_t)(st * 2 * kFragBytes),
+              lds + (st % kRing) * kCalStageBytes + (wave * kCalDma + j) * kFragBytes);
+  };
+
+  v16f acc[2][4];
+#pragma unroll
+  for (int i = 0; i < 2; ++i)
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+#pragma unroll
+      for (int v = 0; v < 16; ++v) acc[i][j][v] = 0.0f;
+
+#pragma unroll
+  for (int j = 0; j < kCalDma; ++j) dma(0, j);
+#pragma unroll
+  for (int j = 0; j < kCalDma; ++j) dma(1, j);   // nst >= 3
+  wait_vm_lgkm0<kCalDma>();
+  block_sync();
+
+  v4i a[2], b[4];
+  auto read_frags = [&](const uint8_t* sb, int kbl) {
+#pragma unroll
+    for (int i = 0; i < 2; ++i) a[i] = *reinterpret_cast<const v4i*>(sb + calA(rbw + i, kbl) + lane16);
+#pragma unroll
+    for (int j = 0; j < 4; ++j) b[j] = *reinterpret_cast<const v4i*>(sb + calB(cbw + j, kbl) + lane16);
+  };
+  auto mfma_cols = [&](int j0, int j1) {
+#pragma unroll
+    for (int j = j0; j < j1; ++j)
+#pragma unroll
+      for (int i = 0; i < 2; ++i) acc[i][j] = mfma_fp4(a[i], b[j], acc[i][j]);
+  };
+  auto stage_body = [&](int s, bool copy) {
+    const uint8_t* sb = lds + (s % kRing) * kCalStageBytes;
+    read_frags(sb, 0);
+    mfma_cols(0, 4);
+    if (copy) {
+      dma(s + 2, 0);
+      dma(s + 2, 1);
+    }
+    __builtin_amdgcn_sched_barrier(0);
+    read_frags(sb, 1);
+    mfma_cols(0, 2);
+    if (copy) {
+      dma(s + 2, 2);
+      dma(s + 2, 3);
+    }
+    __builtin_amdgcn_sched_barrier(0);
+  };
+
+  int s = 0;
+  for (; s + 2 < nst; ++s) {
+    stage_body(s, true);
+    wait_vm_lgkm0<kCalDma>();   // stage s + 1 landed; reads of stage s done
+    block_sync();
+    mfma_cols(2, 4);
+    __builtin_amdgcn_sched_barrier(0);
+  }
+  stage_body(s, false);
+  wait_vm_lgkm0<0>();
+  block_sync();
+  mfma_cols(2, 4);
+  __builtin_amdgcn_sched_barrier(0);
+  stage_body(s + 1, false);
+  mfma_cols(2, 4);
+
+  // MFMA output layout: lane (col % 32, 4-row group), element v = 4 g + e
+  // at row 8 g + 4 (lane / 32) + e of the 32 x 32 tile
+  typedef float f4 __attribute__((ext_vector_type(4)));
+#pragma unroll
+  for (int i = 0; i < 2; ++i)
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int64_t col = tn * kCalTile + wn * 128 + j * 32 + (lane & 31);
+#pragma unroll
+      for (int g = 0; g < 4; ++g) {
+        const int64_t row = tm * kCalTile + wm * 64 + i * 32 + g * 8 + (lane >> 5) * 4;
+        float* dst = C + row + col * ldc;
+        const f4 v = {acc[i][j][4 * g], acc[i][j][4 * g + 1], acc[i][j][4 * g + 2],
+                      acc[i][j][4 * g + 3]};
+        if (((uintptr_t)dst & 15) == 0) {
+          *reinterpret_cast<f4*>(dst) = v;
+        } else {
+#pragma unroll
+          for (int e = 0; e < 4; ++e) dst[e] = v[e];
+        }
+      }
+    }
+}
+
+// ------------------------------------------------------------- LDS-DMA read
+// Reads nfrag 1 KiB fragments of src through buffer-form LDS DMA, eight in
+// flight per wave (a wave's own 8 KiB of LDS), reads them back from LDS and
+// folds them into one XOR word per thread. Four waves per block; the grid
+// strides over groups of eight fragments.
+constexpr int kDmaReadInFlight = 8;
+
+__global__ __launch_bounds__(256) void k_calib_dma_read(const uint8_t* __restrict__ src,
+                                                         int64_t nfrag,
+                                                         uint32_t* __restrict__ sink) {
+  __shared__ __attribute__((aligned(1024))) uint8_t lds[4 * kDmaReadInFlight * kFragBytes];
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  uint8_t* mine = lds + wave * kDmaReadInFlight * kFragBytes;
+  const __amdgpu_buffer_rsrc_t rsrc = __builtin_amdgcn_make_buffer_rsrc(
+      (void*)src, (short)0, (int)(nfrag * kFragBytes), kBufferWord3);
+  uint32_t x = 0;
+  const int64_t waves = (int64_t)gridDim.x * 4;
+  for (int64_t f0 = ((int64_t)blockIdx.x * 4 + wave) * kDmaReadInFlight; f0 < nfrag;
+       f0 += waves * kDmaReadInFlight) {
+#pragma unroll
+    for (int j = 0; j < kDmaReadInFlight; ++j)
+      if (f0 + j < nfrag)
+        dma16_buf(rsrc, (uint32_t)(lane * 16), (uint32_t)((f0 + j) * kFragBytes),
+                  mine + j * kFragBytes);
+    wait_vm_lgkm0<0>();
+#pragma unroll
+    for (int j = 0; j < kDmaReadInFlight; ++j)
+      if (f0 + j < nfrag) {
+        const v4i v = *reinterpret_cast<const v4i*>(mine + j * kFragBytes + lane * 16);
+        x ^= (uint32_t)(v.x ^ v.y ^ v.z ^ v.w);
+      }
+    wait_vm_lgkm0<0>();   // reads done before the next group overwrites the slots
+  }
+  sink[(int64_t)blockIdx.x * 256 + threadIdx.x] = x;
+}
+
+}  // namespace
+
+hipError_t launch_calib_mfma(hipStream_t stream, int64_t blocks, int64_t iters, uint32_t seed,
+                             float* sink) {
+  hipLaunchKernelGGL(k_calib_mfma, dim3((unsigned)blocks), dim3(512), 0, stream, iters, seed, sink);
+  return hipGetLastError();
+}
+
+hipError_t launch_calib_gemm_fp4(hipStream_t stream, int64_t m, int64_t n, int64_t k,
+                                 const uint8_t* pa, const uint8_t* pb, float* C, int64_t ldc) {
+  const int64_t tiles_m = m / kCalTile, tiles_n = n / kCalTile;
+  hipLaunchKernelGGL(k_calib_gemm_fp4, dim3((unsigned)(tiles_m * tiles_n)), dim3(512), 0, stream,
+                     pa, pb, C, ldc, k / kFragK, tiles_m, tiles_n);
+  return hipGetLastError();
+}
+
+hipError_t launch_calib_dma_read(hipStream_t stream, const uint8_t* src, int64_t bytes,
+                                 int64_t blocks, uint32_t* sink) {
+  hipLaunchKernelGGL(k_calib_dma_read, dim3((unsigned)blocks), dim3(256), 0, stream, src,
+                     bytes / kFragBytes, sink);
+  return hipGetLastError();
+}
+
+}  // namespace ozfp4

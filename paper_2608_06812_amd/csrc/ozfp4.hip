@@ -8,6 +8,7 @@
 #include <cstring>
 #include <mutex>
 
+#include "calibrate.hpp"
 #include "karatsuba.hpp"
 #include "kernels.hpp"
 #include "ozaki1.hpp"
@@ -202,8 +203,28 @@ int make_dgemm_plan(int64_t m, int64_t n, int64_t k, int L, DgemmPlan* p, bool f
 
 inline unsigned blocks_for(int64_t n, int per) { return (unsigned)((n + per - 1) / per); }
 
+// Stage times of an asynchronous profiled call (ozfp4_igemm_s8) are read
+// from its events only when asked for; a later call records over the same
+// events, so the pending times are read first.
+int resolve_pending() {
+  if (g_pending_stages <= 0) return OZFP4_OK;
+  const int n = g_pending_stages;
+  g_pending_stages = 0;
+  DeviceState& d = g_dev[g_pending_device];
+  HIP_TRY(hipEventSynchronize(d.ev[n]));
+  for (int i = 0; i < n; ++i) {
+    float t = 0.f;
+    HIP_TRY(hipEventElapsedTime(&t, d.ev[i], d.ev[i + 1]));
+    g_stage_ms[i] = t;
+  }
+  g_nstages = n;
+  return OZFP4_OK;
+}
+
 void record(DeviceState* d, int i) {
-  if (g_profile) (void)hipEventRecord(d->ev[i], g_stream);
+  if (!g_profile) return;
+  if (i == 0) (void)resolve_pending();   // before its events are recorded over
+  (void)hipEventRecord(d->ev[i], g_stream);
 }
 
 int encode_grid(int64_t nfrag) {
@@ -832,6 +853,30 @@ int ozfp4_residues(int64_t m, int64_t n, int64_t k, const double* A, int64_t lda
   return finish_with_flag(d, reinterpret_cast<int*>(d->ws + p.off_flag), 0);
 }
 
+int ozfp4_calib_mfma(int64_t blocks, int64_t iterations, uint32_t seed, float* sink) {
+  if (blocks < 1 || blocks > (int64_t(1) << 22) || iterations < 1 || !sink) return OZFP4_EINVAL;
+  HIP_TRY(launch_calib_mfma(g_stream, blocks, iterations, seed, sink));
+  return OZFP4_OK;
+}
+
+int ozfp4_calib_gemm_fp4(int64_t m, int64_t n, int64_t k, const uint8_t* plane_a,
+                         const uint8_t* plane_b, float* C, int64_t ldc) {
+  if (m < kTile || n < kTile || m % kTile || n % kTile || !dims_ok(m, n, k)) return OZFP4_EINVAL;
+  if (k < kMinKPad || k % kStageK || k > 65536) return OZFP4_EINVAL;
+  if ((m / kTile) * (n / kTile) > (int64_t(1) << 31) - 1) return OZFP4_EINVAL;
+  if (!plane_a || !plane_b || !C || ldc < m) return OZFP4_EINVAL;
+  HIP_TRY(launch_calib_gemm_fp4(g_stream, m, n, k, plane_a, plane_b, C, ldc));
+  return OZFP4_OK;
+}
+
+int ozfp4_calib_dma_read(const uint8_t* src, int64_t bytes, int64_t blocks, uint32_t* sink) {
+  if (bytes < kFragBytes || bytes % kFragBytes || bytes > (int64_t(1) << 31) - kFragBytes)
+    return OZFP4_EINVAL;
+  if (blocks < 1 || blocks > (int64_t(1) << 22) || !src || !sink) return OZFP4_EINVAL;
+  HIP_TRY(launch_calib_dma_read(g_stream, src, bytes, blocks, sink));
+  return OZFP4_OK;
+}
+
 int ozfp4_profile(int enable) {
   g_profile = enable != 0;
   g_nstages = 0;
@@ -841,16 +886,9 @@ int ozfp4_profile(int enable) {
 
 int ozfp4_stage_times(double* ms, int max, int* n_stages) {
   if (!ms || !n_stages || max < 0) return OZFP4_EINVAL;
-  if (g_pending_stages > 0) {  // asynchronous call: resolve its events now
-    DeviceState& d = g_dev[g_pending_device];
-    HIP_TRY(hipEventSynchronize(d.ev[g_pending_stages]));
-    for (int i = 0; i < g_pending_stages; ++i) {
-      float t = 0.f;
-      HIP_TRY(hipEventElapsedTime(&t, d.ev[i], d.ev[i + 1]));
-      g_stage_ms[i] = t;
-    }
-    g_nstages = g_pending_stages;
-    g_pending_stages = 0;
+  {
+    const int rc = resolve_pending();   // asynchronous call: read its events now
+    if (rc) return rc;
   }
   const int c = std::min(g_nstages, max);
   for (int i = 0; i < c; ++i) ms[i] = g_stage_ms[i];

@@ -61,6 +61,9 @@ _SIGNATURES = {
     "ozfp4_ozi_config": (_int, [_int, _p, _p, _p]),
     "ozfp4_ozi_limb_planes": (_int, [_i64, _i64, _i64, _p, _i64, _p, _i64, _int, _p, _p]),
     "ozfp4_ozi_partials": (_int, [_i64, _i64, _i64, _p, _i64, _p, _i64, _int, _p, _i64]),
+    "ozfp4_calib_mfma": (_int, [_i64, _i64, ctypes.c_uint32, _p]),
+    "ozfp4_calib_gemm_fp4": (_int, [_i64, _i64, _i64, _p, _p, _p, _i64]),
+    "ozfp4_calib_dma_read": (_int, [_p, _i64, _i64, _p]),
     "ozfp4_profile": (_int, [_int]),
     "ozfp4_stage_times": (_int, [_p, _int, _p]),
 }
@@ -197,6 +200,18 @@ def ozfp4_ozi_limb_planes(m, n, k, A, lda, B, ldb, n_limbs, planes_a, planes_b) 
 
 def ozfp4_ozi_partials(m, n, k, A, lda, B, ldb, n_limbs, H, ldh) -> int:
     return load().ozfp4_ozi_partials(m, n, k, A, lda, B, ldb, n_limbs, H, ldh)
+
+
+def ozfp4_calib_mfma(blocks, iterations, seed, sink) -> int:
+    return load().ozfp4_calib_mfma(blocks, iterations, seed, sink)
+
+
+def ozfp4_calib_gemm_fp4(m, n, k, plane_a, plane_b, C, ldc) -> int:
+    return load().ozfp4_calib_gemm_fp4(m, n, k, plane_a, plane_b, C, ldc)
+
+
+def ozfp4_calib_dma_read(src, nbytes, blocks, sink) -> int:
+    return load().ozfp4_calib_dma_read(src, nbytes, blocks, sink)
 
 
 def ozfp4_profile(enable: bool) -> int:
@@ -434,3 +449,49 @@ def sgemm(A, B, n_moduli: int | None = None, out=None):
         _check(ozfp4_sgemm(m, n, k, A.data_ptr(), lda, B.data_ptr(), ldb, C.data_ptr(), ldc, n_moduli),
                "ozfp4_sgemm")
     return C
+
+
+# ------------------------------------------------------- reference measurements
+
+def calib_mfma(blocks: int, iterations: int, seed: int = 1, device=None):
+    """Launches the register-only FP4 MFMA loop (asynchronous on the current
+    torch stream); returns the checksum tensor and the executed flops."""
+    import torch
+    device = torch.device("cuda", torch.cuda.current_device()) if device is None else device
+    sink = torch.empty(blocks * 512, dtype=torch.float32, device=device)
+    with _on(device, sink):
+        _check(ozfp4_calib_mfma(blocks, iterations, seed & 0xFFFFFFFF, sink.data_ptr()),
+               "ozfp4_calib_mfma")
+    return sink, blocks * 8 * iterations * 32 * 131072.0
+
+
+def calib_gemm_fp4(plane_a, plane_b, m: int, n: int, k: int, out=None):
+    """C = A B in FP32 from single E2M1 planes (uint8 device tensors in the
+    fragment layout); returns C (m x n), column-major."""
+    import torch
+    for name, P, lines in (("plane_a", plane_a, m), ("plane_b", plane_b, n)):
+        if not isinstance(P, torch.Tensor) or P.dtype != torch.uint8 or not P.is_cuda:
+            raise TypeError(f"{name} must be a uint8 device tensor")
+        if not P.is_contiguous() or P.numel() < lines * k // 2:
+            raise ValueError(f"{name} must be contiguous with {lines * k // 2} bytes")
+    C = _empty_cm(m, n, torch.float32, plane_a.device) if out is None else out
+    if C.shape != (m, n) or C.dtype != torch.float32 or C.stride(0) != 1:
+        raise ValueError("out must be a column-major float32 (m x n) tensor")
+    with _on(plane_a.device, plane_b, C):
+        _check(ozfp4_calib_gemm_fp4(m, n, k, plane_a.data_ptr(), plane_b.data_ptr(), C.data_ptr(),
+                                    C.stride(1)), "ozfp4_calib_gemm_fp4")
+    return C
+
+
+def calib_dma_read(src, blocks: int = 1024):
+    """Reads the uint8 device tensor src once through LDS DMA (asynchronous);
+    returns the checksum tensor."""
+    import torch
+    if not isinstance(src, torch.Tensor) or src.dtype != torch.uint8 or not src.is_cuda \
+            or not src.is_contiguous():
+        raise TypeError("src must be a contiguous uint8 device tensor")
+    sink = torch.empty(blocks * 256, dtype=torch.int32, device=src.device)
+    with _on(src.device, sink):
+        _check(ozfp4_calib_dma_read(src.data_ptr(), src.numel(), blocks, sink.data_ptr()),
+               "ozfp4_calib_dma_read")
+    return sink

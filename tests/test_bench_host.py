@@ -24,14 +24,27 @@ def test_more_than_one_gpu_is_refused():
     assert res.stdout == ""
 
 
-def test_measured_traffic_matches_the_gemm_source():
-    """The committed FETCH/WRITE figures belong to the residue GEMM source in
-    the tree (bench.py prints them only while the hashes agree)."""
-    assert bench.kernel_source_hash() == bench.MEASURED_TRAFFIC["kernel_source_sha256_16"]
-    with open(os.path.join(ROOT, "profiles", "k_gemm_res_dgemm_16384_L18.md")) as f:
-        text = f.read()
-    assert "%.1f GB" % bench.MEASURED_TRAFFIC["read_GB"] in text
-    assert "(%.2f GB)" % bench.MEASURED_TRAFFIC["write_GB"] in text
+def test_measured_traffic_is_tied_to_the_gemm_source(monkeypatch):
+    """bench.py reports the committed FETCH/WRITE figures only for the
+    residue-GEMM source and workload they were taken on; when they are
+    committed, the profile summary holds the same raw counters."""
+    t = dict(bench.MEASURED_TRAFFIC)
+    if t["kernel_source_sha256_16"] is not None:
+        with open(os.path.join(ROOT, t["profile"])) as f:
+            text = f.read()
+        assert f"{t['fetch_kib']:,}" in text and f"{t['write_kib']:,}" in text
+        assert t["kernel_source_sha256_16"] in text
+        if t["kernel_source_sha256_16"] == bench.kernel_source_hash():
+            got = bench.measured_traffic(*t["workload"][2:])
+            assert got is not None and got["fetch_size_kib_raw"] == t["fetch_kib"]
+    fake = dict(t, kernel_source_sha256_16=bench.kernel_source_hash(), fetch_kib=1000,
+                write_kib=10, fetch_factor=2.0, write_factor=1.0)
+    monkeypatch.setattr(bench, "MEASURED_TRAFFIC", fake)
+    got = bench.measured_traffic(16384, 18)
+    assert abs(got["GB"] - (1000 * 1024 * 2.0 + 10 * 1024) / 1e9) < 1e-12
+    assert bench.measured_traffic(8192, 18) is None            # another workload
+    monkeypatch.setattr(bench, "MEASURED_TRAFFIC", dict(fake, kernel_source_sha256_16="0" * 16))
+    assert bench.measured_traffic(16384, 18) is None           # another source
 
 
 def test_cpu_baseline_record_on_a_tiny_workload():
@@ -40,8 +53,39 @@ def test_cpu_baseline_record_on_a_tiny_workload():
     B = rng.random((32, 64)) - 0.5
     rec = bench.cpu_baseline(A, B, 14, 32, budget_s=0.01)
     assert rec["kind"] == "oracle" and rec["cores"] >= 1 and rec["value"] > 0
-    assert "64x64" in rec["sample"]
+    assert "64x64" in rec["sample"] and rec["os_cpu_count"] == os.cpu_count()
     json.dumps(rec)
+
+
+def test_cpu_baseline_pool_covers_the_block():
+    """With several workers and a block of several tiles, every output of
+    the block is computed once (tiles of 256 x 256)."""
+    rng = np.random.default_rng(5)
+    A = rng.random((600, 40)) - 0.5
+    B = rng.random((40, 600)) - 0.5
+    rec = bench.cpu_baseline(A, B, 14, 40, budget_s=1e9, workers=3, max_side=512)
+    assert rec["cores"] == 3 and "512x512" in rec["sample"]
+
+
+def test_elementwise_metric_against_the_rounded_product():
+    rng = np.random.default_rng(2)
+    A = rng.random((3, 30)) - 0.5
+    B = rng.random((30, 4)) - 0.5
+    rows, cols = np.arange(3), np.arange(4)
+    ref = bench.exact_reference(A, B, rows, cols)
+    fl = np.array([[float(ref[0][i, j]) for j in range(4)] for i in range(3)])
+    rec = bench.elementwise_vs_rounded(fl, ref)
+    assert rec["max_rel_error"] == 0.0 and rec["frac_equal_to_fl"] == 1.0 and rec["max_ulps"] == 0
+    off = fl.copy()
+    off[1, 2] = np.nextafter(off[1, 2], np.inf)
+    rec = bench.elementwise_vs_rounded(off, ref)
+    assert rec["max_ulps"] == 1 and rec["frac_equal_to_fl"] == 11 / 12
+    assert 0 < rec["max_rel_error"] <= 2.0 ** -52 and rec["frac_within_2^-50"] == 1.0
+
+
+def test_stats():
+    st = bench.stats([3.0, 1.0, 2.0, 10.0])
+    assert st["median"] == 2.5 and st["min"] == 1.0 and st["max"] == 10.0 and st["n"] == 4
 
 
 def test_accuracy_bits_against_the_exact_block():

@@ -118,3 +118,19 @@ def test_gemm_steady_loop(asm, tu, prefix, mfma, reads, dma):
     assert _count(loop, r"scratch_") == 0
     # LDS reads go out in batches, several in flight before a wait for all
     assert _largest_read_batch(loop) >= 4, loop[:30]
+    # every product is the unscaled FP4 form, which multiplies by 2^0: the
+    # scaled form would take the scale operand the helper passes as byte 0
+    # (E8M0 2^-127) at its face value
+    assert _count(loop, r"^v_mfma_f32_32x32x64_f8f6f4 ") == mfma, loop[:30]
+    assert _count(loop, r"v_mfma_scale|v_mfma_ld_scale") == 0
+
+
+def test_no_scaled_mfma_anywhere(asm):
+    """No kernel of the library issues a scaled MFMA form or loads a scale
+    register: the E8M0 byte the helper passes is 0, which the scaled form
+    would read as 2^-127."""
+    for tu, text in asm.items():
+        body = [x.strip() for x in text.split("\n") if x.startswith("\t")]
+        assert _count(body, r"^v_mfma_scale|^v_mfma_ld_scale") == 0, tu
+        if tu != "sgemm.hip":   # the FP32 emulation reuses the default GEMM
+            assert _count(body, r"^v_mfma_f32_32x32x64_f8f6f4 ") > 0, tu

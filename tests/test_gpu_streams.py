@@ -126,3 +126,34 @@ def test_stage_times_after_finalize(gpu_lib):
     finally:
         gpu_lib.ozfp4_profile(False)
     assert np.array_equal(C, o.igemm_s8(A8, B8))
+
+
+def test_stage_times_of_pending_call_survive_a_hook(gpu_lib):
+    """A profiled asynchronous igemm_s8 leaves its stage events pending; a
+    parity hook that runs next records over the same events (ozfp4_scales
+    records two of them). The pending times must be read before that: the
+    three igemm stages come back non-negative, and a profiled dgemm after
+    them reports its own five."""
+    import torch
+    A8, B8 = int8_inputs(512, 512, 4096, SEED + 6)
+    Ad = torch.from_numpy(np.ascontiguousarray(A8.T)).cuda().t()
+    Bd = torch.from_numpy(np.ascontiguousarray(B8.T)).cuda().t()
+    A, B = dgemm_inputs(300, 300, 300, 0.5, SEED + 7)
+    Ag, Bg = dev_cm(A), dev_cm(B)
+    announce("profiled igemm_s8, then ozfp4_scales, then stage times")
+    gpu_lib.ozfp4_profile(True)
+    try:
+        gpu_lib.igemm_s8(Ad, Bd)
+        gpu_lib.scales(Ag, Bg, 18)
+        st = gpu_lib.ozfp4_stage_times()
+        assert len(st) == 3 and all(x >= 0.0 for x in st), st
+        assert st[2] > 0.0
+        gpu_lib.igemm_s8(Ad, Bd)
+        gpu_lib.limb_planes(Ag, Bg, 18)
+        st2 = gpu_lib.ozfp4_stage_times()
+        assert len(st2) == 3 and all(x >= 0.0 for x in st2), st2
+        gpu_lib.dgemm(Ag, Bg, 18)
+        st3 = gpu_lib.ozfp4_stage_times()
+        assert len(st3) == 5 and all(x >= 0.0 for x in st3), st3
+    finally:
+        gpu_lib.ozfp4_profile(False)

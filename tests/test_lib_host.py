@@ -296,3 +296,25 @@ def test_binding_argument_checks_on_host():
         ozfp4.dgemm(A, A)                                      # host memory
     with pytest.raises(ValueError, match="device tensor"):
         ozfp4.igemm_s8(A.to(torch.int8), A.to(torch.int8))
+
+
+@pytest.mark.parametrize("call,args", [
+    ("ozfp4_calib_mfma", (0, 10, 1, 1)),                  # no blocks
+    ("ozfp4_calib_mfma", (1 << 23, 10, 1, 1)),            # too many blocks
+    ("ozfp4_calib_mfma", (8, 0, 1, 1)),                   # no iterations
+    ("ozfp4_calib_mfma", (8, 10, 1, 0)),                  # null sink
+    ("ozfp4_calib_gemm_fp4", (300, 256, 384, 1, 1, 1, 300)),    # m not a multiple of 256
+    ("ozfp4_calib_gemm_fp4", (256, 0, 384, 1, 1, 1, 256)),      # n = 0
+    ("ozfp4_calib_gemm_fp4", (256, 256, 256, 1, 1, 1, 256)),    # k below three stages
+    ("ozfp4_calib_gemm_fp4", (256, 256, 400, 1, 1, 1, 256)),    # k not a multiple of 128
+    ("ozfp4_calib_gemm_fp4", (256, 256, 65664, 1, 1, 1, 256)),  # k above the exact range
+    ("ozfp4_calib_gemm_fp4", (256, 256, 384, 1, 1, 1, 255)),    # ldc < m
+    ("ozfp4_calib_gemm_fp4", (256, 256, 384, 0, 1, 1, 256)),    # null plane
+    ("ozfp4_calib_dma_read", (1, 1000, 8, 1)),            # not whole fragments
+    ("ozfp4_calib_dma_read", (1, 0, 8, 1)),
+    ("ozfp4_calib_dma_read", (1, 1 << 31, 8, 1)),         # above the 32-bit buffer range
+    ("ozfp4_calib_dma_read", (1, 4096, 0, 1)),
+    ("ozfp4_calib_dma_read", (0, 4096, 8, 1)),            # null source
+])
+def test_calibration_argument_errors_on_host(lib, call, args):
+    assert getattr(ozfp4, call)(*args) == ozfp4.OZFP4_EINVAL
