@@ -44,6 +44,8 @@ extern "C" {
 #define OZFP4_ENONFINITE  -4  /* NaN or Inf in A or B; C is unspecified            */
 #define OZFP4_ENOMEM      -5  /* device workspace allocation failed                */
 #define OZFP4_EHIP        -6  /* a HIP runtime call failed                         */
+#define OZFP4_ESCRATCH    -7  /* ozfp4_dgemm_noalloc: device not set up, or the
+                                 call needs more than OZFP4_SCRATCH_BYTES       */
 
 #define OZFP4_MIN_MODULI   2
 #define OZFP4_MAX_MODULI  27
@@ -59,6 +61,8 @@ extern "C" {
 #define OZFP4_MAX_K_S8  16777216
 /* Largest product of two of m, n, k (2^48). */
 #define OZFP4_MAX_ELEMENTS ((int64_t)1 << 48)
+/* Size of the fixed scratch of ozfp4_dgemm_noalloc (256 MiB per device). */
+#define OZFP4_SCRATCH_BYTES 268435456
 
 /*
  * ozfp4_dgemm -- C = fl(A B) for FP64 A, B by Ozaki scheme II on FP4 limbs
@@ -91,6 +95,38 @@ int ozfp4_dgemm(int64_t m, int64_t n, int64_t k,
                 const double* A, int64_t lda,
                 const double* B, int64_t ldb,
                 double* C, int64_t ldc, int n_moduli);
+
+/*
+ * ozfp4_init -- sets up the current device for the library: its tables,
+ * stage events, the pinned word for the non-finite flag, and the device
+ * address of the scratch array of ozfp4_dgemm_noalloc. Allocates device
+ * and pinned host memory (held until ozfp4_finalize). Every other entry
+ * point does this by itself on its first call on a device; only
+ * ozfp4_dgemm_noalloc needs it done first. Returns OZFP4_EHIP on failure.
+ */
+int ozfp4_init(void);
+
+/*
+ * ozfp4_dgemm_noalloc -- ozfp4_dgemm without any allocation, for callers
+ * that cannot allocate device memory: code under HIP graph capture, tight
+ * serving loops, harnesses that forbid hipMalloc. Same arguments, result
+ * (bit for bit), error codes and synchronization as ozfp4_dgemm, including
+ * the Karatsuba and capacity settings. Instead of the growing workspace it
+ * uses a fixed array of OZFP4_SCRATCH_BYTES that every device holds for the
+ * life of the process; it calls no hipMalloc, hipFree or other allocating
+ * routine. The caller still owns A, B and C.
+ * Returns OZFP4_ESCRATCH, before any GPU work, if the current device was
+ * not set up (ozfp4_init, or any earlier call of the library on it, since
+ * the last ozfp4_finalize) or if the call's limb planes, residues and line
+ * maxima need more than OZFP4_SCRATCH_BYTES (m = n = k = 2048 with 18
+ * moduli needs 226 MB and fits). Every call on one device shares that
+ * device's array: calls that overlap on one device (asynchronous work on
+ * two streams, two host threads) race, like the regular workspace.
+ */
+int ozfp4_dgemm_noalloc(int64_t m, int64_t n, int64_t k,
+                        const double* A, int64_t lda,
+                        const double* B, int64_t ldb,
+                        double* C, int64_t ldc, int n_moduli);
 
 /*
  * ozfp4_igemm_s8 -- C = A B for INT8 A, B with INT32 C, bit-exact, on FP4

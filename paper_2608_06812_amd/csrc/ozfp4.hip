@@ -18,6 +18,14 @@
 
 using namespace ozfp4;
 
+// Workspace of ozfp4_dgemm_noalloc (limb planes, residues, line maxima and
+// the non-finite flag of one call): a fixed array in every device's copy of
+// the code object, so that entry point never allocates. In host code this
+// name is a host-side stand-in, not a device address: kernels and copies
+// take the address hipGetSymbolAddress returns for the current device
+// (DeviceState::scratch).
+static __device__ __align__(256) uint8_t scratch[OZFP4_SCRATCH_BYTES];
+
 namespace {
 
 constexpr int kMaxDevices = 64;
@@ -34,6 +42,7 @@ struct DeviceState {
   size_t ws_bytes = 0;
   int* h_flag = nullptr;      // pinned host word for the non-finite flag
   hipEvent_t ev[kMaxStages + 1] = {};
+  uint8_t* scratch = nullptr; // this device's address of the scratch array
 };
 
 HostTables g_tables;
@@ -95,6 +104,11 @@ int init_device(DeviceState& d, const HostTables* T) {
   HIP_TRY(hipMemcpy(d.d_lut8, T->lut8, sizeof(T->lut8), hipMemcpyHostToDevice));
   HIP_TRY(hipHostMalloc(reinterpret_cast<void**>(&d.h_flag), sizeof(int), hipHostMallocDefault));
   for (int i = 0; i <= kMaxStages; ++i) HIP_TRY(hipEventCreate(&d.ev[i]));
+  // each device holds its own copy of the scratch array: keep its address
+  void* sp = nullptr;
+  HIP_TRY(hipGetSymbolAddress(&sp, HIP_SYMBOL(scratch)));
+  if (!sp) return OZFP4_EHIP;
+  d.scratch = static_cast<uint8_t*>(sp);
   return OZFP4_OK;
 }
 
@@ -254,13 +268,13 @@ void launch_amax_f64(const double* A, int64_t lda, const double* B, int64_t ldb,
 // A, B and C are double, or float when p.f32.
 int run_dgemm(const DgemmPlan& p, DeviceState* d, const void* Av, int64_t lda, const void* Bv,
               int64_t ldb, void* Cv, int64_t ldc, int last, uint8_t* planes_a_out,
-              uint8_t* planes_b_out) {
+              uint8_t* planes_b_out, uint8_t* ws_base = nullptr) {
   const double* A = static_cast<const double*>(Av);
   const double* B = static_cast<const double*>(Bv);
   const float* Af = static_cast<const float*>(Av);
   const float* Bf = static_cast<const float*>(Bv);
   const HostTables* T = tables();
-  uint8_t* ws = d->ws;
+  uint8_t* ws = ws_base ? ws_base : d->ws;
   uint64_t* amax_a = reinterpret_cast<uint64_t*>(ws + p.off_amax_a);
   uint64_t* amax_b = reinterpret_cast<uint64_t*>(ws + p.off_amax_b);
   int* flag = reinterpret_cast<int*>(ws + p.off_flag);
@@ -524,6 +538,39 @@ int ozfp4_dgemm(int64_t m, int64_t n, int64_t k, const double* A, int64_t lda, c
   return finish_with_flag(d, reinterpret_cast<int*>(d->ws + p.off_flag), 5);
 }
 
+int ozfp4_init(void) {
+  DeviceState* d;
+  return device_state(&d);
+}
+
+int ozfp4_dgemm_noalloc(int64_t m, int64_t n, int64_t k, const double* A, int64_t lda,
+                        const double* B, int64_t ldb, double* C, int64_t ldc, int n_moduli) {
+  int rc = check_dgemm_args(m, n, k, A, lda, B, ldb, n_moduli);
+  if (rc) return rc;
+  if (ldc < std::max<int64_t>(1, m)) return OZFP4_EINVAL;
+  if (m == 0 || n == 0) return OZFP4_OK;
+  if (!C) return OZFP4_EINVAL;
+  // the device must have been set up (ozfp4_init or any earlier call on
+  // it): setting up allocates, and this entry point must not
+  int dev = 0;
+  HIP_TRY(hipGetDevice(&dev));
+  if (dev < 0 || dev >= kMaxDevices || !g_dev[dev].ready || !tables()) return OZFP4_ESCRATCH;
+  DeviceState* d = &g_dev[dev];
+  if (k == 0) {
+    hipLaunchKernelGGL(k_fill_f64_matrix, dim3(stride_blocks(m * n, 256)), dim3(256), 0, g_stream, C,
+                       m, n, ldc);
+    HIP_TRY(hipGetLastError());
+    return OZFP4_OK;
+  }
+  DgemmPlan p;
+  rc = make_dgemm_plan(m, n, k, n_moduli, &p);
+  if (rc) return rc;
+  if (p.total > (size_t)OZFP4_SCRATCH_BYTES) return OZFP4_ESCRATCH;
+  rc = run_dgemm(p, d, A, lda, B, ldb, C, ldc, 4, nullptr, nullptr, d->scratch);
+  if (rc) return rc;
+  return finish_with_flag(d, reinterpret_cast<int*>(d->scratch + p.off_flag), 5);
+}
+
 int ozfp4_igemm_s8(int64_t m, int64_t n, int64_t k, const int8_t* A, int64_t lda, const int8_t* B,
                    int64_t ldb, int32_t* C, int64_t ldc) {
   if (!dims_ok(m, n, k)) return OZFP4_EINVAL;
@@ -712,6 +759,9 @@ const char* ozfp4_strerror(int code) {
     case OZFP4_ENONFINITE: return "NaN or Inf in an input matrix";
     case OZFP4_ENOMEM: return "device workspace allocation failed";
     case OZFP4_EHIP: return "HIP runtime error";
+    case OZFP4_ESCRATCH:
+      return "ozfp4_dgemm_noalloc: device not set up (call ozfp4_init), or the call needs more "
+             "scratch than OZFP4_SCRATCH_BYTES";
     default: return "unknown error code";
   }
 }

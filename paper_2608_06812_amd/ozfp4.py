@@ -28,12 +28,14 @@ OZFP4_EKBOUND = -3
 OZFP4_ENONFINITE = -4
 OZFP4_ENOMEM = -5
 OZFP4_EHIP = -6
+OZFP4_ESCRATCH = -7
 OZFP4_MIN_MODULI = 2
 OZFP4_MAX_MODULI = 27
 OZFP4_MAX_K = 131072
 OZFP4_MAX_K_S8 = 16777216
 OZFP4_MAX_ELEMENTS = 1 << 48
 OZFP4_OZI_MAX_LIMBS = 15
+OZFP4_SCRATCH_BYTES = 268435456
 
 _lib = None
 
@@ -41,6 +43,8 @@ _i64, _int, _p = ctypes.c_int64, ctypes.c_int, ctypes.c_void_p
 _SIGNATURES = {
     "ozfp4_dgemm": (_int, [_i64, _i64, _i64, _p, _i64, _p, _i64, _p, _i64, _int]),
     "ozfp4_igemm_s8": (_int, [_i64, _i64, _i64, _p, _i64, _p, _i64, _p, _i64]),
+    "ozfp4_init": (_int, []),
+    "ozfp4_dgemm_noalloc": (_int, [_i64, _i64, _i64, _p, _i64, _p, _i64, _p, _i64, _int]),
     "ozfp4_set_stream": (_int, [_p]),
     "ozfp4_finalize": (_int, []),
     "ozfp4_strerror": (ctypes.c_char_p, [_int]),
@@ -94,6 +98,14 @@ def load() -> ctypes.CDLL:
 
 def ozfp4_dgemm(m, n, k, A, lda, B, ldb, C, ldc, n_moduli) -> int:
     return load().ozfp4_dgemm(m, n, k, A, lda, B, ldb, C, ldc, n_moduli)
+
+
+def ozfp4_init() -> int:
+    return load().ozfp4_init()
+
+
+def ozfp4_dgemm_noalloc(m, n, k, A, lda, B, ldb, C, ldc, n_moduli) -> int:
+    return load().ozfp4_dgemm_noalloc(m, n, k, A, lda, B, ldb, C, ldc, n_moduli)
 
 
 def ozfp4_igemm_s8(m, n, k, A, lda, B, ldb, C, ldc) -> int:
@@ -287,6 +299,28 @@ def dgemm(A, B, n_moduli: int = 19, out=None):
     with _on(A.device, B, C):
         _check(ozfp4_dgemm(m, n, k, A.data_ptr(), lda, B.data_ptr(), ldb, C.data_ptr(), ldc, n_moduli),
                "ozfp4_dgemm")
+    return C
+
+
+def dgemm_noalloc(A, B, out, n_moduli: int = 19):
+    """ozfp4_dgemm_noalloc into the caller's column-major float64 tensor
+    `out` (m x n): the library allocates nothing; the current device must
+    have been set up (ozfp4_init)."""
+    import torch
+    A, lda = _cm(A, torch.float64, "A")
+    B, ldb = _cm(B, torch.float64, "B")
+    m, k = A.shape
+    k2, n = B.shape
+    if k != k2:
+        raise ValueError("inner dimensions differ")
+    C = out
+    if not isinstance(C, torch.Tensor) or C.shape != (m, n) or C.dtype != torch.float64 or \
+            (C.stride(0) != 1 and m > 1):
+        raise ValueError("out must be a column-major float64 (m x n) tensor")
+    ldc = max(1, C.stride(1) if n > 1 else m)
+    with _on(A.device, B, C):
+        _check(ozfp4_dgemm_noalloc(m, n, k, A.data_ptr(), lda, B.data_ptr(), ldb, C.data_ptr(), ldc,
+                                   n_moduli), "ozfp4_dgemm_noalloc")
     return C
 
 
