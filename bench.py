@@ -254,10 +254,69 @@ def cpu_baseline(A, B, L, k, budget_s=20.0, workers=None, max_side=4096):
                       f"{first[0]}x{first[0]}: {first[1]:.2f} s)"}
 
 
+def _line_integers(X):
+    """Each line of X (the last axis runs along k) as integers times a power
+    of two shared by the line: X = sign * N * 2^base, with N = M 2^sh, M the
+    53-bit significand and sh >= 0 its offset above the line's lowest
+    exponent. Returns (sign, M, sh, base)."""
+    import numpy as np
+    f, e = np.frexp(np.abs(X))
+    M = np.ldexp(f, 53).astype(np.int64)
+    E = e.astype(np.int64) - 53
+    big = np.iinfo(np.int64).max
+    Em = np.where(M == 0, big, E)
+    base = Em.min(axis=-1, keepdims=True)
+    base = np.where(base == big, 0, base)
+    sh = np.where(M == 0, 0, E - base)
+    return np.where(X < 0, -1, 1).astype(np.int64), M, sh, base[..., 0]
+
+
+def _digit(M, sh, q, bits=18):
+    """Digit q (bits [bits q, bits (q + 1))) of N = M 2^sh."""
+    import numpy as np
+    lo = bits * q - sh                       # where the digit starts within M
+    Mu = M.astype(np.uint64)
+    mask = np.uint64((1 << bits) - 1)
+    down = (Mu >> np.clip(lo, 0, 63).astype(np.uint64)) & mask
+    up = (Mu << np.clip(-lo, 0, 63).astype(np.uint64)) & mask
+    return np.where(lo >= 53, 0, np.where(lo >= 0, down, np.where(lo <= -bits, 0, up))).astype(np.int64)
+
+
 def exact_reference(A, B, rows, cols):
-    """Exact (AB)_ij and sum_k |A_ik||B_kj| on a block (oracle)."""
-    import oracle
-    return oracle.exact_block(A, B, rows, cols)
+    """Exact (AB)_ij and sum_k |A_ik||B_kj| on the block rows x cols, as
+    arrays of Fractions: every row of A and column of B becomes integers
+    times a power of two, the integers are cut into 18-bit digits, and each
+    pair of digit matrices is multiplied in FP64, exactly (every sum is
+    below 2^36 k <= 2^53 for k < 2^17); the digit products are recombined
+    with Python integers."""
+    import numpy as np
+    from fractions import Fraction
+    Ab = np.asarray(A, dtype=np.float64)[np.asarray(rows), :]
+    Bb = np.asarray(B, dtype=np.float64)[:, np.asarray(cols)].T.copy()   # lines along k
+    k = Ab.shape[1]
+    if k >= 1 << 17:
+        raise ValueError("k too large for exact FP64 digit products")
+    sa, Ma, sha, ba = _line_integers(Ab)
+    sb, Mb, shb, bb = _line_integers(Bb)
+    da = [_digit(Ma, sha, q) for q in range((53 + int(sha.max(initial=0)) + 17) // 18)]
+    db = [_digit(Mb, shb, q) for q in range((53 + int(shb.max(initial=0)) + 17) // 18)]
+    prod = np.zeros((Ab.shape[0], Bb.shape[0]), dtype=object)
+    absum = np.zeros_like(prod)
+    for p, x in enumerate(da):
+        for q, y in enumerate(db):
+            w = 1 << (18 * (p + q))
+            sp = np.rint((sa * x).astype(np.float64) @ (sb * y).astype(np.float64).T)
+            ap = np.rint(x.astype(np.float64) @ y.astype(np.float64).T)
+            prod = prod + sp.astype(np.int64).astype(object) * w
+            absum = absum + ap.astype(np.int64).astype(object) * w
+    ex = np.empty(prod.shape, dtype=object)
+    ab = np.empty(prod.shape, dtype=object)
+    for i in range(prod.shape[0]):
+        for j in range(prod.shape[1]):
+            sc = Fraction(2) ** (int(ba[i]) + int(bb[j]))
+            ex[i, j] = Fraction(int(prod[i, j])) * sc
+            ab[i, j] = Fraction(int(absum[i, j])) * sc
+    return ex, ab
 
 
 def accuracy_bits(C_block, ref):

@@ -107,3 +107,26 @@ def test_source_hash_ignores_comments_but_not_code():
     assert bench.code_only(code) == bench.code_only(code.replace("\n  ", "\n    "))
     assert bench.code_only(code) != bench.code_only(code.replace("x + 1", "x + 2"))
     assert "comment" not in bench.code_only(code) and "another" not in bench.code_only(code)
+
+
+def test_exact_reference_against_fractions():
+    """bench.py's own exact block product (it does not use the oracle)
+    against plain Fraction sums, on entries spread over many binades, zeros
+    and negative values included."""
+    from fractions import Fraction
+    rng = np.random.default_rng(9)
+    A = (rng.random((5, 37)) - 0.5) * np.exp2(rng.integers(-60, 60, (5, 37)))
+    B = (rng.random((37, 4)) - 0.5) * np.exp2(rng.integers(-60, 60, (37, 4)))
+    A[1, :] = 0.0
+    A[2, 3] = 5e-320                     # subnormal
+    B[7, 2] = -0.0
+    rows, cols = np.array([0, 1, 2, 4]), np.array([0, 2, 3])
+    ex, ab = bench.exact_reference(A, B, rows, cols)
+    for a, i in enumerate(rows):
+        for b, j in enumerate(cols):
+            want = sum(Fraction(float(A[i, q])) * Fraction(float(B[q, j])) for q in range(37))
+            wabs = sum(abs(Fraction(float(A[i, q])) * Fraction(float(B[q, j]))) for q in range(37))
+            assert ex[a, b] == want and ab[a, b] == wabs
+    # and the oracle's independent block product agrees
+    oe, oa = o.exact_block(A, B, rows, cols)
+    assert np.all(oe == ex) and np.all(oa == ab)
