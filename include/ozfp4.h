@@ -97,6 +97,30 @@ int ozfp4_dgemm(int64_t m, int64_t n, int64_t k,
                 double* C, int64_t ldc, int n_moduli);
 
 /*
+ * ozfp4_dgemm_split -- C = fl(A B) for FP64 A, B whose rows or columns span
+ * wide exponent ranges: scheme II with a two-term split of the converted
+ * operands (an extension of Sec. IV-B, whose one-term conversion keeps c
+ * bits measured from each line's largest element). With the shifts and
+ * capacities of ozfp4_dgemm under the paper's 53-bit cap and d =
+ * min(c_A, c_B), every element is split into two integers,
+ *     A1 = round_half_even(A 2^s),  A2 = round_half_even((A 2^s - A1) 2^d),
+ * (B1, B2 likewise with the column shifts t), and
+ *     C = RN((2^2d X11 + 2^d X12 + X22) 2^-(s + t + 2d)),
+ * X11 = A1 B1, X12 = A1 B2 + A2 B1, X22 = A2 B2, each integer product exact
+ * (four residue GEMMs over the same n_moduli moduli, combined in 256-bit
+ * integers): one rounding of the exact product of the split operands. An
+ * element within c_A + d bits of its line's largest element is held
+ * exactly, so lines that span fewer than about c_A + d - 53 binades give
+ * the correctly rounded product. Four times the residue-GEMM work of
+ * ozfp4_dgemm. Same arguments, errors and synchronization as ozfp4_dgemm;
+ * ignores the Karatsuba and capacity settings.
+ */
+int ozfp4_dgemm_split(int64_t m, int64_t n, int64_t k,
+                      const double* A, int64_t lda,
+                      const double* B, int64_t ldb,
+                      double* C, int64_t ldc, int n_moduli);
+
+/*
  * ozfp4_init -- sets up the current device for the library: its tables,
  * stage events, the pinned word for the non-finite flag, and the device
  * address of the scratch array of ozfp4_dgemm_noalloc. Allocates device
@@ -406,7 +430,8 @@ int ozfp4_calib_dma_read(const uint8_t* src, int64_t bytes, int64_t blocks, uint
 /* ---- stage timing ------------------------------------------------------ */
 
 /* Enable (1) or disable (0) HIP-event timing of the stages of the next
- * ozfp4_dgemm / ozfp4_sgemm / ozfp4_dgemm_ozi / ozfp4_igemm_s8 calls,
+ * ozfp4_dgemm / ozfp4_dgemm_split / ozfp4_sgemm / ozfp4_dgemm_ozi /
+ * ozfp4_igemm_s8 calls,
  * recorded on the library's stream. */
 int ozfp4_profile(int enable);
 
@@ -414,7 +439,8 @@ int ozfp4_profile(int enable);
  * min(max, stage count) values go to the HOST array ms[max] and the stage
  * count to the HOST *n_stages (0 if no profiled call ran). Returns OZFP4_OK,
  * or OZFP4_EINVAL for a null pointer or max < 0. dgemm and sgemm stages:
- * 0 scale, 1 encode A, 2 encode B, 3 residue GEMM, 4 CRT. dgemm_ozi stages:
+ * 0 scale, 1 encode A, 2 encode B, 3 residue GEMM, 4 CRT (dgemm_split: the
+ * same, each encode covering both terms, the GEMM stage all four products). dgemm_ozi stages:
  * 0 scale, 1 encode A, 2 encode B, 3 limb GEMM, 4 reduction. igemm_s8
  * stages: 0 encode A, 1 encode B, 2 GEMM (asynchronous: this call waits for
  * its last event, and so does the next call of the library that records

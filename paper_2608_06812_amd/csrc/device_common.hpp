@@ -86,6 +86,9 @@ __device__ __forceinline__ int line_shift(uint64_t amax_bits, int cap) {
 //   2^63; the same floor step first brings E x down to an exact E d with
 //   |d| < 2^15 (the quotient is within 2^8 of floor(x / m), and the FMA's
 //   result is representable, so exact), and the step above then runs on d.
+//   kSecond (the two-term split): the value encoded is the second term
+//   x2 = round_half_even((A 2^s - x) 2^d2), |x2| <= 2^(d2 - 1); A 2^s - x
+//   is exact (the fraction of A 2^s), and so is its product by 2^d2.
 constexpr int kEncWaves = 4;
 
 template <typename T>
@@ -94,12 +97,12 @@ __device__ __forceinline__ uint32_t lut_lookup(double y) {
   return *reinterpret_cast<__attribute__((address_space(3))) const T*>((size_t)addr);
 }
 
-template <bool kKar, bool kWide, typename TIn = double>
+template <bool kKar, bool kWide, typename TIn = double, bool kSecond = false>
 __global__ __launch_bounds__(256) void k_encode_dgemm(
     const TIn* __restrict__ X, int64_t rs, int64_t ks, int64_t lines, int64_t k,
     const uint64_t* __restrict__ amax, int cap, uint8_t* __restrict__ planes,
     int64_t plane_bytes, int64_t nfrag, int64_t kblocks, int L,
-    const ModConst* __restrict__ mc, const void* __restrict__ lut, int lut_entries) {
+    const ModConst* __restrict__ mc, const void* __restrict__ lut, int lut_entries, int d2) {
   typedef typename std::conditional<kKar, uint32_t, uint16_t>::type Entry;
   constexpr double kE = (double)sizeof(Entry);
   extern __shared__ __attribute__((aligned(16))) uint8_t s_raw[];
@@ -146,7 +149,9 @@ __global__ __launch_bounds__(256) void k_encode_dgemm(
     }
 #pragma unroll
     for (int e = 0; e < 32; ++e) {
-      const double t = __builtin_rint(__builtin_ldexp(xe[e], s));
+      const double T = __builtin_ldexp(xe[e], s);
+      double t = __builtin_rint(T);
+      if constexpr (kSecond) t = __builtin_rint(__builtin_ldexp(T - t, d2));
       // finite inputs give |t| <= 2^53 (2^63 when wide); NaN/Inf (reported
       // by the scale stage) must not drive the table address out of range
       xe[e] = (__builtin_fabs(t) <= (kWide ? 0x1p63 : 0x1p53)) ? kE * t : 0.0;

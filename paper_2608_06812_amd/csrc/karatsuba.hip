@@ -224,7 +224,7 @@ hipError_t launch_encode_kar(bool wide, unsigned grid, size_t lds_bytes, hipStre
                              const void* lut, int lut_entries) {
   auto kern = wide ? k_encode_dgemm<true, true> : k_encode_dgemm<true, false>;
   hipLaunchKernelGGL(kern, dim3(grid), dim3(256), lds_bytes, stream, X, rs, ks, lines, k, amax,
-                     cap, planes, plane_bytes, nfrag, kblocks, L, mc, lut, lut_entries);
+                     cap, planes, plane_bytes, nfrag, kblocks, L, mc, lut, lut_entries, 0);
   return hipGetLastError();
 }
 

@@ -13,6 +13,7 @@
 #include "kernels.hpp"
 #include "ozaki1.hpp"
 #include "sgemm.hpp"
+#include "split.hpp"
 #include "ozfp4.h"
 #include "tables.hpp"
 
@@ -318,7 +319,7 @@ int run_dgemm(const DgemmPlan& p, DeviceState* d, const void* Av, int64_t lda, c
     hipLaunchKernelGGL(enc,
                        dim3(encode_grid(nfa)), dim3(256), lut_bytes, g_stream, A, (int64_t)1, lda,
                        p.m, p.k, amax_a, p.cA, pa, p.plane_a, nfa, p.kblocks, L, d->d_mod, lut,
-                       lut_entries);
+                       lut_entries, 0);
   }
   HIP_TRY(hipGetLastError());
   record(d, 2);
@@ -335,7 +336,7 @@ int run_dgemm(const DgemmPlan& p, DeviceState* d, const void* Av, int64_t lda, c
     hipLaunchKernelGGL(enc,
                        dim3(encode_grid(nfb)), dim3(256), lut_bytes, g_stream, B, ldb, (int64_t)1,
                        p.n, p.k, amax_b, p.cB, pb, p.plane_b, nfb, p.kblocks, L, d->d_mod, lut,
-                       lut_entries);
+                       lut_entries, 0);
   }
   HIP_TRY(hipGetLastError());
   record(d, 3);
@@ -500,6 +501,96 @@ int finish_with_flag(DeviceState* d, const int* dflag, int nstages) {
   return *d->h_flag ? OZFP4_ENONFINITE : OZFP4_OK;
 }
 
+// ------------------------------------------------------ two-term split
+
+// The split route: the paper's 53-bit capacities for both terms, d =
+// min(c_A, c_B); four planes sets (A1, A2, B1, B2) and four residue sets.
+struct SplitPlan {
+  int64_t m, n, k;
+  int L, cA, cB, d;
+  int64_t m_pad, n_pad, k_pad, kblocks, plane_a, plane_b, rset;
+  size_t off_amax_a, off_amax_b, off_flag, off_pa1, off_pa2, off_pb1, off_pb2, off_r, total;
+};
+
+int make_split_plan(int64_t m, int64_t n, int64_t k, int L, SplitPlan* p) {
+  const HostTables* T = tables();
+  if (!T) return OZFP4_EHIP;
+  p->m = m; p->n = n; p->k = k; p->L = L;
+  if (!capacity_split(T->P[L], k, 53, &p->cA, &p->cB)) return OZFP4_EMODULI;
+  p->d = std::min(p->cA, p->cB);
+  p->m_pad = round_up(m, kTile);
+  p->n_pad = round_up(n, kTile);
+  p->k_pad = plane_k_pad(k);
+  p->kblocks = p->k_pad / kFragK;
+  p->plane_a = p->m_pad * p->k_pad / 2;
+  p->plane_b = p->n_pad * p->k_pad / 2;
+  p->rset = p->m_pad * p->n_pad * L;
+  size_t off = 0;
+  p->off_amax_a = off; off = align256(off + sizeof(uint64_t) * p->m_pad);
+  p->off_amax_b = off; off = align256(off + sizeof(uint64_t) * p->n_pad);
+  p->off_flag = off;   off = align256(off + 256);
+  p->off_pa1 = off;    off = align256(off + (size_t)p->plane_a * 2 * L);
+  p->off_pa2 = off;    off = align256(off + (size_t)p->plane_a * 2 * L);
+  p->off_pb1 = off;    off = align256(off + (size_t)p->plane_b * 2 * L);
+  p->off_pb2 = off;    off = align256(off + (size_t)p->plane_b * 2 * L);
+  p->off_r = off;      off = align256(off + (size_t)p->rset * 4);
+  p->total = off;
+  return OZFP4_OK;
+}
+
+// Stages: 0 scale, 1 encode A (both terms), 2 encode B (both terms), 3 the
+// four residue GEMMs, 4 the combined CRT.
+int run_split(const SplitPlan& p, DeviceState* d, const double* A, int64_t lda, const double* B,
+              int64_t ldb, double* C, int64_t ldc) {
+  const HostTables* T = tables();
+  uint8_t* ws = d->ws;
+  uint64_t* amax_a = reinterpret_cast<uint64_t*>(ws + p.off_amax_a);
+  uint64_t* amax_b = reinterpret_cast<uint64_t*>(ws + p.off_amax_b);
+  int* flag = reinterpret_cast<int*>(ws + p.off_flag);
+  const int L = p.L;
+  record(d, 0);
+  const int64_t nzero = (int64_t)((p.off_flag + 256 - p.off_amax_a) / sizeof(uint64_t));
+  hipLaunchKernelGGL(k_fill_u64, dim3(blocks_for(nzero, 256)), dim3(256), 0, g_stream, amax_a,
+                     nzero, (uint64_t)0);
+  launch_amax_f64(A, lda, B, ldb, p.m, p.n, p.k, amax_a, amax_b, flag);
+  HIP_TRY(hipGetLastError());
+  record(d, 1);
+  const int lut_entries = T->mod.lut_off[L - 1] + 3 * T->mod.m[L - 1];
+  const size_t lut_bytes = sizeof(uint16_t) * (size_t)lut_entries;
+  const int64_t nfa = (p.m_pad / kFragLines) * p.kblocks;
+  const int64_t nfb = (p.n_pad / kFragLines) * p.kblocks;
+  for (int term = 0; term < 2; ++term)
+    HIP_TRY(launch_encode_split(term == 1, false, (unsigned)encode_grid(nfa), lut_bytes, g_stream, A,
+                                (int64_t)1, lda, p.m, p.k, amax_a, p.cA,
+                                ws + (term ? p.off_pa2 : p.off_pa1), p.plane_a, nfa, p.kblocks, L,
+                                d->d_mod, d->d_lut, lut_entries, p.d));
+  record(d, 2);
+  for (int term = 0; term < 2; ++term)
+    HIP_TRY(launch_encode_split(term == 1, false, (unsigned)encode_grid(nfb), lut_bytes, g_stream, B,
+                                ldb, (int64_t)1, p.n, p.k, amax_b, p.cB,
+                                ws + (term ? p.off_pb2 : p.off_pb1), p.plane_b, nfb, p.kblocks, L,
+                                d->d_mod, d->d_lut, lut_entries, p.d));
+  record(d, 3);
+  // residue sets: A1 B1, A1 B2, A2 B1, A2 B2
+  const int64_t tiles_m = p.m_pad / kTileM, tiles_n = p.n_pad / kTileN;
+  const int64_t nblocks = tiles_m * tiles_n * L;
+  const size_t pa[4] = {p.off_pa1, p.off_pa1, p.off_pa2, p.off_pa2};
+  const size_t pb[4] = {p.off_pb1, p.off_pb2, p.off_pb1, p.off_pb2};
+  for (int q = 0; q < 4; ++q)
+    hipLaunchKernelGGL(k_gemm_res, dim3((unsigned)nblocks), dim3(kWaves * 64), 0, g_stream,
+                       ws + pa[q], ws + pb[q], ws + p.off_r + (size_t)q * p.rset, p.plane_a,
+                       p.plane_b, p.kblocks, tiles_m, tiles_n, nblocks, p.m_pad,
+                       p.m_pad * p.n_pad, d->d_mod);
+  HIP_TRY(hipGetLastError());
+  record(d, 4);
+  const uint8_t* R = ws + p.off_r;
+  HIP_TRY(launch_crt_split(g_stream, crt_chunks(L), R, R + p.rset, R + 2 * p.rset, R + 3 * p.rset,
+                           p.m_pad, p.m_pad * p.n_pad, p.m, p.n, amax_a, amax_b, p.cA, p.cB, p.d,
+                           d->d_mod, d->d_crt + L, C, ldc));
+  record(d, 5);
+  return OZFP4_OK;
+}
+
 int prepare(int64_t m, int64_t n, int64_t k, int L, DgemmPlan* p, DeviceState** d,
             bool f32 = false) {
   int rc = make_dgemm_plan(m, n, k, L, p, f32);
@@ -569,6 +660,34 @@ int ozfp4_dgemm_noalloc(int64_t m, int64_t n, int64_t k, const double* A, int64_
   rc = run_dgemm(p, d, A, lda, B, ldb, C, ldc, 4, nullptr, nullptr, d->scratch);
   if (rc) return rc;
   return finish_with_flag(d, reinterpret_cast<int*>(d->scratch + p.off_flag), 5);
+}
+
+int ozfp4_dgemm_split(int64_t m, int64_t n, int64_t k, const double* A, int64_t lda,
+                      const double* B, int64_t ldb, double* C, int64_t ldc, int n_moduli) {
+  int rc = check_dgemm_args(m, n, k, A, lda, B, ldb, n_moduli);
+  if (rc) return rc;
+  if (ldc < std::max<int64_t>(1, m)) return OZFP4_EINVAL;
+  if (m == 0 || n == 0) return OZFP4_OK;
+  if (!C) return OZFP4_EINVAL;
+  DeviceState* d;
+  if (k == 0) {
+    rc = device_state(&d);
+    if (rc) return rc;
+    hipLaunchKernelGGL(k_fill_f64_matrix, dim3(stride_blocks(m * n, 256)), dim3(256), 0, g_stream, C,
+                       m, n, ldc);
+    HIP_TRY(hipGetLastError());
+    return OZFP4_OK;
+  }
+  SplitPlan p;
+  rc = make_split_plan(m, n, k, n_moduli, &p);
+  if (rc) return rc;
+  rc = device_state(&d);
+  if (rc) return rc;
+  rc = ensure_workspace(d, p.total);
+  if (rc) return rc;
+  rc = run_split(p, d, A, lda, B, ldb, C, ldc);
+  if (rc) return rc;
+  return finish_with_flag(d, reinterpret_cast<int*>(d->ws + p.off_flag), 5);
 }
 
 int ozfp4_igemm_s8(int64_t m, int64_t n, int64_t k, const int8_t* A, int64_t lda, const int8_t* B,

@@ -160,7 +160,7 @@ hipError_t launch_encode_f32(unsigned grid, size_t lds_bytes, hipStream_t stream
                              const void* lut, int lut_entries) {
   hipLaunchKernelGGL((k_encode_dgemm<false, false, float>), dim3(grid), dim3(256), lds_bytes,
                      stream, X, rs, ks, lines, k, amax, cap, planes, plane_bytes, nfrag, kblocks, L,
-                     mc, lut, lut_entries);
+                     mc, lut, lut_entries, 0);
   return hipGetLastError();
 }
 

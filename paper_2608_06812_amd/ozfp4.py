@@ -44,6 +44,7 @@ _SIGNATURES = {
     "ozfp4_dgemm": (_int, [_i64, _i64, _i64, _p, _i64, _p, _i64, _p, _i64, _int]),
     "ozfp4_igemm_s8": (_int, [_i64, _i64, _i64, _p, _i64, _p, _i64, _p, _i64]),
     "ozfp4_init": (_int, []),
+    "ozfp4_dgemm_split": (_int, [_i64, _i64, _i64, _p, _i64, _p, _i64, _p, _i64, _int]),
     "ozfp4_dgemm_noalloc": (_int, [_i64, _i64, _i64, _p, _i64, _p, _i64, _p, _i64, _int]),
     "ozfp4_set_stream": (_int, [_p]),
     "ozfp4_finalize": (_int, []),
@@ -98,6 +99,10 @@ def load() -> ctypes.CDLL:
 
 def ozfp4_dgemm(m, n, k, A, lda, B, ldb, C, ldc, n_moduli) -> int:
     return load().ozfp4_dgemm(m, n, k, A, lda, B, ldb, C, ldc, n_moduli)
+
+
+def ozfp4_dgemm_split(m, n, k, A, lda, B, ldb, C, ldc, n_moduli) -> int:
+    return load().ozfp4_dgemm_split(m, n, k, A, lda, B, ldb, C, ldc, n_moduli)
 
 
 def ozfp4_init() -> int:
@@ -299,6 +304,27 @@ def dgemm(A, B, n_moduli: int = 19, out=None):
     with _on(A.device, B, C):
         _check(ozfp4_dgemm(m, n, k, A.data_ptr(), lda, B.data_ptr(), ldb, C.data_ptr(), ldc, n_moduli),
                "ozfp4_dgemm")
+    return C
+
+
+def dgemm_split(A, B, n_moduli: int = 19, out=None):
+    """C = fl(A B) for float64 device tensors by scheme II with the two-term
+    split of the converted operands (ozfp4_dgemm_split); returns C (m x n),
+    column-major."""
+    import torch
+    A, lda = _cm(A, torch.float64, "A")
+    B, ldb = _cm(B, torch.float64, "B")
+    m, k = A.shape
+    k2, n = B.shape
+    if k != k2:
+        raise ValueError("inner dimensions differ")
+    C = _empty_cm(m, n, torch.float64, A.device) if out is None else out
+    if C.shape != (m, n) or C.dtype != torch.float64 or (C.stride(0) != 1 and m > 1):
+        raise ValueError("out must be a column-major float64 (m x n) tensor")
+    ldc = max(1, C.stride(1) if n > 1 else m)
+    with _on(A.device, B, C):
+        _check(ozfp4_dgemm_split(m, n, k, A.data_ptr(), lda, B.data_ptr(), ldb, C.data_ptr(), ldc,
+                                 n_moduli), "ozfp4_dgemm_split")
     return C
 
 

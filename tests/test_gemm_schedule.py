@@ -37,7 +37,8 @@ def asm(tmp_path_factory):
         pytest.skip("no hipcc")
     out = {}
     d = tmp_path_factory.mktemp("asm")
-    for tu in ("ozfp4.hip", "karatsuba.hip", "ozaki1.hip", "sgemm.hip"):
+    for tu in ("ozfp4.hip", "karatsuba.hip", "ozaki1.hip", "sgemm.hip", "split.hip",
+               "calibrate.hip"):
         path = str(d / (tu + ".s"))
         subprocess.run([hipcc, *FLAGS, os.path.join(CSRC, tu), "-o", path], check=True,
                        capture_output=True)
@@ -132,5 +133,5 @@ def test_no_scaled_mfma_anywhere(asm):
     for tu, text in asm.items():
         body = [x.strip() for x in text.split("\n") if x.startswith("\t")]
         assert _count(body, r"^v_mfma_scale|^v_mfma_ld_scale") == 0, tu
-        if tu != "sgemm.hip":   # the FP32 emulation reuses the default GEMM
+        if tu not in ("sgemm.hip", "split.hip"):   # these reuse the default GEMM
             assert _count(body, r"^v_mfma_f32_32x32x64_f8f6f4 ") > 0, tu

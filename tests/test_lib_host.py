@@ -167,9 +167,12 @@ def test_strerror(lib):
 ])
 def test_dgemm_argument_errors_on_host(lib, args, code):
     assert ozfp4.ozfp4_dgemm(*args) == code
+    # the two-term split route checks its arguments the same way
+    assert ozfp4.ozfp4_dgemm_split(*args) == code
 
 
 def test_dgemm_empty_is_noop(lib):
+    assert ozfp4.ozfp4_dgemm_split(0, 5, 5, 0, 1, 0, 5, 0, 1, 19) == ozfp4.OZFP4_OK
     assert ozfp4.ozfp4_dgemm(0, 5, 5, 0, 1, 0, 5, 0, 1, 19) == ozfp4.OZFP4_OK
     assert ozfp4.ozfp4_dgemm(5, 0, 5, 0, 5, 0, 5, 0, 5, 19) == ozfp4.OZFP4_OK
 
