@@ -55,10 +55,13 @@ CPU_SHARE = 16                  # host cores that go with one GPU
 # FETCH_SIZE). Valid only for the GEMM source they were taken on, identified
 # by the hash of its code. None: not yet taken on the current source.
 MEASURED_TRAFFIC = {
-    "kernel_source_sha256_16": None,
+    "kernel_source_sha256_16": "9bebb506c97596dd",
     "workload": (16384, 16384, 16384, 18),
-    "fetch_kib": None, "write_kib": None,
-    "fetch_factor": None, "write_factor": None,
+    # means over the four dispatches of one run
+    "fetch_kib": 75_497_685, "write_kib": 4_747_422,
+    # 1 GiB read through the LDS-DMA path: 524,304 KiB; plain 1 GiB copy:
+    # 524,300 KiB read, 1,048,576 KiB written
+    "fetch_factor": 2.0, "write_factor": 1.0,
     "profile": "profiles/k_gemm_res_dgemm_16384_L18.md",
 }
 SEED = 20260806
@@ -372,7 +375,7 @@ def block_of(C, rows, cols, torch):
     return C[r][:, c].cpu().numpy()
 
 
-def measure_attainable(ozfp4, torch, target_ms=60.0, reps=3):
+def measure_attainable(ozfp4, torch, target_ms=80.0, reps=3):
     """The register-only FP4 MFMA loop (one block of eight waves per CU, the
     residue GEMM's register tile and product order, operands changed every
     k fragment) sustained over about target_ms per launch: the matrix-core

@@ -359,7 +359,7 @@ int run_dgemm(const DgemmPlan& p, DeviceState* d, const void* Av, int64_t lda, c
   if (last < 4) return OZFP4_OK;
 
   // stage 4: CRT reconstruction and inverse scaling
-  const int64_t nthreads = ((p.m + 3) / 4) * p.n;
+  const int64_t nthreads = ((p.m + kCrtRows - 1) / kCrtRows) * p.n;
   if (p.f32) {
     HIP_TRY(launch_crt_f32(g_stream, crt_chunks(L), R, p.m_pad, p.m_pad * p.n_pad, p.m, p.n,
                            amax_a, amax_b, p.cA, p.cB, d->d_crt + L, static_cast<float*>(Cv),

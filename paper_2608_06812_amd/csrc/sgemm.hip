@@ -69,7 +69,9 @@ __global__ __launch_bounds__(256) void k_amax_contig_lines_f32(
 }
 
 // CRT of the FP32 emulation (Sec. V-B): the FP64 path's chunk sums and
-// quotient, then the exact symmetric integer and one rounding to binary32.
+// quotient, then one rounding to binary32: with three chunks through
+// crt_fast3_f32 (round to odd at 53 bits in FP64, then one conversion),
+// else, or where that path gives up, from the exact symmetric integer.
 // One thread per 4 consecutive rows of a column.
 template <int NC>
 __global__ __launch_bounds__(256) void k_crt_f32(
@@ -117,8 +119,12 @@ __global__ __launch_bounds__(256) void k_crt_f32(
 #pragma unroll
       for (int c = NC - 2; c >= 0; --c) Qe = __builtin_fma(sig[e][c], cc->Qc[c], Qe);
       const double q = __builtin_rint(Qe);
-      outv[e] =
-          crt_exact_f32(sig[e][0], sig[e][1], sig[e][2], NC == 4 ? sig[e][NC - 1] : 0.0, q, cc, e2);
+      float out;
+      bool done = false;
+      if constexpr (NC == 3) done = crt_fast3_f32(sig[e][0], sig[e][1], sig[e][2], q, cc, e2, &out);
+      if (!done)
+        out = crt_exact_f32(sig[e][0], sig[e][1], sig[e][2], NC == 4 ? sig[e][NC - 1] : 0.0, q, cc, e2);
+      outv[e] = out;
     }
   }
   // one 16-byte store for the four rows where the column is aligned

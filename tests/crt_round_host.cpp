@@ -39,8 +39,12 @@ int main() {
     const double ex = crt_exact(sig[0], sig[1], sig[2], NC == 4 ? sig[3] : 0.0, q, cc, e2);
     if (!fast) out = ex;
     const float f = crt_exact_f32(sig[0], sig[1], sig[2], NC == 4 ? sig[3] : 0.0, q, cc, e2);
-    std::printf("%016llx %016llx %d %08x\n", (unsigned long long)bits_of(out),
-                (unsigned long long)bits_of(ex), fast ? 1 : 0, __builtin_bit_cast(uint32_t, f));
+    float ff = f;
+    bool fast32 = false;
+    if (NC == 3) fast32 = crt_fast3_f32(sig[0], sig[1], sig[2], q, cc, e2, &ff);
+    std::printf("%016llx %016llx %d %08x %08x %d\n", (unsigned long long)bits_of(out),
+                (unsigned long long)bits_of(ex), fast ? 1 : 0, __builtin_bit_cast(uint32_t, f),
+                __builtin_bit_cast(uint32_t, ff), fast32 ? 1 : 0);
   }
   return 0;
 }

@@ -87,16 +87,20 @@ def test_crt_round_matches_exact_rational(crt_bin, L):
     text = "".join(f"{L} {e2} " + " ".join(map(str, r)) + "\n" for _, e2, r in cases)
     res = subprocess.run([crt_bin], input=text, capture_output=True, text=True, check=True)
     lines = res.stdout.split("\n")
-    fast_count = 0
+    fast_count = fast32_count = 0
     for (x, e2, r), line in zip(cases, lines):
-        got, exact, fast, f32 = line.split()
+        got, exact, fast, f32, f32fast, fast32 = line.split()
         want = struct.unpack("<Q", struct.pack("<d", o.round_scaled(x, -e2)))[0]
         assert int(exact, 16) == want, (L, x, e2, "exact path")
         assert int(got, 16) == want, (L, x, e2, "fast path" if fast == "1" else "exact path")
-        assert int(f32, 16) == int(o.round_scaled_f32(x, -e2).view("uint32")), (L, x, e2, "binary32")
+        want32 = int(o.round_scaled_f32(x, -e2).view("uint32"))
+        assert int(f32, 16) == want32, (L, x, e2, "binary32")
+        if fast32 == "1":
+            assert int(f32fast, 16) == want32, (L, x, e2, "binary32 fast path")
         fast_count += int(fast)
+        fast32_count += int(fast32)
     assert len(lines) >= len(cases)
-    if L <= 19:   # three chunks: most elements take the fast path
-        assert fast_count > 0.8 * len(cases)
+    if L <= 19:   # three chunks: most elements take the fast paths
+        assert fast_count > 0.8 * len(cases) and fast32_count > 0.8 * len(cases)
     else:
-        assert fast_count == 0
+        assert fast_count == 0 and fast32_count == 0
