@@ -2,8 +2,8 @@
 generator draws m, n, k (from 1 to 300, most of them ragged
 against every tile), the number of moduli, the exponent spread phi of the
 inputs, the capacity cap and the residue-GEMM route, and the library's C is
-compared bit for bit with the oracle's. Scheme I, the FP32 emulation and
-INT8 get their own draws. Each case prints its parameters before it runs,
+compared bit for bit with the oracle's. Scheme I, the FP32 emulation, INT8
+and the two-term split route get their own draws. Each case prints its parameters before it runs,
 so a failure names them."""
 
 import numpy as np
@@ -12,12 +12,13 @@ import pytest
 import oracle as o
 from gpu_util import announce, bits_equal, dev_cm, to_np
 from oracle.sgemm_fp4 import capacity_bits_fp32, sgemm as oracle_sgemm
+from oracle.split2_fp4 import dgemm_split2 as oracle_split2
 from paper_2608_06812_amd.workloads import dgemm_inputs, int8_inputs
 
 pytestmark = pytest.mark.gpu
 
 SEED = 20261204
-N_DGEMM, N_SGEMM, N_OZI, N_INT8 = 40, 16, 16, 16
+N_DGEMM, N_SGEMM, N_OZI, N_INT8, N_SPLIT = 40, 16, 16, 16, 16
 
 
 def _dim(rng):
@@ -126,3 +127,26 @@ def test_random_igemm_s8(gpu_lib, case):
     Bd = torch.from_numpy(np.ascontiguousarray(B.T)).cuda().t()
     C = gpu_lib.igemm_s8(Ad, Bd).cpu().numpy()
     assert np.array_equal(C, want)
+
+
+@pytest.mark.parametrize("case", range(N_SPLIT))
+def test_random_split(gpu_lib, case):
+    """The two-term split route (53-bit capacities), phi up to 12 so the
+    second terms carry many bits."""
+    rng = np.random.default_rng([SEED + 4, case])
+    m, n, k = _dim(rng), _dim(rng), _dim(rng)
+
+    def cap_ok(k_, L_):
+        try:
+            o.capacity_bits(k_, o.select_moduli(L_))
+            return True
+        except ValueError:
+            return False
+    L = _moduli_for(k, rng, cap_ok)
+    phi = float(rng.choice([0.5, 4.0, 12.0]))
+    seed = int(rng.integers(1 << 30))
+    A, B = dgemm_inputs(m, n, k, phi, seed)
+    want = oracle_split2(A, B, L)["C"]
+    announce(f"random split case {case}: m={m} n={n} k={k} L={L} phi={phi} seed={seed}")
+    C = to_np(gpu_lib.dgemm_split(dev_cm(A), dev_cm(B), L))
+    assert bits_equal(C, want)
