@@ -419,18 +419,16 @@ def measure_plain_gemm(ozfp4, torch, N=16384, target_ms=100.0):
             "kernel": "k_calib_gemm_fp4 (ozfp4_calib_gemm_fp4)"}
 
 
-def measure_copy_beta(torch, reps=5):
+def measure_copy_beta(torch, reps=21):
     """beta of the runtime model: a plain 1 GiB device copy, read plus
-    written bytes over its time (the paper's copy benchmark)."""
+    written bytes over its time (the paper's copy benchmark), the median
+    of `reps` copies each timed alone with HIP events."""
     src = torch.empty(1 << 27, dtype=torch.float64, device="cuda").fill_(1.0)
     dst = torch.empty_like(src)
-    dst.copy_(src)
-
-    def run():
-        for _ in range(reps):
-            dst.copy_(src)
-    t = event_ms(torch, run)
-    beta = 2.0 * src.numel() * 8 * reps / (t * 1e-3) / 1e9
+    for _ in range(3):
+        dst.copy_(src)
+    ms = stats([event_ms(torch, lambda: dst.copy_(src)) for _ in range(reps)])["median"]
+    beta = 2.0 * src.numel() * 8 / (ms * 1e-3) / 1e9
     del src, dst
     return beta
 
