@@ -1,6 +1,7 @@
 """CPU oracle for FP64 matrix multiplication through Ozaki schemes II and I on
 base-13 E2M1 limbs (scheme II also with a two-term split of the converted
-operands), and for FP32 matrix multiplication through scheme II.
+operands, and with the one-limb modulus 11 in the moduli list), and for FP32
+matrix multiplication through scheme II.
 
 TEST INFRASTRUCTURE ONLY. Nothing in the product path may import, call or
 execute this package: only ``tests/``, ``__graft_entry__.smoke()`` and the
@@ -21,5 +22,7 @@ from .sgemm_fp4 import *  # noqa: F401,F403
 from .sgemm_fp4 import __all__ as _all32
 from .split2_fp4 import *  # noqa: F401,F403
 from .split2_fp4 import __all__ as _alls
+from .one_limb_fp4 import *  # noqa: F401,F403
+from .one_limb_fp4 import __all__ as _all1l
 
-__all__ = list(_all2) + list(_all1) + list(_all32) + list(_alls)
+__all__ = list(_all2) + list(_all1) + list(_all32) + list(_alls) + list(_all1l)

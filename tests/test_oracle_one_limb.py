@@ -1,0 +1,189 @@
+"""Pins of the one-limb-modulus oracle (oracle/one_limb_fp4.py): each check
+ties it to something other than itself.
+
+* Which moduli are one-limb, by brute force over every class; that each is
+  also a two-limb modulus (c1 = 0); that 11 is the only one coprime to the
+  greedy list's first 26 moduli, and the greedy rule's own 27th pick.
+* The one-limb representative of every residue of 11, written out by hand
+  from S = {0, +-1, +-2, +-3, +-4, +-6, +-8, +-12}; its E2M1 round trip.
+* FP32 exactness of the single limb product at the largest k (bound and an
+  adversarial emulated accumulation).
+* P and the capacities of the one-limb list against the printed moduli.
+* Brute force on tiny matrices: the residue route equals the exact product of
+  the converted operands, and C its one rounding; every residue equals the
+  exact integer product mod m.
+* Integer inputs small enough for every capacity give fl(AB) = the exact
+  product, by both lists.
+* Planted mistakes (the two-limb route's c0 used as the one limb, a
+  composition weight on the one-limb product, the modulus dropped from the
+  list) are each caught."""
+
+import json
+import math
+import os
+from fractions import Fraction
+
+import numpy as np
+import pytest
+
+import oracle as o
+import oracle.one_limb_fp4 as ol
+
+GOLDEN = os.path.join(os.path.dirname(__file__), "golden", "paper_values.json")
+
+
+def _printed_moduli():
+    with open(GOLDEN) as f:
+        return json.load(f)["moduli_L19"]["value"]
+
+
+def test_one_limb_moduli_by_brute_force():
+    S = [0, 1, -1, 2, -2, 3, -3, 4, -4, 6, -6, 8, -8, 12, -12]
+    want = [m for m in range(2, 200) if all(any((c - r) % m == 0 for c in S) for r in range(m))]
+    assert want == [2, 3, 4, 5, 6, 7, 8, 9, 11, 13]
+    assert o.one_limb_moduli(199) == want
+    assert all(o.is_two_limb_modulus(m) for m in want)
+
+
+def test_eleven_is_the_only_coprime_one_limb_modulus():
+    greedy26 = o.select_moduli(26)
+    assert greedy26[:19] == _printed_moduli()
+    free = [m for m in o.one_limb_moduli() if all(math.gcd(m, q) == 1 for q in greedy26)]
+    assert free == [11]
+    assert o.select_moduli(27)[-1] == 11 and 11 not in greedy26
+
+
+def test_one_limb_list():
+    printed = _printed_moduli()
+    assert o.select_moduli_one_limb(18) == [11] + printed[:17]
+    assert o.select_moduli_one_limb(2) == [11, 169]
+    lst = o.select_moduli_one_limb(27)
+    assert len(set(lst)) == 27
+    assert all(math.gcd(a, b) == 1 for i, a in enumerate(lst) for b in lst[i + 1:])
+    for bad in (1, 28):
+        with pytest.raises(ValueError):
+            o.select_moduli_one_limb(bad)
+
+
+def test_one_limb_representatives_of_eleven():
+    # 0..4 are in S; 5 = -6 + 11; 6 is in S; 7 = -4 + 11; 8 = -3 + 11 (|-3| < 8);
+    # 9 = -2 + 11; 10 = -1 + 11
+    assert o.one_limb_table(11) == [0, 1, 2, 3, 4, -6, 6, -4, -3, -2, -1]
+    for r, c in enumerate(o.one_limb_table(11)):
+        assert (c - r) % 11 == 0
+        assert int(2 * o.e2m1_decode(o.e2m1_code(c))) == c
+        assert abs(c) <= 6
+    for m in o.one_limb_moduli():
+        for r in range(m):
+            c = o.one_limb_split(r, m)
+            assert (c - r) % m == 0 and c in o.doubled_set()
+
+
+def test_one_limb_product_exact_in_fp32():
+    K = o.MAX_K_FP32
+    assert o.fp32_exact_bound(K, max_limb=6, terms=1)
+    a = np.full(K, 6)
+    b = np.full(K, 6)
+    assert o.fp32_accumulate_emulated(a, b) == 36 * K
+    a[::2] = -6
+    assert o.fp32_accumulate_emulated(a, b) == 0
+    assert 36 * K < 2 ** 31          # 4 acc converts to int32 exactly
+
+
+def test_product_and_capacities():
+    printed = _printed_moduli()
+    P17 = math.prod(printed[:17])
+    assert o.moduli_product(o.select_moduli_one_limb(18)) == 11 * P17
+    # b is the largest integer with 2 k 2^b < P: log2(11 P17) = 115.07
+    assert math.isclose(math.log2(11 * P17), 115.073, abs_tol=1e-3)
+    assert o.capacity_bits(16384, o.select_moduli_one_limb(18)) == (50, 50)
+    assert o.capacity_bits(4096, o.select_moduli_one_limb(18)) == (51, 51)
+    assert o.capacity_bits(16384, o.select_moduli_one_limb(19)) == (53, 52)
+
+
+def _tiny(seed, m, n, k, spread=30):
+    rng = np.random.default_rng(seed)
+    A = (rng.random((m, k)) - 0.5) * np.exp2(rng.integers(-spread, spread, (m, k)))
+    B = (rng.random((k, n)) - 0.5) * np.exp2(rng.integers(-spread, spread, (k, n)))
+    return A, B
+
+
+@pytest.mark.parametrize("L", [3, 8, 14, 18, 19, 20])
+def test_brute_force_tiny(L):
+    for seed in range(3):
+        A, B = _tiny(100 * L + seed, 3, 4, 6)
+        A[1, :] = 0.0
+        out = o.dgemm_one_limb(A, B, L, check_definition=True)
+        assert out["moduli"][0] == 11
+        assert np.array_equal(out["C"], o.dgemm_one_limb_definition(A, B, L))
+        exact = o.exact_int_matmul(out["Ai"], out["Bi"])
+        for q, r in zip(out["moduli"], out["r"]):
+            assert np.array_equal(np.asarray(r, dtype=object), np.mod(exact, q))
+        # C is RN of the exact product of the converted operands, scaled
+        for i in range(3):
+            for j in range(4):
+                x = Fraction(int(exact[i, j])) / Fraction(2) ** (int(out["s"][i]) + int(out["t"][j]))
+                assert out["C"][i, j] == float(x)
+
+
+def test_block_restriction_matches_whole():
+    A, B = _tiny(7, 9, 8, 40)
+    full = o.dgemm_one_limb(A, B, 16)["C"]
+    blk = o.dgemm_one_limb(A, B, 16, rows=[1, 4, 8], cols=[0, 7])["C"]
+    assert np.array_equal(blk, full[np.ix_([1, 4, 8], [0, 7])])
+
+
+def test_small_integers_give_the_exact_product_by_both_lists():
+    rng = np.random.default_rng(5)
+    A = rng.integers(-(1 << 20), 1 << 20, (6, 50)).astype(np.float64)
+    B = rng.integers(-(1 << 20), 1 << 20, (50, 5)).astype(np.float64)
+    exact = A.astype(object) @ B.astype(object)
+    want = np.array([[float(v) for v in row] for row in exact])
+    assert np.array_equal(o.dgemm_one_limb(A, B, 18)["C"], want)
+    assert np.array_equal(o.dgemm(A, B, 18)["C"], want)
+
+
+def _mismatch(L=14):
+    for seed in range(4):
+        A, B = _tiny(900 + seed, 3, 4, 5)
+        try:
+            got = o.dgemm_one_limb(A, B, L)["C"]
+        except (AssertionError, ValueError):
+            return True
+        if not np.array_equal(got, o.dgemm_one_limb_definition(A, B, L)):
+            return True
+    return False
+
+
+def test_unmutated_passes():
+    assert not _mismatch()
+
+
+def test_two_limb_low_limb_as_the_one_limb_is_caught(monkeypatch):
+    # the canonical two-limb split of r' = +-5 mod 11 is (-+8, +-1): its low
+    # limb alone is not congruent to r
+    monkeypatch.setattr(ol, "one_limb_table", lambda m: [o.two_limb_split(r, m)[0] for r in range(m)])
+    assert _mismatch()
+
+
+def test_composition_weight_on_the_one_limb_product_is_caught(monkeypatch):
+    orig = ol.residue_products_one_limb
+
+    def bad(Ai, Bi, m):
+        out = orig(Ai, Bi, m)
+        out["r"] = np.mod(4 * out["G0"], m)
+        return out
+    monkeypatch.setattr(ol, "residue_products_one_limb", bad)
+    assert _mismatch()
+
+
+def _list_pins_fail():
+    lst = ol.select_moduli_one_limb(18)
+    return lst != [11] + _printed_moduli()[:17] or o.capacity_bits(16384, lst) != (50, 50)
+
+
+def test_dropping_the_modulus_is_caught(monkeypatch):
+    assert not _list_pins_fail()
+    orig = ol.select_moduli_one_limb
+    monkeypatch.setattr(ol, "select_moduli_one_limb", lambda L: orig(L)[1:] + [o.select_moduli(L)[-1]])
+    assert _list_pins_fail()
