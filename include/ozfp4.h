@@ -198,6 +198,28 @@ int ozfp4_set_karatsuba(int enable);
  */
 int ozfp4_set_max_capacity(int bits);
 
+/*
+ * ozfp4_set_one_limb_modulus -- the moduli list of subsequent FP64 scheme-II
+ * calls (ozfp4_dgemm, ozfp4_dgemm_noalloc and the hooks ozfp4_scales,
+ * ozfp4_limb_planes, ozfp4_residues), default 0. An extension of the moduli
+ * choice of Sec. V-A: 11 is a one-limb modulus (every class mod 11 holds an
+ * element of S: 0, +-1, +-2, +-3, +-4, and 5 = -6, 6 = 6 mod 11), so its
+ * residues need one limb (c1 = 0) and its residue product is the single
+ * limb product a0 b0 (mod 11), one FP4 product instead of four. With 1,
+ * n_moduli = L selects 11 followed by the first L - 1 moduli of the greedy
+ * list (11 is the only one-limb modulus coprime to all of them); P, the
+ * capacities and hence C follow from that list by the same rules (at
+ * k = 16384 and L = 18: P = 2^115.07, c_A = c_B = 50, against 51 with the
+ * greedy 18). Modulus index 0 of the planes and residues is 11 (its second
+ * limb plane is all zero); the others are the greedy list's. The Karatsuba
+ * mode cannot be combined with it: those calls return OZFP4_EINVAL.
+ * ozfp4_sgemm, ozfp4_dgemm_split and ozfp4_dgemm_ozi keep their own
+ * moduli. The host queries (ozfp4_moduli, ozfp4_capacity,
+ * ozfp4_two_limb_table, ozfp4_plane_count) follow the setting. A
+ * process-wide setting, like the stream.
+ */
+int ozfp4_set_one_limb_modulus(int enable);
+
 /* Releases every device workspace and table of the library, after waiting
  * for each device's work. A later call sets them up again. */
 int ozfp4_finalize(void);
@@ -207,18 +229,22 @@ const char* ozfp4_strerror(int code);
 
 /* ---- host-only queries (no GPU work; usable without a device) ---------- */
 
-/* Writes the first n_moduli moduli (Sec. V-A greedy order) to the HOST array
+/* Writes the first n_moduli moduli (Sec. V-A greedy order; with the one-limb
+ * setting 11 first, see ozfp4_set_one_limb_modulus) to the HOST array
  * out[n_moduli]; n_moduli in 1..OZFP4_MAX_MODULI, else OZFP4_EINVAL. */
 int ozfp4_moduli(int n_moduli, int32_t* out);
 
-/* Capacities (c_A, c_B) used for inner dimension k with n_moduli moduli
- * and the current capacity cap (see ozfp4_dgemm). HOST pointers.
+/* Capacities (c_A, c_B) used for inner dimension k with n_moduli moduli,
+ * the current capacity cap and moduli list (see ozfp4_dgemm and
+ * ozfp4_set_one_limb_modulus). HOST pointers.
  * OZFP4_EINVAL for k < 1 or a null pointer, OZFP4_EMODULI when n_moduli is
  * outside 2..27 or the moduli cannot hold k. */
 int ozfp4_capacity(int64_t k, int n_moduli, int32_t* c_a, int32_t* c_b);
 
 /* Canonical two-limb split of every residue r in [0, m_l) of modulus l
- * (index in the greedy list): HOST array out[m_l] of bytes, E2M1 code of
+ * (index in the current moduli list; for the one-limb modulus 11 the
+ * element of S congruent to r of smallest magnitude, c1 = 0): HOST array
+ * out[m_l] of bytes, E2M1 code of
  * c0 in the low nibble and of c1 in the high nibble, where
  * c0 + 13 c1 = r (mod m_l). The split takes the representative r' of r in
  * (-m/2, m/2], splits it greedily (smallest-magnitude digit mod 13, +-5
@@ -244,7 +270,8 @@ int ozfp4_sum_limb_table(int modulus_index, uint8_t* out, int32_t* m_out);
  * (c0 + c1) per Karatsuba modulus among them. HOST outputs: *n_planes, and
  * when sum_plane is not NULL the index of the sum plane of each modulus in
  * sum_plane[n_moduli] (-1 for none). OZFP4_EMODULI for n_moduli outside
- * 2..27, OZFP4_EINVAL for a null n_planes. */
+ * 2..27, OZFP4_EINVAL for a null n_planes or with both the Karatsuba and the
+ * one-limb setting on. */
 int ozfp4_plane_count(int n_moduli, int32_t* n_planes, int32_t* sum_plane);
 
 /* Layout of the packed FP4 limb planes (the debug hook below returns them):

@@ -12,17 +12,18 @@ import sys
 HERE = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(HERE)
 LIB = os.path.join(HERE, "libozfp4.so")
-# six translation units: the API with the default kernels, the Karatsuba
+# seven translation units: the API with the default kernels, the Karatsuba
 # mode's kernels, the scheme-I kernels, the FP32-emulation kernels, the
-# two-term split's kernels and the reference-measurement kernels (kept apart
-# so they cannot change the default kernels' code)
+# two-term split's kernels, the one-limb modulus's GEMM and the
+# reference-measurement kernels (kept apart so they cannot change the
+# default kernels' code)
 SOURCES = [os.path.join(HERE, "csrc", n)
            for n in ("ozfp4.hip", "karatsuba.hip", "ozaki1.hip", "sgemm.hip", "split.hip",
-                     "calibrate.hip")]
+                     "onelimb.hip", "calibrate.hip")]
 HEADERS = [os.path.join(HERE, "csrc", n) for n in
            ("device_common.hpp", "kernels.hpp", "karatsuba.hpp", "crt_round.hpp", "tables.hpp",
             "ozaki1.hpp", "ozi_round.hpp", "sgemm.hpp", "crt_round_f32.hpp",
-            "calibrate.hpp", "split.hpp", "crt_split.hpp")] + \
+            "calibrate.hpp", "split.hpp", "crt_split.hpp", "onelimb.hpp", "plain_gemm.hpp")] + \
           [os.path.join(ROOT, "include", "ozfp4.h")]
 
 # -packed-fp32-ops: keep the compiler from emitting packed FP32 arithmetic.

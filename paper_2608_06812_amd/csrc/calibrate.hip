@@ -13,6 +13,7 @@
 // compiler schedules the default kernels.
 #include "calibrate.hpp"
 #include "device_common.hpp"
+#include "plain_gemm.hpp"
 
 namespace ozfp4 {
 
@@ -103,116 +104,21 @@ __global__ __launch_bounds__(512, 1) void k_calib_mfma(int64_t iters, uint32_t s
 }
 
 // ------------------------------------------------------------ plain FP4 GEMM
-// C (FP32, column-major, ldc) = A B for one FP4 plane of A (m lines) and one
-// of B (n lines), both in the fragment layout of the limb planes with k
-// fragments per 32-line block. m, n multiples of 256, k a multiple of 128,
-// at least 384. The products are multiples of 1/4 of magnitude <= 36, so C
-// is exact for k <= 2^16 (sums below 2^22).
-//
-// Block tile 256 x 256, eight waves (two per SIMD) of 64 x 128 (2 x 4 MFMA
-// tiles, 128 accumulator registers). A k = 128 stage is 32 fragments (A: 8
-// line blocks x 2 k fragments, then B the same), 32 KiB, streamed into a
-// 3-slot LDS ring by the residue GEMM's buffer-form DMA, two stages ahead,
-// 4 copies per wave in pairs between the MFMAs; the stage handover (wait
-// for the next stage, barrier) sits before the stage's last four MFMAs.
-constexpr int kCalTile = 256;
-constexpr int kCalStageFrags = 32;
-constexpr int kCalStageBytes = kCalStageFrags * kFragBytes;
-constexpr int kCalDma = kCalStageFrags / kWaves;   // 4
-
-__device__ __forceinline__ constexpr int calA(int rb, int kbl) { return (rb * 2 + kbl) * kFragBytes; }
-__device__ __forceinline__ constexpr int calB(int cb, int kbl) { return (16 + cb * 2 + kbl) * kFragBytes; }
-
+// C (FP32, column-major, ldc) = A B for one FP4 plane of A and one of B
+// (plain_gemm.hpp): the main loop shared with the one-limb residue GEMM,
+// then the accumulators stored as FP32.
 __global__ __launch_bounds__(512, 1) void k_calib_gemm_fp4(
     const uint8_t* __restrict__ PA, const uint8_t* __restrict__ PB, float* __restrict__ C,
     int64_t ldc, int64_t kblocks, int64_t tiles_m, int64_t tiles_n) {
-  __shared__ __attribute__((aligned(1024))) uint8_t lds[kRing * kCalStageBytes];
+  __shared__ __attribute__((aligned(1024))) uint8_t lds[kPlainLdsBytes];
   int l;
   int64_t tm, tn;
   tile_coords(blockIdx.x, tiles_m * tiles_n, tiles_m, tiles_n, &l, &tm, &tn);
-  const int tid = threadIdx.x, lane = tid & 63;
-  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-  const int wm = wave >> 1, wn = wave & 1;
-  const int rbw = 2 * wm, cbw = 4 * wn;   // this wave's first A / B line block
-
-  const int nst = (int)(kblocks / 2);
-  __amdgpu_buffer_rsrc_t src[kCalDma];
-#pragma unroll
-  for (int j = 0; j < kCalDma; ++j) {
-    const int f = wave * kCalDma + j;
-    const int g = f & 15, kbl = g & 1, blk = g >> 1;
-    const uint8_t* base = f < 16 ? PA + ((tm * 8 + blk) * kblocks + kbl) * kFragBytes
-                                 : PB + ((tn * 8 + blk) * kblocks + kbl) * kFragBytes;
-    src[j] = __builtin_amdgcn_make_buffer_rsrc((void*)base, (short)0, nst * 2 * kFragBytes,
-                                               kBufferWord3);
-  }
-  const int lane16 = lane * 16;
-  auto dma = [&](int st, int j) {
-    dma16_buf(src[j], (uint32_t)lane16, (uint32_t)(st * 2 * kFragBytes),
-              lds + (st % kRing) * kCalStageBytes + (wave * kCalDma + j) * kFragBytes);
-  };
-
   v16f acc[2][4];
-#pragma unroll
-  for (int i = 0; i < 2; ++i)
-#pragma unroll
-    for (int j = 0; j < 4; ++j)
-#pragma unroll
-      for (int v = 0; v < 16; ++v) acc[i][j][v] = 0.0f;
-
-#pragma unroll
-  for (int j = 0; j < kCalDma; ++j) dma(0, j);
-#pragma unroll
-  for (int j = 0; j < kCalDma; ++j) dma(1, j);   // nst >= 3
-  wait_vm_lgkm0<kCalDma>();
-  block_sync();
-
-  v4i a[2], b[4];
-  auto read_frags = [&](const uint8_t* sb, int kbl) {
-#pragma unroll
-    for (int i = 0; i < 2; ++i) a[i] = *reinterpret_cast<const v4i*>(sb + calA(rbw + i, kbl) + lane16);
-#pragma unroll
-    for (int j = 0; j < 4; ++j) b[j] = *reinterpret_cast<const v4i*>(sb + calB(cbw + j, kbl) + lane16);
-  };
-  auto mfma_cols = [&](int j0, int j1) {
-#pragma unroll
-    for (int j = j0; j < j1; ++j)
-#pragma unroll
-      for (int i = 0; i < 2; ++i) acc[i][j] = mfma_fp4(a[i], b[j], acc[i][j]);
-  };
-  auto stage_body = [&](int s, bool copy) {
-    const uint8_t* sb = lds + (s % kRing) * kCalStageBytes;
-    read_frags(sb, 0);
-    mfma_cols(0, 4);
-    if (copy) {
-      dma(s + 2, 0);
-      dma(s + 2, 1);
-    }
-    __builtin_amdgcn_sched_barrier(0);
-    read_frags(sb, 1);
-    mfma_cols(0, 2);
-    if (copy) {
-      dma(s + 2, 2);
-      dma(s + 2, 3);
-    }
-    __builtin_amdgcn_sched_barrier(0);
-  };
-
-  int s = 0;
-  for (; s + 2 < nst; ++s) {
-    stage_body(s, true);
-    wait_vm_lgkm0<kCalDma>();   // stage s + 1 landed; reads of stage s done
-    block_sync();
-    mfma_cols(2, 4);
-    __builtin_amdgcn_sched_barrier(0);
-  }
-  stage_body(s, false);
-  wait_vm_lgkm0<0>();
-  block_sync();
-  mfma_cols(2, 4);
-  __builtin_amdgcn_sched_barrier(0);
-  stage_body(s + 1, false);
-  mfma_cols(2, 4);
+  plain_gemm_tile(lds, PA, PB, kblocks, tm, tn, acc);
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int wm = wave >> 1, wn = wave & 1;
 
   // MFMA output layout: lane (col % 32, 4-row group), element v = 4 g + e
   // at row 8 g + 4 (lane / 32) + e of the 32 x 32 tile
@@ -221,10 +127,10 @@ __global__ __launch_bounds__(512, 1) void k_calib_gemm_fp4(
   for (int i = 0; i < 2; ++i)
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
-      const int64_t col = tn * kCalTile + wn * 128 + j * 32 + (lane & 31);
+      const int64_t col = tn * kPlainTile + wn * 128 + j * 32 + (lane & 31);
 #pragma unroll
       for (int g = 0; g < 4; ++g) {
-        const int64_t row = tm * kCalTile + wm * 64 + i * 32 + g * 8 + (lane >> 5) * 4;
+        const int64_t row = tm * kPlainTile + wm * 64 + i * 32 + g * 8 + (lane >> 5) * 4;
         float* dst = C + row + col * ldc;
         const f4 v = {acc[i][j][4 * g], acc[i][j][4 * g + 1], acc[i][j][4 * g + 2],
                       acc[i][j][4 * g + 3]};
@@ -285,7 +191,7 @@ hipError_t launch_calib_mfma(hipStream_t stream, int64_t blocks, int64_t iters, 
 
 hipError_t launch_calib_gemm_fp4(hipStream_t stream, int64_t m, int64_t n, int64_t k,
                                  const uint8_t* pa, const uint8_t* pb, float* C, int64_t ldc) {
-  const int64_t tiles_m = m / kCalTile, tiles_n = n / kCalTile;
+  const int64_t tiles_m = m / kPlainTile, tiles_n = n / kPlainTile;
   hipLaunchKernelGGL(k_calib_gemm_fp4, dim3((unsigned)(tiles_m * tiles_n)), dim3(512), 0, stream,
                      pa, pb, C, ldc, k / kFragK, tiles_m, tiles_n);
   return hipGetLastError();

@@ -190,6 +190,24 @@ inline bool sum_limb_split(int r, int m, int* c0, int* c1) {
   return found;
 }
 
+// One-limb moduli (an extension of Sec. V-A): every class of m holds an
+// element of S, so one limb represents each residue (c1 = 0). Of them only
+// 11 is coprime to the first 26 moduli of the greedy list; the one-limb
+// list is 11 followed by that list.
+constexpr int kOneLimbModulus = 11;
+
+// the element of S congruent to r mod m of smallest magnitude, the positive
+// one on a tie; false if there is none
+inline bool one_limb_split(int r, int m, int* c) {
+  static const int S[] = {0, 1, -1, 2, -2, 3, -3, 4, -4, 6, -6, 8, -8, 12, -12};
+  for (int v : S)   // ascending magnitude, positive first
+    if ((((v - r) % m) + m) % m == 0) {
+      *c = v;
+      return true;
+    }
+  return false;
+}
+
 // ---- device-side constant blocks (plain data, copied once per device) ----
 struct ModConst {
   int m[kMaxModuli];
@@ -226,8 +244,52 @@ struct HostTables {
   int nk[kMaxModuli + 1];                  // Karatsuba moduli among the first L
   uint16_t lut8[256];                      // int8 -> three limb codes
   Big P[kMaxModuli + 1];                   // product of the first L moduli
+  // the one-limb list: 11, then the first 26 greedy moduli
+  std::vector<int> moduli1;
+  ModConst mod1;
+  CrtConst crt1[kMaxModuli + 1];
+  std::vector<uint16_t> lut1;
+  Big P1[kMaxModuli + 1];
   bool ok = false;
 };
+
+// P and the CRT constants of every prefix of a moduli list (Sec. V-B)
+inline bool build_crt(const std::vector<int>& moduli, CrtConst* crt, Big* P) {
+  for (int L = 0; L <= kMaxModuli; ++L) {
+    std::memset(&crt[L], 0, sizeof(CrtConst));
+    P[L] = Big(1);
+    if (L < 1) continue;
+    for (int l = 0; l < L; ++l) P[L].mul_small((uint32_t)moduli[l]);
+    CrtConst& c = crt[L];
+    c.L = L;
+    c.nc = crt_chunks(L);
+    const int B = kCrtChunkBits;
+    if (P[L].bitlen() > c.nc * B) return false;
+    double Pd = 0.0;
+    for (int q = 0; q < 4; ++q) {
+      c.Pc[q] = (double)P[L].bits(B * q, B);
+      Pd += std::ldexp(c.Pc[q], B * q);
+    }
+    for (int q = 0; q < 4; ++q) c.Qc[q] = std::ldexp(1.0 / Pd, B * q);
+    c.sym_limit = 0.5 * Pd * (1.0 - std::ldexp(1.0, -30));
+    for (int q = 0; q < 3; ++q) c.P[q] = P[L].bits(64 * q, 32) | (P[L].bits(64 * q + 32, 32) << 32);
+    for (int l = 0; l < L; ++l) {
+      int m = moduli[l];
+      Big Mi = P[L];
+      Mi.div_small((uint32_t)m);          // exact: M_l = P / m_l
+      Big tmp = Mi;
+      uint32_t Mmod = tmp.div_small((uint32_t)m);
+      int u = -1;
+      for (int x = 1; x < m; ++x)
+        if ((uint64_t)Mmod * x % m == 1) { u = x; break; }
+      if (u < 0) return false;
+      Big w = Mi;
+      w.mul_small((uint32_t)u);           // w_l = M_l u_l < P
+      for (int q = 0; q < 4; ++q) c.W[l][q] = (double)w.bits(B * q, B);
+    }
+  }
+  return true;
+}
 
 // Encoder LUT of modulus m: 3m entries, index r + m for a remainder
 // estimate r in [-m, 2m) of a signed integer x; entry = code(c0) |
@@ -283,40 +345,38 @@ inline bool build_tables(HostTables& T) {
     if (rest != 0) return false;
     T.lut8[v + 128] = (uint16_t)codes;
   }
-  // CRT constants for every L
-  for (int L = 0; L <= kMaxModuli; ++L) {
-    std::memset(&T.crt[L], 0, sizeof(CrtConst));
-    T.P[L] = Big(1);
-    if (L < 1) continue;
-    for (int l = 0; l < L; ++l) T.P[L].mul_small((uint32_t)T.moduli[l]);
-    CrtConst& c = T.crt[L];
-    c.L = L;
-    c.nc = crt_chunks(L);
-    const int B = kCrtChunkBits;
-    if (T.P[L].bitlen() > c.nc * B) return false;
-    double Pd = 0.0;
-    for (int q = 0; q < 4; ++q) {
-      c.Pc[q] = (double)T.P[L].bits(B * q, B);
-      Pd += std::ldexp(c.Pc[q], B * q);
-    }
-    for (int q = 0; q < 4; ++q) c.Qc[q] = std::ldexp(1.0 / Pd, B * q);
-    c.sym_limit = 0.5 * Pd * (1.0 - std::ldexp(1.0, -30));
-    for (int q = 0; q < 3; ++q) c.P[q] = T.P[L].bits(64 * q, 32) | (T.P[L].bits(64 * q + 32, 32) << 32);
-    for (int l = 0; l < L; ++l) {
-      int m = T.moduli[l];
-      Big Mi = T.P[L];
-      Mi.div_small((uint32_t)m);          // exact: M_l = P / m_l
-      Big tmp = Mi;
-      uint32_t Mmod = tmp.div_small((uint32_t)m);
-      int u = -1;
-      for (int x = 1; x < m; ++x)
-        if ((uint64_t)Mmod * x % m == 1) { u = x; break; }
-      if (u < 0) return false;
-      Big w = Mi;
-      w.mul_small((uint32_t)u);           // w_l = M_l u_l < P
-      for (int q = 0; q < 4; ++q) c.W[l][q] = (double)w.bits(B * q, B);
-    }
+  if (!build_crt(T.moduli, T.crt, T.P)) return false;
+
+  // the one-limb list: 11 (one limb, its LUT first), then the greedy
+  // moduli with their LUT entries unchanged
+  T.moduli1.assign(1, kOneLimbModulus);
+  T.moduli1.insert(T.moduli1.end(), T.moduli.begin(), T.moduli.begin() + (kMaxModuli - 1));
+  for (size_t l = 1; l < T.moduli1.size(); ++l)   // 11 is prime: coprime unless a multiple
+    if (T.moduli1[l] % kOneLimbModulus == 0) return false;
+  std::memset(&T.mod1, 0, sizeof(T.mod1));
+  T.lut1.clear();
+  const int m1 = kOneLimbModulus;
+  T.mod1.m[0] = m1;
+  T.mod1.ksum[0] = -1;
+  T.mod1.lut_off[0] = 0;
+  T.mod1.inv[0] = 1.0 / (double)m1;
+  T.mod1.md[0] = (double)m1;
+  for (int ri = -m1; ri < 2 * m1; ++ri) {
+    int c0;
+    if (!one_limb_split(((ri % m1) + m1) % m1, m1, &c0)) return false;
+    const int k0 = e2m1_code_of_limb(c0);
+    if (k0 < 0) return false;
+    T.lut1.push_back((uint16_t)k0);   // c1 = 0: code 0
   }
+  for (int l = 1; l < kMaxModuli; ++l) {
+    T.mod1.m[l] = T.mod.m[l - 1];
+    T.mod1.ksum[l] = -1;
+    T.mod1.lut_off[l] = 3 * m1 + T.mod.lut_off[l - 1];
+    T.mod1.inv[l] = T.mod.inv[l - 1];
+    T.mod1.md[l] = T.mod.md[l - 1];
+  }
+  T.lut1.insert(T.lut1.end(), T.lut.begin(), T.lut.begin() + T.mod.lut_off[kMaxModuli - 1]);
+  if (!build_crt(T.moduli1, T.crt1, T.P1)) return false;
   T.ok = true;
   return true;
 }

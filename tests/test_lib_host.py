@@ -37,7 +37,7 @@ def test_header_declares_the_boundary():
                      "ozfp4_sum_limb_table", "ozfp4_plane_count", "ozfp4_set_karatsuba",
                      "ozfp4_set_max_capacity", "ozfp4_dgemm_ozi", "ozfp4_ozi_config",
                      "ozfp4_ozi_limb_planes", "ozfp4_ozi_partials", "ozfp4_sgemm",
-                     "ozfp4_sgemm_capacity"):
+                     "ozfp4_sgemm_capacity", "ozfp4_set_one_limb_modulus"):
         assert required in names
 
 
@@ -126,6 +126,57 @@ def test_plane_count_in_both_modes(lib):
     finally:
         ozfp4.ozfp4_set_karatsuba(False)
     assert ozfp4.ozfp4_plane_count(18)[0] == 36
+
+
+def test_one_limb_list_matches_oracle(lib):
+    """With the one-limb setting the host queries follow the list 11, then
+    the greedy moduli: the list itself, the capacities at every L and cap,
+    the one-limb representatives of 11 (second limb 0) and the unchanged
+    two-limb tables of the others, two planes per modulus; the Karatsuba
+    mode is refused with it."""
+    try:
+        assert ozfp4.ozfp4_set_one_limb_modulus(True) == ozfp4.OZFP4_OK
+        for L in (2, 18, 19, 27):
+            assert ozfp4.ozfp4_moduli(L) == o.select_moduli_one_limb(L)
+        for cmax in (53, 63):
+            assert ozfp4.ozfp4_set_max_capacity(cmax) == ozfp4.OZFP4_OK
+            for L in range(2, 28):
+                ms = o.select_moduli_one_limb(L)
+                for k in (1, 3, 256, 4096, 16384, 32768, 131072):
+                    try:
+                        want = o.capacity_bits(k, ms, cmax)
+                    except ValueError:
+                        with pytest.raises(ozfp4.OzFP4Error) as ei:
+                            ozfp4.ozfp4_capacity(k, L)
+                        assert ei.value.code == ozfp4.OZFP4_EMODULI
+                        continue
+                    assert ozfp4.ozfp4_capacity(k, L) == want, (k, L, cmax)
+        ozfp4.ozfp4_set_max_capacity(53)
+        assert ozfp4.ozfp4_capacity(16384, 18) == (50, 50)
+        for idx, m in enumerate(o.select_moduli_one_limb(27)):
+            got_m, table = ozfp4.ozfp4_two_limb_table(idx)
+            assert got_m == m
+            for r in range(m):
+                if idx == 0:
+                    want = o.e2m1_code(o.one_limb_split(r, m))
+                else:
+                    c0, c1 = o.two_limb_split(r, m)
+                    want = o.e2m1_code(c0) | (o.e2m1_code(c1) << 4)
+                assert table[r] == want, (m, r)
+        assert ozfp4.ozfp4_plane_count(18) == (36, [-1] * 18)
+        ozfp4.ozfp4_set_karatsuba(True)
+        with pytest.raises(ozfp4.OzFP4Error) as ei:
+            ozfp4.ozfp4_plane_count(18)
+        assert ei.value.code == ozfp4.OZFP4_EINVAL
+        A = (ctypes.c_double * 4)()
+        C = (ctypes.c_double * 4)()
+        assert lib.ozfp4_dgemm(2, 2, 2, A, 2, A, 2, C, 2, 18) == ozfp4.OZFP4_EINVAL
+    finally:
+        ozfp4.ozfp4_set_karatsuba(False)
+        ozfp4.ozfp4_set_max_capacity(53)
+        ozfp4.ozfp4_set_one_limb_modulus(False)
+    assert ozfp4.ozfp4_moduli(18) == o.select_moduli(18)
+    assert ozfp4.ozfp4_capacity(16384, 18) == (51, 51)
 
 
 def test_plane_layout(lib):
