@@ -463,13 +463,15 @@ def main() -> int:
                     help="skip the paper's accuracy experiment (its input law, K = 8192, 128 x 128)")
     ap.add_argument("--no-table1", action="store_true",
                     help="skip the paper's configuration (19 moduli) at N = 4096, 8192, 16384")
+    ap.add_argument("--no-one-limb", action="store_true",
+                    help="skip the one-limb moduli list (11 first, one FP4 product for it)")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="also run a plain 1 GiB device copy and a 1 GiB read through the LDS-DMA path "
                          "(known traffic for the HBM byte counters)")
     args = ap.parse_args()
     if args.quick:
         for name in ("cpu_baseline", "native", "int8", "accuracy", "sweep4096", "phi4", "karatsuba",
-                     "ozi", "sgemm", "paper_accuracy", "table1"):
+                     "ozi", "sgemm", "paper_accuracy", "table1", "one_limb"):
             setattr(args, "no_" + name, True)
 
     world = int(os.environ.get("WORLD_SIZE", "1"))
@@ -505,6 +507,15 @@ def main() -> int:
 
     Ad, Bd = dev_cm(A, torch), dev_cm(B, torch)
     C = torch.empty_strided((N, N), (1, N), dtype=torch.float64, device="cuda")
+
+    def one_limb(call):
+        """call() with the one-limb moduli list (11 first), then the
+        greedy list again."""
+        ozfp4.ozfp4_set_one_limb_modulus(True)
+        try:
+            return call()
+        finally:
+            ozfp4.ozfp4_set_one_limb_modulus(False)
 
     if args.sweep:
         # accuracy on a 128 x 128 output block at full k (all 16384 elements)
@@ -650,15 +661,17 @@ def main() -> int:
         calls = {"emulation_L18": lambda: ozfp4.dgemm(Ad, Bd, 18, out=C),
                  "native_fp64": lambda: torch.matmul(Ar, Br, out=Cn),
                  "emulation_L19": lambda: ozfp4.dgemm(Ad, Bd, 19, out=C)}
+        if not args.no_one_limb:
+            calls["emulation_one_limb_L18"] = lambda: one_limb(lambda: ozfp4.dgemm(Ad, Bd, 18, out=C))
         rounds = max(5, args.steps)
         times = paired_times(torch, calls, rounds, max(2, args.warmup))
         st = {name: stats(v) for name, v in times.items()}
         nat = st["native_fp64"]
         cmp = {}
-        for Lc in (18, 19):
-            em = st[f"emulation_L{Lc}"]
+        for key in [n for n in calls if n != "native_fp64"]:
+            em = st[key]
             ratio = nat["median"] / em["median"]
-            cmp[f"L{Lc}"] = {
+            cmp[key.replace("emulation_", "")] = {
                 "speedup_of_emulation": ratio,
                 "emulation_ms": em, "emulation_tflops": 2.0 * N ** 3 / em["median"] / 1e9,
                 # a win only if every native call was slower than every emulated one
@@ -684,6 +697,33 @@ def main() -> int:
         ozfp4.dgemm(Ad, Bd, L, out=C)
         del Ar, Br, Cn
         torch.cuda.empty_cache()
+
+    if not args.no_one_limb:
+        # the one-limb moduli list: 11 (one limb, one FP4 product) and the
+        # first L - 1 greedy moduli, in place of the greedy list's L-th
+        # modulus (four products); reported beside the headline
+        log(f"one-limb moduli list, {L} moduli")
+        oms, ost = time_call(ozfp4, torch, lambda: one_limb(lambda: ozfp4.dgemm(Ad, Bd, L, out=C)),
+                             args.steps, args.warmup)
+        q1 = 4 * (L - 1) - 1 + 1      # the greedy L - 1 (169 without a1 b1), then 11's one product
+        rec = {"moduli": one_limb(lambda: ozfp4.ozfp4_moduli(L)),
+               "capacity_bits": list(one_limb(lambda: ozfp4.ozfp4_capacity(N, L))),
+               "ms": oms, "tflops": 2.0 * N ** 3 / oms / 1e9,
+               "stages_ms": dict(zip(stage_names, ost)),
+               "products_per_element": q1, "headline_products_per_element": Q,
+               "gemm_fp4_tflops": q1 * 2.0 * N ** 3 / ost[3] / 1e9,
+               "speedup_vs_headline": ms / oms}
+        if ref_block is not None:
+            Cb1 = block_of(C, rows, cols, torch)
+            b1, w1 = accuracy_bits(Cb1, ref_block)
+            rec.update({"error_bits": b1, "max_normalized_error": w1, "fp64_accurate": w1 <= 2.0 ** -50,
+                        "vs_rounded_product": elementwise_vs_rounded(Cb1, ref_block)})
+        if "native_fp64" in result:
+            rec["vs_native_fp64"] = result["native_fp64"]["vs_emulation"]["one_limb_L18"] \
+                if L == 18 else None
+        result["one_limb"] = rec
+        log(json.dumps(rec))
+        ozfp4.dgemm(Ad, Bd, L, out=C)
 
     if not args.no_sweep4096:
         # the moduli count of the headline: the smallest count whose output
@@ -712,6 +752,19 @@ def main() -> int:
                                "columns 0..127)", "runs": sw,
                                "smallest_fp64_accurate_moduli": min(ok) if ok else None,
                                "headline_moduli_is_smallest": (ok == [18])}
+        if not args.no_one_limb:
+            sw1 = []
+            for L2 in (17, 18):
+                ms2, _ = one_limb(lambda: time_dgemm(ozfp4, torch, A2d, B2d, C2, L2, 10, 2))
+                Cb2 = block_of(C2, rows2, rows2, torch)
+                bits2, worst2 = accuracy_bits(Cb2, ref2)
+                sw1.append({"n_moduli": L2,
+                            "capacity_bits": list(one_limb(lambda: ozfp4.ozfp4_capacity(N2, L2))),
+                            "ms": ms2, "tflops": 2.0 * N2 ** 3 / ms2 / 1e9,
+                            "error_bits": bits2, "max_normalized_error": worst2,
+                            "fp64_accurate": worst2 <= 2.0 ** -50})
+                log(json.dumps(sw1[-1]))
+            result["sweep4096"]["one_limb_runs"] = sw1
         del A2d, B2d, C2
         torch.cuda.empty_cache()
 
