@@ -20,7 +20,8 @@ documents the same one):
     congruent to r of smallest magnitude, the positive one on a tie;
   * everything else is scheme II unchanged: capacities from P by the same
     rule (here P = 11 P_{n-1}), the same shifts, integer conversion, CRT and
-    one rounding.
+    one rounding; for FP32 inputs the FP32 emulation's capacities and its
+    one rounding to binary32.
 """
 
 from __future__ import annotations
@@ -32,11 +33,12 @@ import numpy as np
 from .ozaki2_fp4 import (capacity_bits, crt_reconstruct, doubled_set, exact_int_matmul,
                          residue_products, residues, round_scaled, select_moduli,
                          shift_exponents, to_integers, to_integers_fraction)
+from .sgemm_fp4 import capacity_bits_fp32, round_scaled_f32
 
 __all__ = [
     "is_one_limb_modulus", "one_limb_moduli", "ONE_LIMB_MODULUS", "select_moduli_one_limb",
     "one_limb_split", "one_limb_table", "one_limb_plane", "residue_products_one_limb",
-    "dgemm_one_limb", "dgemm_one_limb_definition",
+    "dgemm_one_limb", "dgemm_one_limb_definition", "sgemm_one_limb",
 ]
 
 #: The one-limb modulus of the extension.
@@ -151,3 +153,33 @@ def dgemm_one_limb_definition(A: np.ndarray, B: np.ndarray, n_moduli: int,
             acc = sum(int(Ai[i, q]) * int(Bi[q, j]) for q in range(k))
             C[i, j] = round_scaled(acc, int(s[i]) + int(t[j]))
     return C
+
+
+def sgemm_one_limb(A: np.ndarray, B: np.ndarray, n_moduli: int, rows=None, cols=None) -> dict:
+    """C = A B for FP32 A, B by the FP32 emulation over the one-limb list:
+    the FP32 capacities c_A = min(24, ceil(b/2)), c_B = min(24, b - c_A)
+    from the list's P, the one-limb product for 11, and one rounding of the
+    exact product to binary32."""
+    A = np.asarray(A, dtype=np.float32).astype(np.float64)
+    B = np.asarray(B, dtype=np.float32).astype(np.float64)
+    m, k = A.shape
+    assert B.shape[0] == k
+    n = B.shape[1]
+    rows = np.arange(m) if rows is None else np.asarray(rows)
+    cols = np.arange(n) if cols is None else np.asarray(cols)
+    moduli = select_moduli_one_limb(n_moduli)
+    cA, cB = capacity_bits_fp32(k, moduli)
+    As, Bs = A[rows, :], B[:, cols]
+    s = shift_exponents(As, axis=1, c=cA)
+    t = shift_exponents(Bs, axis=0, c=cB)
+    Ai = to_integers(As, s, axis=1)
+    Bi = to_integers(Bs, t, axis=0)
+    res = [(residue_products_one_limb if q == ONE_LIMB_MODULUS else residue_products)(Ai, Bi, q)["r"]
+           for q in moduli]
+    x = crt_reconstruct(res, moduli)
+    C = np.empty((len(rows), len(cols)), dtype=np.float32)
+    for i in range(len(rows)):
+        for j in range(len(cols)):
+            C[i, j] = round_scaled_f32(x[i, j], int(s[i]) + int(t[j]))
+    return {"moduli": moduli, "cA": cA, "cB": cB, "s": s, "t": t, "Ai": Ai, "Bi": Bi,
+            "r": res, "x": x, "C": C}

@@ -2,8 +2,8 @@
 generator draws m, n, k (from 1 to 300, most of them ragged
 against every tile), the number of moduli, the exponent spread phi of the
 inputs, the capacity cap and the residue-GEMM route, and the library's C is
-compared bit for bit with the oracle's. Scheme I, the FP32 emulation, INT8
-and the two-term split route get their own draws. Each case prints its parameters before it runs,
+compared bit for bit with the oracle's. Scheme I, the FP32 emulation, INT8,
+the two-term split route and the one-limb moduli list get their own draws. Each case prints its parameters before it runs,
 so a failure names them."""
 
 import numpy as np
@@ -12,13 +12,14 @@ import pytest
 import oracle as o
 from gpu_util import announce, bits_equal, dev_cm, to_np
 from oracle.sgemm_fp4 import capacity_bits_fp32, sgemm as oracle_sgemm
+from oracle.one_limb_fp4 import dgemm_one_limb as oracle_one_limb
 from oracle.split2_fp4 import dgemm_split2 as oracle_split2
 from paper_2608_06812_amd.workloads import dgemm_inputs, int8_inputs
 
 pytestmark = pytest.mark.gpu
 
 SEED = 20261204
-N_DGEMM, N_SGEMM, N_OZI, N_INT8, N_SPLIT = 40, 16, 16, 16, 16
+N_DGEMM, N_SGEMM, N_OZI, N_INT8, N_SPLIT, N_ONE = 40, 16, 16, 16, 16, 16
 
 
 def _dim(rng):
@@ -149,4 +150,33 @@ def test_random_split(gpu_lib, case):
     want = oracle_split2(A, B, L)["C"]
     announce(f"random split case {case}: m={m} n={n} k={k} L={L} phi={phi} seed={seed}")
     C = to_np(gpu_lib.dgemm_split(dev_cm(A), dev_cm(B), L))
+    assert bits_equal(C, want)
+
+
+@pytest.mark.parametrize("case", range(N_ONE))
+def test_random_one_limb(gpu_lib, case):
+    """The one-limb moduli list (11 first) at caps 53 and 63."""
+    rng = np.random.default_rng([SEED + 5, case])
+    m, n, k = _dim(rng), _dim(rng), _dim(rng)
+    cmax = 63 if rng.random() < 0.3 else 53
+
+    def cap_ok(k_, L_):
+        try:
+            o.capacity_bits(k_, o.select_moduli_one_limb(L_), cmax=cmax)
+            return True
+        except ValueError:
+            return False
+    L = _moduli_for(k, rng, cap_ok)
+    phi = float(rng.choice([0.0, 0.5, 2.0, 6.0]))
+    seed = int(rng.integers(1 << 30))
+    A, B = dgemm_inputs(m, n, k, phi, seed)
+    want = oracle_one_limb(A, B, L, cmax=cmax)["C"]
+    announce(f"random one-limb case {case}: m={m} n={n} k={k} L={L} phi={phi} cmax={cmax} seed={seed}")
+    try:
+        gpu_lib.ozfp4_set_max_capacity(cmax)
+        gpu_lib.ozfp4_set_one_limb_modulus(True)
+        C = to_np(gpu_lib.dgemm(dev_cm(A), dev_cm(B), L))
+    finally:
+        gpu_lib.ozfp4_set_one_limb_modulus(False)
+        gpu_lib.ozfp4_set_max_capacity(53)
     assert bits_equal(C, want)

@@ -14,6 +14,10 @@ ties it to something other than itself.
   exact integer product mod m.
 * Integer inputs small enough for every capacity give fl(AB) = the exact
   product, by both lists.
+* The FP32 emulation over the list: capacities 24 / 24 at k = 16384 with
+  10 moduli, C on tiny matrices against the exact product of the converted
+  operands rounded once to binary32 (numpy's single rounding of the exact
+  double where that is exact), and small integers giving the exact product.
 * Planted mistakes (the two-limb route's c0 used as the one limb, a
   composition weight on the one-limb product, the modulus dropped from the
   list) are each caught."""
@@ -187,3 +191,32 @@ def test_dropping_the_modulus_is_caught(monkeypatch):
     orig = ol.select_moduli_one_limb
     monkeypatch.setattr(ol, "select_moduli_one_limb", lambda L: orig(L)[1:] + [o.select_moduli(L)[-1]])
     assert _list_pins_fail()
+
+
+def test_sgemm_one_limb_capacities_and_brute_force():
+    assert o.capacity_bits_fp32(16384, o.select_moduli_one_limb(10)) == (24, 24)
+    assert o.capacity_bits_fp32(16384, o.select_moduli_one_limb(9)) == (22, 21)
+    for L in (4, 10, 14):
+        for seed in range(3):
+            A, B = _tiny(500 + 10 * L + seed, 3, 4, 7, spread=12)
+            A, B = A.astype(np.float32), B.astype(np.float32)
+            out = o.sgemm_one_limb(A, B, L)
+            exact = o.exact_int_matmul(out["Ai"], out["Bi"])
+            assert np.all(exact == out["x"])
+            for i in range(3):
+                for j in range(4):
+                    v = Fraction(int(exact[i, j])) / Fraction(2) ** (int(out["s"][i]) + int(out["t"][j]))
+                    d = float(v)
+                    if Fraction(d) == v:        # exact in FP64: one rounding to binary32
+                        assert out["C"][i, j] == np.float32(d)
+                    assert out["C"][i, j] == o.round_scaled_f32(int(exact[i, j]),
+                                                                int(out["s"][i]) + int(out["t"][j]))
+
+
+def test_sgemm_one_limb_small_integers_exact():
+    rng = np.random.default_rng(8)
+    A = rng.integers(-(1 << 10), 1 << 10, (5, 30)).astype(np.float32)
+    B = rng.integers(-(1 << 10), 1 << 10, (30, 6)).astype(np.float32)
+    exact = A.astype(np.int64) @ B.astype(np.int64)
+    assert np.array_equal(o.sgemm_one_limb(A, B, 10)["C"], exact.astype(np.float32))
+    assert np.array_equal(o.sgemm(A, B, 10)["C"], exact.astype(np.float32))
