@@ -881,6 +881,31 @@ def main() -> int:
         nms32 = (time.perf_counter() - t0) * 1e3 / 5
         nbits32, nworst32 = accuracy_bits(block_of(Cn32, rows32, rows32, torch).astype(np.float64), ref32)
         flops32 = (4 * L32 - 1) * 2.0 * N ** 3
+        one32 = None
+        if not args.no_one_limb:
+            # the one-limb list (11 first): the same 24-bit capacities with
+            # 4 (L - 1) - 1 + 1 products; then the emulation with both lists
+            # and native FP32 timed alike, alternating
+            L1 = one_limb(lambda: ozfp4.sgemm_moduli(N))
+            oms32, ost32 = one_limb(lambda: time_call(
+                ozfp4, torch, lambda: ozfp4.sgemm(A32d, B32d, L1, out=C32), max(3, args.steps // 2), 1))
+            obits32, oworst32 = accuracy_bits(block_of(C32, rows32, rows32, torch).astype(np.float64),
+                                              ref32)
+            calls32 = {"emulation": lambda: ozfp4.sgemm(A32d, B32d, L32, out=C32),
+                       "emulation_one_limb": lambda: one_limb(lambda: ozfp4.sgemm(A32d, B32d, L1, out=C32)),
+                       "native_fp32": lambda: torch.matmul(Ar32, Br32, out=Cn32)}
+            t32 = {k: stats(v) for k, v in paired_times(torch, calls32, max(5, args.steps // 2), 1).items()}
+            one32 = {"n_moduli": L1, "capacity_bits": list(one_limb(lambda: ozfp4.ozfp4_sgemm_capacity(N, L1))),
+                     "ms": oms32, "tflops": 2.0 * N ** 3 / oms32 / 1e9,
+                     "stages_ms": dict(zip(stage_names, ost32)),
+                     "products_per_element": 4 * (L1 - 1), "error_bits": obits32,
+                     "max_normalized_error": oworst32,
+                     "paired": {"protocol": "each call alone between synchronisations, HIP events, "
+                                            "the three alternating", "ms": t32,
+                                "one_limb_vs_native_fp32": t32["native_fp32"]["median"] /
+                                t32["emulation_one_limb"]["median"],
+                                "greedy_vs_native_fp32": t32["native_fp32"]["median"] /
+                                t32["emulation"]["median"]}}
         result["sgemm"] = {
             "workload": f"sgemm m=n=k={N}, phi=0.5 inputs rounded to FP32", "n_moduli": L32,
             "capacity_bits": list(ozfp4.ozfp4_sgemm_capacity(N, L32)), "ms": sms,
@@ -891,7 +916,7 @@ def main() -> int:
             "block": "64x64 (every 256th row and column)",
             "native_fp32": {"ms": nms32, "tflops": 2.0 * N ** 3 / nms32 / 1e9,
                             "error_bits": nbits32, "max_normalized_error": nworst32},
-            "speedup_vs_native_fp32": nms32 / sms}
+            "speedup_vs_native_fp32": nms32 / sms, "one_limb": one32}
         log(json.dumps(result["sgemm"]))
         del A32d, B32d, C32, Ar32, Br32, Cn32
         torch.cuda.empty_cache()

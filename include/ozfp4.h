@@ -199,9 +199,9 @@ int ozfp4_set_karatsuba(int enable);
 int ozfp4_set_max_capacity(int bits);
 
 /*
- * ozfp4_set_one_limb_modulus -- the moduli list of subsequent FP64 scheme-II
- * calls (ozfp4_dgemm, ozfp4_dgemm_noalloc and the hooks ozfp4_scales,
- * ozfp4_limb_planes, ozfp4_residues), default 0. An extension of the moduli
+ * ozfp4_set_one_limb_modulus -- the moduli list of subsequent scheme-II
+ * calls (ozfp4_dgemm, ozfp4_dgemm_noalloc, ozfp4_sgemm and the hooks
+ * ozfp4_scales, ozfp4_limb_planes, ozfp4_residues), default 0. An extension of the moduli
  * choice of Sec. V-A: 11 is a one-limb modulus (every class mod 11 holds an
  * element of S: 0, +-1, +-2, +-3, +-4, and 5 = -6, 6 = 6 mod 11), so its
  * residues need one limb (c1 = 0) and its residue product is the single
@@ -210,11 +210,12 @@ int ozfp4_set_max_capacity(int bits);
  * list (11 is the only one-limb modulus coprime to all of them); P, the
  * capacities and hence C follow from that list by the same rules (at
  * k = 16384 and L = 18: P = 2^115.07, c_A = c_B = 50, against 51 with the
- * greedy 18). Modulus index 0 of the planes and residues is 11 (its second
- * limb plane is all zero); the others are the greedy list's. The Karatsuba
- * mode cannot be combined with it: those calls return OZFP4_EINVAL.
- * ozfp4_sgemm, ozfp4_dgemm_split and ozfp4_dgemm_ozi keep their own
- * moduli. The host queries (ozfp4_moduli, ozfp4_capacity,
+ * greedy 18; for ozfp4_sgemm at k = 16384, 10 moduli still give 24 / 24).
+ * Modulus index 0 of the planes and residues is 11 (its second limb plane
+ * is all zero); the others are the greedy list's. The Karatsuba mode cannot
+ * be combined with it: those FP64 calls return OZFP4_EINVAL.
+ * ozfp4_dgemm_split and ozfp4_dgemm_ozi keep their own moduli. The host
+ * queries (ozfp4_moduli, ozfp4_capacity, ozfp4_sgemm_capacity,
  * ozfp4_two_limb_table, ozfp4_plane_count) follow the setting. A
  * process-wide setting, like the stream.
  */

@@ -211,8 +211,8 @@ int make_dgemm_plan(int64_t m, int64_t n, int64_t k, int L, DgemmPlan* p, bool f
   if (!T) return OZFP4_EHIP;
   p->m = m; p->n = n; p->k = k; p->L = L;
   p->f32 = f32;
-  p->one_limb = g_one_limb && !f32;
-  if (p->one_limb && g_karatsuba) return OZFP4_EINVAL;
+  p->one_limb = g_one_limb;
+  if (p->one_limb && g_karatsuba && !f32) return OZFP4_EINVAL;
   if (!capacity_split(p->one_limb ? T->P1[L] : T->P[L], k, f32 ? kFp32Capacity : g_cmax, &p->cA,
                       &p->cB))
     return OZFP4_EMODULI;
@@ -330,7 +330,7 @@ int run_dgemm(const DgemmPlan& p, DeviceState* d, const void* Av, int64_t lda, c
   // Karatsuba mode's encoder lives in its own translation unit
   if (p.f32) {
     HIP_TRY(launch_encode_f32((unsigned)encode_grid(nfa), lut_bytes, g_stream, Af, (int64_t)1, lda,
-                              p.m, p.k, amax_a, p.cA, pa, p.plane_a, nfa, p.kblocks, L, d->d_mod,
+                              p.m, p.k, amax_a, p.cA, pa, p.plane_a, nfa, p.kblocks, L, d_mod,
                               lut, lut_entries));
   } else if (p.kar) {
     HIP_TRY(launch_encode_kar(p.cA > 53, (unsigned)encode_grid(nfa), lut_bytes, g_stream, A,
@@ -347,7 +347,7 @@ int run_dgemm(const DgemmPlan& p, DeviceState* d, const void* Av, int64_t lda, c
   record(d, 2);
   if (p.f32) {
     HIP_TRY(launch_encode_f32((unsigned)encode_grid(nfb), lut_bytes, g_stream, Bf, ldb, (int64_t)1,
-                              p.n, p.k, amax_b, p.cB, pb, p.plane_b, nfb, p.kblocks, L, d->d_mod,
+                              p.n, p.k, amax_b, p.cB, pb, p.plane_b, nfb, p.kblocks, L, d_mod,
                               lut, lut_entries));
   } else if (p.kar) {
     HIP_TRY(launch_encode_kar(p.cB > 53, (unsigned)encode_grid(nfb), lut_bytes, g_stream, B, ldb,
@@ -394,15 +394,15 @@ int run_dgemm(const DgemmPlan& p, DeviceState* d, const void* Av, int64_t lda, c
 
   // stage 4: CRT reconstruction and inverse scaling
   const int64_t nthreads = ((p.m + kCrtRows - 1) / kCrtRows) * p.n;
+  const CrtConst* crt = (p.one_limb ? d->d_crt1 : d->d_crt) + L;
   if (p.f32) {
     HIP_TRY(launch_crt_f32(g_stream, crt_chunks(L), R, p.m_pad, rplane, p.m, p.n,
-                           amax_a, amax_b, p.cA, p.cB, d->d_crt + L, static_cast<float*>(Cv),
+                           amax_a, amax_b, p.cA, p.cB, crt, static_cast<float*>(Cv),
                            ldc));
     record(d, 5);
     return OZFP4_OK;
   }
   double* C = static_cast<double*>(Cv);
-  const CrtConst* crt = (p.one_limb ? d->d_crt1 : d->d_crt) + L;
   for (int64_t t0 = 0; t0 < nthreads; t0 += kLaunchThreads) {
     const unsigned grid = blocks_for(std::min(nthreads - t0, kLaunchThreads), 256);
     if (crt_chunks(L) == 3)
@@ -805,7 +805,8 @@ int ozfp4_sgemm_capacity(int64_t k, int n_moduli, int32_t* c_a, int32_t* c_b) {
   const HostTables* T = tables();
   if (!T) return OZFP4_EHIP;
   int a, b;
-  if (!capacity_split(T->P[n_moduli], k, kFp32Capacity, &a, &b)) return OZFP4_EMODULI;
+  if (!capacity_split(g_one_limb ? T->P1[n_moduli] : T->P[n_moduli], k, kFp32Capacity, &a, &b))
+    return OZFP4_EMODULI;
   *c_a = a;
   *c_b = b;
   return OZFP4_OK;

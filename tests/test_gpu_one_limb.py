@@ -4,9 +4,9 @@
 residue plane (11's from the single-product GEMM, the others from the
 default GEMM), and C bit for bit, on ragged shapes, shapes whose tile grid
 takes the XCD-share mapping of both GEMMs, edge values, the largest k, the
-wide capacity cap, the allocation-free entry point, and sampled outputs of
-m = n = k = 16384 with 18 moduli, whose normalized error must stay within
-2^-50."""
+wide capacity cap, the allocation-free entry point, the FP32 emulation over
+the list, and sampled outputs of m = n = k = 16384 with 18 moduli, whose
+normalized error must stay within 2^-50."""
 
 import numpy as np
 import pytest
@@ -147,6 +147,17 @@ def test_one_limb_noalloc_matches(gpu_lib):
     gpu_lib.dgemm_noalloc(Ad, Bd, out, 18)
     assert bits_equal(to_np(out), ref)
     assert bits_equal(ref, o.dgemm_one_limb(A, B, 18)["C"])
+
+
+@pytest.mark.parametrize("m,n,k,L", [(131, 67, 129, 10), (300, 300, 200, 10), (64, 700, 64, 19),
+                                     (1, 1, 1, 10)])
+def test_one_limb_sgemm_bit_exact(gpu_lib, m, n, k, L):
+    A, B = dgemm_inputs(m, n, k, 2.0, SEED + 10 + m)
+    A, B = A.astype(np.float32), B.astype(np.float32)
+    want = o.sgemm_one_limb(A, B, L)["C"]
+    announce(f"one-limb sgemm m={m} n={n} k={k} L={L}")
+    C = to_np(gpu_lib.sgemm(dev_cm(A), dev_cm(B), L))
+    assert C.dtype == np.float32 and np.array_equal(C.view(np.uint32), want.view(np.uint32))
 
 
 def test_one_limb_too_few_moduli_refused(gpu_lib):

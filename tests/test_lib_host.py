@@ -261,6 +261,22 @@ def test_sgemm_capacity_matches_oracle(lib):
         assert ozfp4.ozfp4_sgemm_capacity(16384, 19) == (24, 24)
     finally:
         ozfp4.ozfp4_set_max_capacity(53)
+    # with the one-limb list the FP32 capacities follow its P
+    try:
+        assert ozfp4.ozfp4_set_one_limb_modulus(True) == ozfp4.OZFP4_OK
+        for L in range(2, 28):
+            for k in (1, 100, 16384, 131072):
+                try:
+                    want = o.capacity_bits_fp32(k, o.select_moduli_one_limb(L))
+                except ValueError:
+                    with pytest.raises(ozfp4.OzFP4Error):
+                        ozfp4.ozfp4_sgemm_capacity(k, L)
+                    continue
+                assert ozfp4.ozfp4_sgemm_capacity(k, L) == want
+        assert ozfp4.sgemm_moduli(16384) == 10
+        assert ozfp4.ozfp4_sgemm_capacity(16384, 9) == (22, 21)
+    finally:
+        ozfp4.ozfp4_set_one_limb_modulus(False)
 
 
 @pytest.mark.parametrize("args,code", [
