@@ -119,7 +119,7 @@ __global__ __launch_bounds__(256) void k_crt_f32(
 #pragma unroll
       for (int c = NC - 2; c >= 0; --c) Qe = __builtin_fma(sig[e][c], cc->Qc[c], Qe);
       const double q = __builtin_rint(Qe);
-      float out;
+      float out = 0.0f;
       bool done = false;
       if constexpr (NC == 3) done = crt_fast3_f32(sig[e][0], sig[e][1], sig[e][2], q, cc, e2, &out);
       if (!done)
