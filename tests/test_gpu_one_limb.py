@@ -178,6 +178,28 @@ def test_one_limb_off_restores_the_greedy_list(gpu_lib):
     assert bits_equal(to_np(gpu_lib.dgemm(dev_cm(A), dev_cm(B), 14)), o.dgemm(A, B, 14)["C"])
 
 
+def test_one_limb_residues_4096_every_modulus_full(gpu_lib):
+    """m = n = k = 4096 with 18 moduli of the one-limb list: all 2^24
+    residues of every modulus (11's from k_gemm_one_limb over 16 x 16 tiles,
+    the others from k_gemm_res over 16 x 32 tiles per modulus) against
+    ((A~ mod m)(B~ mod m)) mod m from the oracle's converted integers, one
+    exact CPU FP64 product per modulus."""
+    N, L = 4096, 18
+    A, B = dgemm_inputs(N, N, N, 0.5, SEED + 11)
+    moduli = o.select_moduli_one_limb(L)
+    cA, cB = o.capacity_bits(N, moduli)
+    Ai = o.to_integers(A, o.shift_exponents(A, axis=1, c=cA), axis=1)
+    Bi = o.to_integers(B, o.shift_exponents(B, axis=0, c=cB), axis=0)
+    announce("one-limb residues 4096^3 L=18, every modulus in full")
+    R = to_np(gpu_lib.residues(dev_cm(A), dev_cm(B), L))
+    assert 168.0 ** 2 * N < 2.0 ** 53
+    for l, m in enumerate(moduli):
+        ra = o.residues(Ai, m).astype(np.float64)
+        rb = o.residues(Bi, m).astype(np.float64)
+        want = np.mod(np.rint(ra @ rb).astype(np.int64), m)
+        assert np.array_equal(R[l].T.astype(np.int64), want), f"modulus {m}"
+
+
 @pytest.mark.slow
 def test_one_limb_16384_sampled_and_accurate(gpu_lib):
     """m = n = k = 16384 with 18 moduli of the one-limb list (capacities
