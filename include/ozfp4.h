@@ -146,6 +146,11 @@ int ozfp4_init(void);
  * moduli needs 226 MB and fits). Every call on one device shares that
  * device's array: calls that overlap on one device (asynchronous work on
  * two streams, two host threads) race, like the regular workspace.
+ * When the library stream is capturing (hipStreamBeginCapture), the call
+ * only records its kernels into the graph and returns OZFP4_OK: it does not
+ * synchronize, reads back no non-finite flag (C is unspecified for NaN or
+ * Inf inputs) and records no stage times. Every launch of such a graph
+ * reuses the same scratch array, so launches must not overlap on a device.
  */
 int ozfp4_dgemm_noalloc(int64_t m, int64_t n, int64_t k,
                         const double* A, int64_t lda,

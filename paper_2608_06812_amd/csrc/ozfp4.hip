@@ -692,8 +692,17 @@ int ozfp4_dgemm_noalloc(int64_t m, int64_t n, int64_t k, const double* A, int64_
   rc = make_dgemm_plan(m, n, k, n_moduli, &p);
   if (rc) return rc;
   if (p.total > (size_t)OZFP4_SCRATCH_BYTES) return OZFP4_ESCRATCH;
+  // under stream capture the kernels are recorded into the caller's graph:
+  // no stage events, and no read-back of the non-finite flag (that would
+  // synchronize the capturing stream)
+  hipStreamCaptureStatus capture = hipStreamCaptureStatusNone;
+  HIP_TRY(hipStreamIsCapturing(g_stream, &capture));
+  const bool captured = capture != hipStreamCaptureStatusNone;
+  const bool profile = g_profile;
+  if (captured) g_profile = false;
   rc = run_dgemm(p, d, A, lda, B, ldb, C, ldc, 4, nullptr, nullptr, d->scratch);
-  if (rc) return rc;
+  g_profile = profile;
+  if (rc || captured) return rc;
   return finish_with_flag(d, reinterpret_cast<int*>(d->scratch + p.off_flag), 5);
 }
 

@@ -3,7 +3,9 @@ nothing: through the C ABI, two calls in a row (the second smaller) give C
 bit for bit equal to ozfp4_dgemm's on the same inputs and to the oracle's;
 the device's free memory does not change across the calls; calls beyond the
 fixed scratch or on a device that was not set up are refused before any GPU
-work; ozfp4_dgemm still works afterwards."""
+work; ozfp4_dgemm still works afterwards; recorded into a graph by stream
+capture and replayed several times, with eager work between the replays,
+every replay gives the eager result."""
 
 import numpy as np
 import pytest
@@ -74,3 +76,51 @@ def test_noalloc_refusals_and_dgemm_after(gpu_lib):
     want = o.dgemm(A, B, 16)["C"]
     assert bits_equal(to_np(C), want)
     assert bits_equal(to_np(gpu_lib.dgemm(Ad, Bd, 16)), want)
+
+
+def test_noalloc_captured_graph_replays(gpu_lib):
+    """Recorded into a graph by torch's stream capture and replayed three
+    times, with the program's own eager work between the replays (C cleared
+    by a fill kernel, an eager allocation-free call on other inputs that
+    reuses the scratch array, an eager ozfp4_dgemm) and synchronizations:
+    every replay gives the eager result bit for bit."""
+    import torch
+    assert gpu_lib.ozfp4_init() == gpu_lib.OZFP4_OK
+    m, n, k, L = 300, 260, 500, 18
+    A, B = dgemm_inputs(m, n, k, 0.5, SEED + 5)
+    Ad, Bd = dev_cm(A), dev_cm(B)
+    want = o.dgemm(A, B, L)["C"]
+    A2, B2 = dgemm_inputs(200, 100, 300, 0.5, SEED + 6)
+    A2d, B2d = dev_cm(A2), dev_cm(B2)
+    want2 = o.dgemm(A2, B2, 14)["C"]
+    C = torch.zeros((n, m), dtype=torch.float64, device="cuda").t()
+    C2 = torch.zeros((100, 200), dtype=torch.float64, device="cuda").t()
+    # eager warm-up on a side stream before the capture
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        gpu_lib.ozfp4_set_stream(side.cuda_stream)
+        assert _call_noalloc(gpu_lib, Ad, Bd, C, L) == gpu_lib.OZFP4_OK
+    torch.cuda.current_stream().wait_stream(side)
+    torch.cuda.synchronize()
+    assert bits_equal(to_np(C), want)
+    graph = torch.cuda.CUDAGraph()
+    announce("dgemm_noalloc under stream capture")
+    with torch.cuda.graph(graph):
+        gpu_lib.ozfp4_set_stream(torch.cuda.current_stream().cuda_stream)
+        rc = _call_noalloc(gpu_lib, Ad, Bd, C, L)
+    assert rc == gpu_lib.OZFP4_OK
+    for r in range(3):
+        C.fill_(float("nan"))
+        torch.cuda.synchronize()
+        announce(f"graph replay {r}")
+        graph.replay()
+        torch.cuda.synchronize()
+        assert bits_equal(to_np(C), want), f"replay {r}"
+        gpu_lib.ozfp4_set_stream(torch.cuda.current_stream().cuda_stream)
+        assert _call_noalloc(gpu_lib, A2d, B2d, C2, 14) == gpu_lib.OZFP4_OK
+        torch.cuda.synchronize()
+        assert bits_equal(to_np(C2), want2)
+        assert bits_equal(to_np(gpu_lib.dgemm(A2d, B2d, 14)), want2)
+        torch.cuda.synchronize()
+    del graph
