@@ -9,12 +9,17 @@ representative c0 + 13 c1 with c0, c1 in S, and picks them greedily,
 largest first, pairwise coprime. A modulus whose every class already holds
 an element of S needs only c1 = 0: one limb per operand, so its residue
 product is the single limb product a0 b0 instead of four. Such one-limb
-moduli are small (at most 13), and of them only 11 is coprime to the greedy
-list's first 26 moduli (11 is the greedy rule's own 27th pick).
+moduli are small (2..9, 11, 13); 11 is the only one coprime to the greedy
+list's first 26 moduli (it is the greedy rule's own 27th pick).
 
 Reading of this extension (the paper does not use it; the GPU library
 documents the same one):
-  * n moduli = 11 followed by the first n - 1 moduli of the greedy list,
+  * with h one-limb heads (0 <= h <= 5), the list of n moduli starts with
+    the first min(h, n) of 11, 9, 8, 7, 5 (pairwise coprime one-limb
+    moduli, each taking one product) and continues by the greedy rule of
+    Sec. V-A over the two-limb moduli, seeded with those heads: descending,
+    each pick coprime to every modulus chosen so far; h = 0 is the greedy
+    list, h = 1 is 11 followed by the first n - 1 greedy moduli;
     2 <= n <= 27;
   * the one-limb representative of a residue r mod m is the element of S
     congruent to r of smallest magnitude, the positive one on a tie;
@@ -31,18 +36,22 @@ import math
 import numpy as np
 
 from .ozaki2_fp4 import (capacity_bits, crt_reconstruct, doubled_set, exact_int_matmul,
-                         residue_products, residues, round_scaled, select_moduli,
-                         shift_exponents, to_integers, to_integers_fraction)
+                         residue_products, residues, round_scaled, shift_exponents,
+                         to_integers, to_integers_fraction, two_limb_moduli)
 from .sgemm_fp4 import capacity_bits_fp32, round_scaled_f32
 
 __all__ = [
-    "is_one_limb_modulus", "one_limb_moduli", "ONE_LIMB_MODULUS", "select_moduli_one_limb",
+    "is_one_limb_modulus", "one_limb_moduli", "ONE_LIMB_MODULUS", "ONE_LIMB_HEADS",
+    "select_moduli_one_limb",
     "one_limb_split", "one_limb_table", "one_limb_plane", "residue_products_one_limb",
     "dgemm_one_limb", "dgemm_one_limb_definition", "sgemm_one_limb",
 ]
 
 #: The one-limb modulus of the extension.
 ONE_LIMB_MODULUS = 11
+
+#: The one-limb heads, in the order a list takes them.
+ONE_LIMB_HEADS = (11, 9, 8, 7, 5)
 
 
 def is_one_limb_modulus(m: int) -> bool:
@@ -55,14 +64,26 @@ def one_limb_moduli(limit: int = 64) -> list[int]:
     return [m for m in range(2, limit + 1) if is_one_limb_modulus(m)]
 
 
-def select_moduli_one_limb(L: int) -> list[int]:
-    """11, then the first L - 1 moduli of the greedy list (Sec. V-A)."""
+def select_moduli_one_limb(L: int, heads: int = 1) -> list[int]:
+    """The first min(heads, L) of 11, 9, 8, 7, 5, then the greedy rule of
+    Sec. V-A over the two-limb moduli seeded with them, L moduli in all."""
     if not 2 <= L <= 27:
         raise ValueError("the one-limb list has 2..27 moduli")
-    rest = select_moduli(L - 1)
-    if any(math.gcd(ONE_LIMB_MODULUS, q) != 1 for q in rest):
-        raise ValueError("11 must be coprime to the greedy moduli")
-    return [ONE_LIMB_MODULUS] + rest
+    if not 0 <= heads <= len(ONE_LIMB_HEADS):
+        raise ValueError("0..5 one-limb heads")
+    chosen = list(ONE_LIMB_HEADS[:min(heads, L)])
+    for m in sorted(two_limb_moduli(), reverse=True):
+        if len(chosen) == L:
+            break
+        if all(math.gcd(m, q) == 1 for q in chosen):
+            chosen.append(m)
+    if len(chosen) != L:
+        raise ValueError(f"only {len(chosen)} coprime moduli exist")
+    return chosen
+
+
+def _heads_of(moduli, heads: int) -> set:
+    return set(moduli[:min(heads, len(moduli))])
 
 
 def one_limb_split(r: int, m: int) -> int:
@@ -97,9 +118,9 @@ def residue_products_one_limb(Ai: np.ndarray, Bi: np.ndarray, m: int) -> dict:
 
 
 def dgemm_one_limb(A: np.ndarray, B: np.ndarray, n_moduli: int, rows=None, cols=None,
-                   check_definition: bool = False, cmax: int = 53) -> dict:
-    """C = A B by scheme II over 11 and the first n_moduli - 1 greedy moduli:
-    the one-limb product for 11, the four-product two-limb route for the
+                   check_definition: bool = False, cmax: int = 53, heads: int = 1) -> dict:
+    """C = A B by scheme II over the list of select_moduli_one_limb: the
+    one-limb product for the heads, the four-product two-limb route for the
     others (Sec. V-A, Sec. VI-D), the CRT and one rounding (Sec. V-B).
 
     rows / cols restrict the output to a block (the shifts still come from
@@ -112,7 +133,8 @@ def dgemm_one_limb(A: np.ndarray, B: np.ndarray, n_moduli: int, rows=None, cols=
     n = B.shape[1]
     rows = np.arange(m) if rows is None else np.asarray(rows)
     cols = np.arange(n) if cols is None else np.asarray(cols)
-    moduli = select_moduli_one_limb(n_moduli)
+    moduli = select_moduli_one_limb(n_moduli, heads)
+    one = _heads_of(moduli, heads)
     cA, cB = capacity_bits(k, moduli, cmax)
     As, Bs = A[rows, :], B[:, cols]
     s = shift_exponents(As, axis=1, c=cA)
@@ -120,7 +142,7 @@ def dgemm_one_limb(A: np.ndarray, B: np.ndarray, n_moduli: int, rows=None, cols=
     Ai = to_integers(As, s, axis=1)
     Bi = to_integers(Bs, t, axis=0)
     assert np.all(np.abs(Ai) <= (1 << cA)) and np.all(np.abs(Bi) <= (1 << cB))
-    res = [(residue_products_one_limb if q == ONE_LIMB_MODULUS else residue_products)(Ai, Bi, q)["r"]
+    res = [(residue_products_one_limb if q in one else residue_products)(Ai, Bi, q)["r"]
            for q in moduli]
     x = crt_reconstruct(res, moduli)
     if check_definition:
@@ -134,7 +156,7 @@ def dgemm_one_limb(A: np.ndarray, B: np.ndarray, n_moduli: int, rows=None, cols=
 
 
 def dgemm_one_limb_definition(A: np.ndarray, B: np.ndarray, n_moduli: int,
-                              cmax: int = 53) -> np.ndarray:
+                              cmax: int = 53, heads: int = 1) -> np.ndarray:
     """The defined result without the residue route, capacities from the
     one-limb list's P: C_ij = RN(sum_k A~_ik B~_kj 2^-(s_i+t_j)) by
     Python-int sums (tiny inputs)."""
@@ -142,7 +164,7 @@ def dgemm_one_limb_definition(A: np.ndarray, B: np.ndarray, n_moduli: int,
     B = np.asarray(B, dtype=np.float64)
     m, k = A.shape
     n = B.shape[1]
-    cA, cB = capacity_bits(k, select_moduli_one_limb(n_moduli), cmax)
+    cA, cB = capacity_bits(k, select_moduli_one_limb(n_moduli, heads), cmax)
     s = shift_exponents(A, axis=1, c=cA)
     t = shift_exponents(B, axis=0, c=cB)
     Ai = to_integers_fraction(A, s, axis=1)
@@ -155,7 +177,8 @@ def dgemm_one_limb_definition(A: np.ndarray, B: np.ndarray, n_moduli: int,
     return C
 
 
-def sgemm_one_limb(A: np.ndarray, B: np.ndarray, n_moduli: int, rows=None, cols=None) -> dict:
+def sgemm_one_limb(A: np.ndarray, B: np.ndarray, n_moduli: int, rows=None, cols=None,
+                   heads: int = 1) -> dict:
     """C = A B for FP32 A, B by the FP32 emulation over the one-limb list:
     the FP32 capacities c_A = min(24, ceil(b/2)), c_B = min(24, b - c_A)
     from the list's P, the one-limb product for 11, and one rounding of the
@@ -167,14 +190,15 @@ def sgemm_one_limb(A: np.ndarray, B: np.ndarray, n_moduli: int, rows=None, cols=
     n = B.shape[1]
     rows = np.arange(m) if rows is None else np.asarray(rows)
     cols = np.arange(n) if cols is None else np.asarray(cols)
-    moduli = select_moduli_one_limb(n_moduli)
+    moduli = select_moduli_one_limb(n_moduli, heads)
+    one = _heads_of(moduli, heads)
     cA, cB = capacity_bits_fp32(k, moduli)
     As, Bs = A[rows, :], B[:, cols]
     s = shift_exponents(As, axis=1, c=cA)
     t = shift_exponents(Bs, axis=0, c=cB)
     Ai = to_integers(As, s, axis=1)
     Bi = to_integers(Bs, t, axis=0)
-    res = [(residue_products_one_limb if q == ONE_LIMB_MODULUS else residue_products)(Ai, Bi, q)["r"]
+    res = [(residue_products_one_limb if q in one else residue_products)(Ai, Bi, q)["r"]
            for q in moduli]
     x = crt_reconstruct(res, moduli)
     C = np.empty((len(rows), len(cols)), dtype=np.float32)

@@ -14,6 +14,14 @@ ties it to something other than itself.
   exact integer product mod m.
 * Integer inputs small enough for every capacity give fl(AB) = the exact
   product, by both lists.
+* Lists with h one-limb heads (11, 9, 8, 7, 5): the heads are one-limb and
+  pairwise coprime, h = 0 and h = 1 give the greedy list and 11 followed by
+  it, the 21-moduli lists with 4 and 5 heads are written out by hand; where
+  a list's capacities equal the greedy list's (5 heads and 21 moduli
+  against the greedy 18 at k = 16384 and 4096, 4 heads and 21 against the
+  greedy 19), C is the same bit for bit; brute force for every h; the
+  representatives of 9, 8, 7 and 5 written out by hand; an unseeded tail
+  (a two-limb modulus sharing a factor with a head) is caught.
 * The FP32 emulation over the list: capacities 24 / 24 at k = 16384 with
   10 moduli, C on tiny matrices against the exact product of the converted
   operands rounded once to binary32 (numpy's single rounding of the exact
@@ -220,3 +228,88 @@ def test_sgemm_one_limb_small_integers_exact():
     exact = A.astype(np.int64) @ B.astype(np.int64)
     assert np.array_equal(o.sgemm_one_limb(A, B, 10)["C"], exact.astype(np.float32))
     assert np.array_equal(o.sgemm(A, B, 10)["C"], exact.astype(np.float32))
+
+
+def test_heads_are_coprime_one_limb_moduli():
+    assert o.ONE_LIMB_HEADS == (11, 9, 8, 7, 5)
+    h = o.ONE_LIMB_HEADS
+    assert all(o.is_one_limb_modulus(m) for m in h)
+    assert all(math.gcd(a, b) == 1 for i, a in enumerate(h) for b in h[i + 1:])
+    # 9 * 8 * 7 * 5 = 2520 and 11: no other set of pairwise coprime one-limb
+    # moduli (2..9, 11, 13) has a larger product without 13
+    assert math.prod(h) == 27720
+
+
+def test_heads_lists():
+    printed = _printed_moduli()
+    for L in range(2, 28):
+        assert o.select_moduli_one_limb(L, heads=0) == o.select_moduli(L)
+        assert o.select_moduli_one_limb(L, heads=1) == [11] + o.select_moduli(L - 1)
+    # 5 heads: 115 (5), 112 (7, 2), 111 (3) are skipped by the seeded rule
+    assert o.select_moduli_one_limb(21, heads=5) == [
+        11, 9, 8, 7, 5, 169, 113, 109, 107, 103, 101, 97, 89, 83, 79, 73, 71, 67, 61, 59, 53]
+    assert o.select_moduli_one_limb(21, heads=4) == [
+        11, 9, 8, 7, 169, 115, 113, 109, 107, 103, 101, 97, 89, 83, 79, 73, 71, 67, 61, 59, 53]
+    assert o.select_moduli_one_limb(3, heads=5) == [11, 9, 8]
+    for h in range(6):
+        lst = o.select_moduli_one_limb(27, heads=h)
+        assert len(set(lst)) == 27
+        assert all(math.gcd(a, b) == 1 for i, a in enumerate(lst) for b in lst[i + 1:])
+    assert printed[:18] == o.select_moduli(18)
+    with pytest.raises(ValueError):
+        o.select_moduli_one_limb(18, heads=6)
+
+
+def test_heads_capacities_match_the_greedy_lists():
+    five = o.select_moduli_one_limb(21, heads=5)
+    four = o.select_moduli_one_limb(21, heads=4)
+    for k in (4096, 16384):
+        assert o.capacity_bits(k, five) == o.capacity_bits(k, o.select_moduli(18))
+        assert o.capacity_bits(k, four) == o.capacity_bits(k, o.select_moduli(19))
+    assert o.capacity_bits(16384, five) == (51, 51)
+    assert o.capacity_bits(16384, four) == (53, 53)
+
+
+def test_representatives_of_the_other_heads():
+    assert o.one_limb_table(9) == [0, 1, 2, 3, 4, -4, -3, -2, -1]
+    assert o.one_limb_table(8) == [0, 1, 2, 3, 4, -3, -2, -1]
+    assert o.one_limb_table(7) == [0, 1, 2, 3, -3, -2, -1]
+    assert o.one_limb_table(5) == [0, 1, 2, -2, -1]
+
+
+@pytest.mark.parametrize("h,L", [(2, 9), (3, 12), (4, 21), (5, 21), (5, 6), (0, 14)])
+def test_heads_brute_force_tiny(h, L):
+    for seed in range(3):
+        A, B = _tiny(700 + 10 * h + seed, 3, 4, 6)
+        out = o.dgemm_one_limb(A, B, L, check_definition=True, heads=h)
+        assert np.array_equal(out["C"], o.dgemm_one_limb_definition(A, B, L, heads=h))
+        exact = o.exact_int_matmul(out["Ai"], out["Bi"])
+        for q, r in zip(out["moduli"], out["r"]):
+            assert np.array_equal(np.asarray(r, dtype=object), np.mod(exact, q))
+
+
+def test_same_capacities_give_the_same_c():
+    """At k = 16384 the 21-moduli lists with 5 and 4 heads have the
+    capacities of the greedy 18 and 19: C is the same bit for bit."""
+    rng = np.random.default_rng(12)
+    k = 16384
+    A = (rng.random((3, k)) - 0.5) * np.exp(0.5 * rng.standard_normal((3, k)))
+    B = (rng.random((k, 4)) - 0.5) * np.exp(0.5 * rng.standard_normal((k, 4)))
+    g18, g19 = o.dgemm(A, B, 18)["C"], o.dgemm(A, B, 19)["C"]
+    assert not np.array_equal(g18, g19)
+    assert np.array_equal(o.dgemm_one_limb(A, B, 21, heads=5)["C"].view(np.int64), g18.view(np.int64))
+    assert np.array_equal(o.dgemm_one_limb(A, B, 21, heads=4)["C"].view(np.int64), g19.view(np.int64))
+
+
+def test_unseeded_tail_is_caught(monkeypatch):
+    orig = ol.select_moduli_one_limb
+
+    def unseeded(L, heads=1):
+        h = list(o.ONE_LIMB_HEADS[:min(heads, L)])
+        return h + o.select_moduli(L - len(h))
+    monkeypatch.setattr(ol, "select_moduli_one_limb", unseeded)
+    A, B = _tiny(31, 3, 4, 5)
+    with pytest.raises((ValueError, AssertionError)):
+        o.dgemm_one_limb(A, B, 14, heads=5, check_definition=True)
+    monkeypatch.setattr(ol, "select_moduli_one_limb", orig)
+    o.dgemm_one_limb(A, B, 14, heads=5, check_definition=True)
