@@ -511,11 +511,11 @@ def main() -> int:
     def one_limb(call):
         """call() with the one-limb moduli list (11 first), then the
         greedy list again."""
-        ozfp4.ozfp4_set_one_limb_modulus(True)
+        ozfp4.ozfp4_set_one_limb_moduli(1)
         try:
             return call()
         finally:
-            ozfp4.ozfp4_set_one_limb_modulus(False)
+            ozfp4.ozfp4_set_one_limb_moduli(0)
 
     if args.sweep:
         # accuracy on a 128 x 128 output block at full k (all 16384 elements)

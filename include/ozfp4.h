@@ -204,27 +204,33 @@ int ozfp4_set_karatsuba(int enable);
 int ozfp4_set_max_capacity(int bits);
 
 /*
- * ozfp4_set_one_limb_modulus -- the moduli list of subsequent scheme-II
- * calls (ozfp4_dgemm, ozfp4_dgemm_noalloc, ozfp4_sgemm and the hooks
- * ozfp4_scales, ozfp4_limb_planes, ozfp4_residues), default 0. An extension of the moduli
- * choice of Sec. V-A: 11 is a one-limb modulus (every class mod 11 holds an
- * element of S: 0, +-1, +-2, +-3, +-4, and 5 = -6, 6 = 6 mod 11), so its
+ * ozfp4_set_one_limb_moduli -- the moduli list of subsequent scheme-II calls
+ * (ozfp4_dgemm, ozfp4_dgemm_noalloc, ozfp4_sgemm and the hooks
+ * ozfp4_scales, ozfp4_limb_planes, ozfp4_residues): heads = 0..5 one-limb
+ * heads, default 0. An extension of the moduli choice of Sec. V-A: a
+ * one-limb modulus has an element of S in every residue class (11: 0, +-1,
+ * +-2, +-3, +-4, and 5 = -6, 6 = 6 mod 11; 9, 8, 7 and 5 likewise), so its
  * residues need one limb (c1 = 0) and its residue product is the single
- * limb product a0 b0 (mod 11), one FP4 product instead of four. With 1,
- * n_moduli = L selects 11 followed by the first L - 1 moduli of the greedy
- * list (11 is the only one-limb modulus coprime to all of them); P, the
- * capacities and hence C follow from that list by the same rules (at
- * k = 16384 and L = 18: P = 2^115.07, c_A = c_B = 50, against 51 with the
- * greedy 18; for ozfp4_sgemm at k = 16384, 10 moduli still give 24 / 24).
- * Modulus index 0 of the planes and residues is 11 (its second limb plane
- * is all zero); the others are the greedy list's. The Karatsuba mode cannot
- * be combined with it: those FP64 calls return OZFP4_EINVAL.
+ * limb product a0 b0 mod m, one FP4 product instead of four. With h heads,
+ * n_moduli = L selects the first min(h, L) of 11, 9, 8, 7, 5, then the
+ * two-limb moduli by the greedy rule of Sec. V-A seeded with those heads
+ * (descending, each pick coprime to every modulus chosen so far); h = 0 is
+ * the greedy list, h = 1 is 11 followed by the greedy list's first L - 1.
+ * P, the capacities and hence C follow from that list by the same rules;
+ * where they equal another list's capacities, C is the same bit for bit. At
+ * k = 16384: h = 1, L = 18 gives 50 / 50 bits (the greedy 18: 51 / 51);
+ * h = 5, L = 21 gives 51 / 51 (C of the greedy 18) and h = 4, L = 21 gives
+ * 53 / 53 (C of the greedy 19); for ozfp4_sgemm, h = 1 and 10 moduli still
+ * give 24 / 24. Modulus indices 0..min(h, L) - 1 of the planes and residues
+ * are the heads (second limb plane all zero). The Karatsuba mode cannot be
+ * combined with heads: those FP64 calls return OZFP4_EINVAL.
  * ozfp4_dgemm_split and ozfp4_dgemm_ozi keep their own moduli. The host
  * queries (ozfp4_moduli, ozfp4_capacity, ozfp4_sgemm_capacity,
- * ozfp4_two_limb_table, ozfp4_plane_count) follow the setting. A
- * process-wide setting, like the stream.
+ * ozfp4_two_limb_table, ozfp4_plane_count) follow the setting. Returns
+ * OZFP4_EINVAL for heads outside 0..5. A process-wide setting, like the
+ * stream.
  */
-int ozfp4_set_one_limb_modulus(int enable);
+int ozfp4_set_one_limb_moduli(int heads);
 
 /* Releases every device workspace and table of the library, after waiting
  * for each device's work. A later call sets them up again. */
@@ -235,21 +241,22 @@ const char* ozfp4_strerror(int code);
 
 /* ---- host-only queries (no GPU work; usable without a device) ---------- */
 
-/* Writes the first n_moduli moduli (Sec. V-A greedy order; with the one-limb
- * setting 11 first, see ozfp4_set_one_limb_modulus) to the HOST array
+/* Writes the first n_moduli moduli (Sec. V-A greedy order; with one-limb
+ * heads the heads first, see ozfp4_set_one_limb_moduli) to the HOST array
  * out[n_moduli]; n_moduli in 1..OZFP4_MAX_MODULI, else OZFP4_EINVAL. */
 int ozfp4_moduli(int n_moduli, int32_t* out);
 
 /* Capacities (c_A, c_B) used for inner dimension k with n_moduli moduli,
  * the current capacity cap and moduli list (see ozfp4_dgemm and
- * ozfp4_set_one_limb_modulus). HOST pointers.
+ * ozfp4_set_one_limb_moduli). HOST pointers.
  * OZFP4_EINVAL for k < 1 or a null pointer, OZFP4_EMODULI when n_moduli is
  * outside 2..27 or the moduli cannot hold k. */
 int ozfp4_capacity(int64_t k, int n_moduli, int32_t* c_a, int32_t* c_b);
 
 /* Canonical two-limb split of every residue r in [0, m_l) of modulus l
- * (index in the current moduli list; for the one-limb modulus 11 the
- * element of S congruent to r of smallest magnitude, c1 = 0): HOST array
+ * (index in the current moduli list; for a one-limb head the element of S
+ * congruent to r of smallest magnitude, the positive one on a tie, and
+ * c1 = 0): HOST array
  * out[m_l] of bytes, E2M1 code of
  * c0 in the low nibble and of c1 in the high nibble, where
  * c0 + 13 c1 = r (mod m_l). The split takes the representative r' of r in

@@ -40,9 +40,13 @@ struct DeviceState {
   uint16_t* d_lut = nullptr;
   uint32_t* d_lut_k = nullptr;   // encoder LUT of the Karatsuba mode
   uint16_t* d_lut8 = nullptr;
-  ModConst* d_mod1 = nullptr;   // the one-limb list
-  CrtConst* d_crt1 = nullptr;
-  uint16_t* d_lut1 = nullptr;
+  struct List {                 // a list with one-limb heads (index h)
+    ModConst* mod = nullptr;
+    ModConst* tail = nullptr;
+    ModConst* head = nullptr;
+    CrtConst* crt = nullptr;    // kMaxModuli + 1 entries, index L
+    uint16_t* lut = nullptr;
+  } lists[kMaxHeads + 1];
   uint8_t* ws = nullptr;
   size_t ws_bytes = 0;
   int* h_flag = nullptr;      // pinned host word for the non-finite flag
@@ -57,7 +61,7 @@ DeviceState g_dev[kMaxDevices];
 hipStream_t g_stream = nullptr;
 bool g_profile = false;
 bool g_karatsuba = false;
-bool g_one_limb = false;     // FP64 scheme II over the one-limb list (11 first)
+int g_heads = 0;             // one-limb heads of the scheme-II moduli list (0..kMaxHeads)
 int g_cmax = 53;             // capacity cap: 53 (the paper's rule) .. 63
 double g_stage_ms[kMaxStages];
 int g_nstages = 0;
@@ -90,9 +94,13 @@ void release_device(DeviceState& d) {
   (void)hipFree(d.d_lut);
   (void)hipFree(d.d_lut_k);
   (void)hipFree(d.d_lut8);
-  (void)hipFree(d.d_mod1);
-  (void)hipFree(d.d_crt1);
-  (void)hipFree(d.d_lut1);
+  for (auto& Ld : d.lists) {
+    (void)hipFree(Ld.mod);
+    (void)hipFree(Ld.tail);
+    (void)hipFree(Ld.head);
+    (void)hipFree(Ld.crt);
+    (void)hipFree(Ld.lut);
+  }
   if (d.h_flag) (void)hipHostFree(d.h_flag);
   for (int e = 0; e <= kMaxStages; ++e)
     if (d.ev[e]) (void)hipEventDestroy(d.ev[e]);
@@ -111,13 +119,21 @@ int init_device(DeviceState& d, const HostTables* T) {
   HIP_TRY(hipMemcpy(d.d_lut_k, T->lut_k.data(), T->lut_k.size() * sizeof(uint32_t),
                     hipMemcpyHostToDevice));
   HIP_TRY(hipMemcpy(d.d_lut8, T->lut8, sizeof(T->lut8), hipMemcpyHostToDevice));
-  HIP_TRY(hipMalloc(&d.d_mod1, sizeof(ModConst)));
-  HIP_TRY(hipMalloc(&d.d_crt1, sizeof(CrtConst) * (kMaxModuli + 1)));
-  HIP_TRY(hipMalloc(&d.d_lut1, T->lut1.size() * sizeof(uint16_t)));
-  HIP_TRY(hipMemcpy(d.d_mod1, &T->mod1, sizeof(ModConst), hipMemcpyHostToDevice));
-  HIP_TRY(hipMemcpy(d.d_crt1, T->crt1, sizeof(CrtConst) * (kMaxModuli + 1), hipMemcpyHostToDevice));
-  HIP_TRY(hipMemcpy(d.d_lut1, T->lut1.data(), T->lut1.size() * sizeof(uint16_t),
-                    hipMemcpyHostToDevice));
+  for (int h = 1; h <= kMaxHeads; ++h) {
+    const HostTables::List& Lh = T->lists[h];
+    DeviceState::List& Ld = d.lists[h];
+    HIP_TRY(hipMalloc(&Ld.mod, sizeof(ModConst)));
+    HIP_TRY(hipMalloc(&Ld.tail, sizeof(ModConst)));
+    HIP_TRY(hipMalloc(&Ld.head, sizeof(ModConst)));
+    HIP_TRY(hipMalloc(&Ld.crt, sizeof(CrtConst) * (kMaxModuli + 1)));
+    HIP_TRY(hipMalloc(&Ld.lut, Lh.lut.size() * sizeof(uint16_t)));
+    HIP_TRY(hipMemcpy(Ld.mod, &Lh.mod, sizeof(ModConst), hipMemcpyHostToDevice));
+    HIP_TRY(hipMemcpy(Ld.tail, &Lh.tail, sizeof(ModConst), hipMemcpyHostToDevice));
+    HIP_TRY(hipMemcpy(Ld.head, &Lh.head, sizeof(ModConst), hipMemcpyHostToDevice));
+    HIP_TRY(hipMemcpy(Ld.crt, Lh.crt, sizeof(CrtConst) * (kMaxModuli + 1), hipMemcpyHostToDevice));
+    HIP_TRY(hipMemcpy(Ld.lut, Lh.lut.data(), Lh.lut.size() * sizeof(uint16_t),
+                      hipMemcpyHostToDevice));
+  }
   HIP_TRY(hipHostMalloc(reinterpret_cast<void**>(&d.h_flag), sizeof(int), hipHostMallocDefault));
   for (int i = 0; i <= kMaxStages; ++i) HIP_TRY(hipEventCreate(&d.ev[i]));
   // each device holds its own copy of the scratch array: keep its address
@@ -175,7 +191,8 @@ struct DgemmPlan {
   int64_t plane_a, plane_b;  // bytes per plane
   bool kar;                  // Karatsuba mode
   bool f32;                  // FP32 inputs and output (capacity cap 24)
-  bool one_limb;             // the one-limb list: 11 (one limb), then the greedy moduli
+  int heads;                 // one-limb heads of the list (0: the greedy list)
+  int nh;                    // of them among the call's L moduli: min(heads, L)
   int nplanes;               // planes per operand: 2L, plus the sum planes in the Karatsuba mode
   // workspace offsets
   size_t off_amax_a, off_amax_b, off_flag, off_pa, off_pb, off_r, total;
@@ -211,10 +228,11 @@ int make_dgemm_plan(int64_t m, int64_t n, int64_t k, int L, DgemmPlan* p, bool f
   if (!T) return OZFP4_EHIP;
   p->m = m; p->n = n; p->k = k; p->L = L;
   p->f32 = f32;
-  p->one_limb = g_one_limb;
-  if (p->one_limb && g_karatsuba && !f32) return OZFP4_EINVAL;
-  if (!capacity_split(p->one_limb ? T->P1[L] : T->P[L], k, f32 ? kFp32Capacity : g_cmax, &p->cA,
-                      &p->cB))
+  p->heads = g_heads;
+  p->nh = std::min(g_heads, L);
+  if (p->heads && g_karatsuba && !f32) return OZFP4_EINVAL;
+  if (!capacity_split(p->heads ? T->lists[p->heads].P[L] : T->P[L], k,
+                      f32 ? kFp32Capacity : g_cmax, &p->cA, &p->cB))
     return OZFP4_EMODULI;
   p->m_pad = round_up(m, kTile);
   p->n_pad = round_up(n, kTile);
@@ -318,12 +336,12 @@ int run_dgemm(const DgemmPlan& p, DeviceState* d, const void* Av, int64_t lda, c
   if (last < 1) return OZFP4_OK;
 
   // stage 1, 2: fused conversion + residues + limbs + E2M1 packing
-  const ModConst& mod = p.one_limb ? T->mod1 : T->mod;
-  const ModConst* d_mod = p.one_limb ? d->d_mod1 : d->d_mod;
+  const ModConst& mod = p.heads ? T->lists[p.heads].mod : T->mod;
+  const ModConst* d_mod = p.heads ? d->lists[p.heads].mod : d->d_mod;
   const int lut_entries = mod.lut_off[L - 1] + 3 * mod.m[L - 1];
   const size_t lut_bytes = (p.kar ? sizeof(uint32_t) : sizeof(uint16_t)) * (size_t)lut_entries;
   const void* lut = p.kar ? static_cast<const void*>(d->d_lut_k)
-                          : static_cast<const void*>(p.one_limb ? d->d_lut1 : d->d_lut);
+                          : static_cast<const void*>(p.heads ? d->lists[p.heads].lut : d->d_lut);
   const int64_t nfa = (p.m_pad / kFragLines) * p.kblocks;
   const int64_t nfb = (p.n_pad / kFragLines) * p.kblocks;
   // an operand whose capacity exceeds 53 bits takes the wide encoder; the
@@ -364,21 +382,24 @@ int run_dgemm(const DgemmPlan& p, DeviceState* d, const void* Av, int64_t lda, c
   record(d, 3);
   if (last < 3) return OZFP4_OK;
 
-  // stage 3: fused residue GEMM for all moduli. In the one-limb list the
-  // moduli after the first are the greedy list's first L - 1, so the
-  // default GEMM covers them from their planes and residue planes on; the
-  // one-limb modulus takes the single-product GEMM.
+  // stage 3: fused residue GEMM for all moduli. In a list with one-limb
+  // heads, the default GEMM covers the two-limb moduli after the heads from
+  // their planes and residue planes on (with the list's tail constants),
+  // and the heads take the single-product GEMM.
   const int64_t tiles_m = p.m_pad / kTileM, tiles_n = p.n_pad / kTileN;
-  const int Lg = p.one_limb ? L - 1 : L;
+  const int Lg = L - p.nh;
   const int64_t nblocks = tiles_m * tiles_n * Lg;
   const int64_t rplane = p.m_pad * p.n_pad;
-  if (p.one_limb) {
-    hipLaunchKernelGGL(k_gemm_res, dim3((unsigned)nblocks), dim3(kWaves * 64), 0, g_stream,
-                       pa + 2 * p.plane_a, pb + 2 * p.plane_b, R + rplane, p.plane_a, p.plane_b,
-                       p.kblocks, tiles_m, tiles_n, nblocks, p.m_pad, rplane, d->d_mod);
-    HIP_TRY(hipGetLastError());
-    HIP_TRY(launch_gemm_one_limb(g_stream, pa, pb, R, p.m_pad, p.m_pad, p.n_pad, p.kblocks,
-                                 T->mod1.m[0]));
+  if (p.heads) {
+    if (Lg > 0) {
+      hipLaunchKernelGGL(k_gemm_res, dim3((unsigned)nblocks), dim3(kWaves * 64), 0, g_stream,
+                         pa + 2 * p.nh * p.plane_a, pb + 2 * p.nh * p.plane_b, R + p.nh * rplane,
+                         p.plane_a, p.plane_b, p.kblocks, tiles_m, tiles_n, nblocks, p.m_pad,
+                         rplane, d->lists[p.heads].tail);
+      HIP_TRY(hipGetLastError());
+    }
+    HIP_TRY(launch_gemm_one_limb(g_stream, pa, pb, R, p.m_pad, rplane, p.plane_a, p.plane_b,
+                                 p.m_pad, p.n_pad, p.kblocks, p.nh, d->lists[p.heads].head));
   } else if (p.kar) {
     HIP_TRY(launch_gemm_res_kar((unsigned)nblocks, g_stream, pa, pb, R, p.plane_a, p.plane_b,
                                 p.kblocks, tiles_m, tiles_n, nblocks, p.m_pad, p.m_pad * p.n_pad,
@@ -394,9 +415,10 @@ int run_dgemm(const DgemmPlan& p, DeviceState* d, const void* Av, int64_t lda, c
 
   // stage 4: CRT reconstruction and inverse scaling
   const int64_t nthreads = ((p.m + kCrtRows - 1) / kCrtRows) * p.n;
-  const CrtConst* crt = (p.one_limb ? d->d_crt1 : d->d_crt) + L;
+  const CrtConst* crt = (p.heads ? d->lists[p.heads].crt : d->d_crt) + L;
+  const int nc = (p.heads ? T->lists[p.heads].crt : T->crt)[L].nc;
   if (p.f32) {
-    HIP_TRY(launch_crt_f32(g_stream, crt_chunks(L), R, p.m_pad, rplane, p.m, p.n,
+    HIP_TRY(launch_crt_f32(g_stream, nc, R, p.m_pad, rplane, p.m, p.n,
                            amax_a, amax_b, p.cA, p.cB, crt, static_cast<float*>(Cv),
                            ldc));
     record(d, 5);
@@ -405,7 +427,7 @@ int run_dgemm(const DgemmPlan& p, DeviceState* d, const void* Av, int64_t lda, c
   double* C = static_cast<double*>(Cv);
   for (int64_t t0 = 0; t0 < nthreads; t0 += kLaunchThreads) {
     const unsigned grid = blocks_for(std::min(nthreads - t0, kLaunchThreads), 256);
-    if (crt_chunks(L) == 3)
+    if (nc == 3)
       hipLaunchKernelGGL(k_crt<3>, dim3(grid), dim3(256), 0, g_stream, R, p.m_pad,
                          rplane, p.m, p.n, amax_a, amax_b, p.cA, p.cB, crt, C,
                          ldc, t0);
@@ -619,7 +641,7 @@ int run_split(const SplitPlan& p, DeviceState* d, const double* A, int64_t lda, 
   HIP_TRY(hipGetLastError());
   record(d, 4);
   const uint8_t* R = ws + p.off_r;
-  HIP_TRY(launch_crt_split(g_stream, crt_chunks(L), R, R + p.rset, R + 2 * p.rset, R + 3 * p.rset,
+  HIP_TRY(launch_crt_split(g_stream, T->crt[L].nc, R, R + p.rset, R + 2 * p.rset, R + 3 * p.rset,
                            p.m_pad, p.m_pad * p.n_pad, p.m, p.n, amax_a, amax_b, p.cA, p.cB, p.d,
                            d->d_mod, d->d_crt + L, C, ldc));
   record(d, 5);
@@ -814,7 +836,8 @@ int ozfp4_sgemm_capacity(int64_t k, int n_moduli, int32_t* c_a, int32_t* c_b) {
   const HostTables* T = tables();
   if (!T) return OZFP4_EHIP;
   int a, b;
-  if (!capacity_split(g_one_limb ? T->P1[n_moduli] : T->P[n_moduli], k, kFp32Capacity, &a, &b))
+  if (!capacity_split(g_heads ? T->lists[g_heads].P[n_moduli] : T->P[n_moduli], k, kFp32Capacity,
+                      &a, &b))
     return OZFP4_EMODULI;
   *c_a = a;
   *c_b = b;
@@ -934,7 +957,7 @@ int ozfp4_moduli(int n_moduli, int32_t* out) {
   if (n_moduli < 1 || n_moduli > OZFP4_MAX_MODULI || !out) return OZFP4_EINVAL;
   const HostTables* T = tables();
   if (!T) return OZFP4_EHIP;
-  const std::vector<int>& list = g_one_limb ? T->moduli1 : T->moduli;
+  const std::vector<int>& list = g_heads ? T->lists[g_heads].moduli : T->moduli;
   for (int i = 0; i < n_moduli; ++i) out[i] = list[i];
   return OZFP4_OK;
 }
@@ -945,7 +968,7 @@ int ozfp4_capacity(int64_t k, int n_moduli, int32_t* c_a, int32_t* c_b) {
   const HostTables* T = tables();
   if (!T) return OZFP4_EHIP;
   int a, b;
-  if (!capacity_split(g_one_limb ? T->P1[n_moduli] : T->P[n_moduli], k, g_cmax, &a, &b))
+  if (!capacity_split(g_heads ? T->lists[g_heads].P[n_moduli] : T->P[n_moduli], k, g_cmax, &a, &b))
     return OZFP4_EMODULI;
   *c_a = a;
   *c_b = b;
@@ -956,9 +979,9 @@ int ozfp4_two_limb_table(int modulus_index, uint8_t* out, int32_t* m_out) {
   if (modulus_index < 0 || modulus_index >= OZFP4_MAX_MODULI || !out || !m_out) return OZFP4_EINVAL;
   const HostTables* T = tables();
   if (!T) return OZFP4_EHIP;
-  const ModConst& mod = g_one_limb ? T->mod1 : T->mod;
+  const ModConst& mod = g_heads ? T->lists[g_heads].mod : T->mod;
   const int m = mod.m[modulus_index];
-  const uint16_t* lut = (g_one_limb ? T->lut1.data() : T->lut.data()) + mod.lut_off[modulus_index];
+  const uint16_t* lut = (g_heads ? T->lists[g_heads].lut.data() : T->lut.data()) + mod.lut_off[modulus_index];
   for (int r = 0; r < m; ++r) {
     const uint16_t e = lut[r + m];  // remainder estimate r, non-negative value
     out[r] = (uint8_t)((e & 0xf) | ((e >> 8) & 0xf) << 4);
@@ -987,8 +1010,9 @@ int ozfp4_set_karatsuba(int enable) {
   return OZFP4_OK;
 }
 
-int ozfp4_set_one_limb_modulus(int enable) {
-  g_one_limb = enable != 0;
+int ozfp4_set_one_limb_moduli(int heads) {
+  if (heads < 0 || heads > kMaxHeads) return OZFP4_EINVAL;
+  g_heads = heads;
   return OZFP4_OK;
 }
 
@@ -1003,7 +1027,7 @@ int ozfp4_plane_count(int n_moduli, int32_t* n_planes, int32_t* sum_plane) {
   if (!n_planes) return OZFP4_EINVAL;
   const HostTables* T = tables();
   if (!T) return OZFP4_EHIP;
-  if (g_karatsuba && g_one_limb) return OZFP4_EINVAL;
+  if (g_karatsuba && g_heads) return OZFP4_EINVAL;
   *n_planes = 2 * n_moduli + (g_karatsuba ? T->nk[n_moduli] : 0);
   if (sum_plane)
     for (int l = 0; l < n_moduli; ++l)

@@ -103,7 +103,8 @@ inline int greedy13(int x) {
 inline bool limb_in_S(int c) { return e2m1_code_of_limb(c) >= 0; }
 
 // ---- Sec. V-A: two-limb moduli and the greedy list ----
-inline std::vector<int> greedy_moduli() {
+// every two-limb modulus up to 400, descending
+inline std::vector<int> two_limb_moduli_desc() {
   static const int S[] = {-12, -8, -6, -4, -3, -2, -1, 0, 1, 2, 3, 4, 6, 8, 12};
   std::vector<int> two_limb;
   for (int m = 400; m >= 2; --m) {
@@ -116,8 +117,16 @@ inline std::vector<int> greedy_moduli() {
       }
     if (count == m) two_limb.push_back(m);
   }
-  std::vector<int> chosen;
-  for (int m : two_limb) {  // descending
+  return two_limb;
+}
+
+// the greedy choice of Sec. V-A seeded with `seed`: descending over the
+// two-limb moduli, each pick coprime to every modulus chosen so far, until
+// kMaxModuli moduli (the seed first)
+inline std::vector<int> greedy_seeded(const std::vector<int>& seed) {
+  std::vector<int> chosen = seed;
+  for (int m : two_limb_moduli_desc()) {
+    if ((int)chosen.size() >= kMaxModuli) break;
     bool ok = true;
     for (int q : chosen) {
       int a = m, b = q;
@@ -125,10 +134,11 @@ inline std::vector<int> greedy_moduli() {
       if (a != 1) { ok = false; break; }
     }
     if (ok) chosen.push_back(m);
-    if ((int)chosen.size() == kMaxModuli) break;
   }
   return chosen;
 }
+
+inline std::vector<int> greedy_moduli() { return greedy_seeded({}); }
 
 // canonical two-limb split of residue r in [0, m): returns false if none
 inline bool two_limb_split(int r, int m, int* c0, int* c1) {
@@ -191,10 +201,13 @@ inline bool sum_limb_split(int r, int m, int* c0, int* c1) {
 }
 
 // One-limb moduli (an extension of Sec. V-A): every class of m holds an
-// element of S, so one limb represents each residue (c1 = 0). Of them only
-// 11 is coprime to the first 26 moduli of the greedy list; the one-limb
-// list is 11 followed by that list.
-constexpr int kOneLimbModulus = 11;
+// element of S, so one limb represents each residue (c1 = 0) and the
+// residue product is one limb product. A list with h one-limb heads starts
+// with the first h of 11, 9, 8, 7, 5 (pairwise coprime) and continues by the
+// greedy rule seeded with them; h = 1 is 11 followed by the greedy list
+// (11 is coprime to its first 26 moduli).
+constexpr int kMaxHeads = 5;
+constexpr int kOneLimbHeads[kMaxHeads] = {11, 9, 8, 7, 5};
 
 // the element of S congruent to r mod m of smallest magnitude, the positive
 // one on a tie; false if there is none
@@ -223,11 +236,10 @@ struct ModConst {
 // is an integer below 2^53 and exact in FP64. Three chunks (126 bits) cover
 // P for up to 19 moduli (P < 2^124), four (168 bits) up to 27 (P < 2^162).
 constexpr int kCrtChunkBits = 42;
-inline int crt_chunks(int L) { return L <= 19 ? 3 : 4; }
 
 struct CrtConst {
   int L;
-  int nc;                    // chunks in use, crt_chunks(L)
+  int nc;                    // chunks in use: 3 while P < 2^126, else 4
   double W[kMaxModuli][4];   // 42-bit chunks of w_l
   double Pc[4];              // 42-bit chunks of P
   double Qc[4];              // ~ 2^(42 c) / P, weights of the quotient estimate
@@ -244,12 +256,16 @@ struct HostTables {
   int nk[kMaxModuli + 1];                  // Karatsuba moduli among the first L
   uint16_t lut8[256];                      // int8 -> three limb codes
   Big P[kMaxModuli + 1];                   // product of the first L moduli
-  // the one-limb list: 11, then the first 26 greedy moduli
-  std::vector<int> moduli1;
-  ModConst mod1;
-  CrtConst crt1[kMaxModuli + 1];
-  std::vector<uint16_t> lut1;
-  Big P1[kMaxModuli + 1];
+  // the lists with h = 1..kMaxHeads one-limb heads (index h; 0 unused)
+  struct List {
+    std::vector<int> moduli;               // kMaxModuli, heads first
+    ModConst mod;                          // the whole list (encoder)
+    ModConst tail;                         // the two-limb moduli after the heads (residue GEMM)
+    ModConst head;                         // the heads (single-product GEMM)
+    std::vector<uint16_t> lut;             // encoder LUT of the whole list
+    CrtConst crt[kMaxModuli + 1];
+    Big P[kMaxModuli + 1];
+  } lists[kMaxHeads + 1];
   bool ok = false;
 };
 
@@ -262,8 +278,8 @@ inline bool build_crt(const std::vector<int>& moduli, CrtConst* crt, Big* P) {
     for (int l = 0; l < L; ++l) P[L].mul_small((uint32_t)moduli[l]);
     CrtConst& c = crt[L];
     c.L = L;
-    c.nc = crt_chunks(L);
     const int B = kCrtChunkBits;
+    c.nc = P[L].bitlen() <= 3 * B ? 3 : 4;
     if (P[L].bitlen() > c.nc * B) return false;
     double Pd = 0.0;
     for (int q = 0; q < 4; ++q) {
@@ -347,36 +363,45 @@ inline bool build_tables(HostTables& T) {
   }
   if (!build_crt(T.moduli, T.crt, T.P)) return false;
 
-  // the one-limb list: 11 (one limb, its LUT first), then the greedy
-  // moduli with their LUT entries unchanged
-  T.moduli1.assign(1, kOneLimbModulus);
-  T.moduli1.insert(T.moduli1.end(), T.moduli.begin(), T.moduli.begin() + (kMaxModuli - 1));
-  for (size_t l = 1; l < T.moduli1.size(); ++l)   // 11 is prime: coprime unless a multiple
-    if (T.moduli1[l] % kOneLimbModulus == 0) return false;
-  std::memset(&T.mod1, 0, sizeof(T.mod1));
-  T.lut1.clear();
-  const int m1 = kOneLimbModulus;
-  T.mod1.m[0] = m1;
-  T.mod1.ksum[0] = -1;
-  T.mod1.lut_off[0] = 0;
-  T.mod1.inv[0] = 1.0 / (double)m1;
-  T.mod1.md[0] = (double)m1;
-  for (int ri = -m1; ri < 2 * m1; ++ri) {
-    int c0;
-    if (!one_limb_split(((ri % m1) + m1) % m1, m1, &c0)) return false;
-    const int k0 = e2m1_code_of_limb(c0);
-    if (k0 < 0) return false;
-    T.lut1.push_back((uint16_t)k0);   // c1 = 0: code 0
+  // the lists with one-limb heads: the heads' one-limb codes (second limb
+  // 0), the two-limb moduli's canonical splits
+  for (int h = 1; h <= kMaxHeads; ++h) {
+    HostTables::List& Ls = T.lists[h];
+    Ls.moduli = greedy_seeded(std::vector<int>(kOneLimbHeads, kOneLimbHeads + h));
+    if ((int)Ls.moduli.size() != kMaxModuli) return false;
+    std::memset(&Ls.mod, 0, sizeof(ModConst));
+    std::memset(&Ls.tail, 0, sizeof(ModConst));
+    std::memset(&Ls.head, 0, sizeof(ModConst));
+    Ls.lut.clear();
+    int off1 = 0;
+    for (int l = 0; l < kMaxModuli; ++l) {
+      const int m = Ls.moduli[l];
+      ModConst& part = l < h ? Ls.head : Ls.tail;
+      const int pl = l < h ? l : l - h;
+      for (ModConst* mc : {&Ls.mod, &part}) {
+        const int i = mc == &Ls.mod ? l : pl;
+        mc->m[i] = m;
+        mc->ksum[i] = -1;
+        mc->lut_off[i] = off1;
+        mc->inv[i] = 1.0 / (double)m;
+        mc->md[i] = (double)m;
+      }
+      for (int ri = -m; ri < 2 * m; ++ri) {
+        const int cls = ((ri % m) + m) % m;
+        int c0, c1 = 0;
+        if (l < h) {
+          if (!one_limb_split(cls, m, &c0)) return false;
+        } else if (!two_limb_split(cls, m, &c0, &c1)) {
+          return false;
+        }
+        const int k0 = e2m1_code_of_limb(c0), k1 = e2m1_code_of_limb(c1);
+        if (k0 < 0 || k1 < 0) return false;
+        Ls.lut.push_back((uint16_t)(k0 | (k1 << 8)));
+      }
+      off1 += 3 * m;
+    }
+    if (!build_crt(Ls.moduli, Ls.crt, Ls.P)) return false;
   }
-  for (int l = 1; l < kMaxModuli; ++l) {
-    T.mod1.m[l] = T.mod.m[l - 1];
-    T.mod1.ksum[l] = -1;
-    T.mod1.lut_off[l] = 3 * m1 + T.mod.lut_off[l - 1];
-    T.mod1.inv[l] = T.mod.inv[l - 1];
-    T.mod1.md[l] = T.mod.md[l - 1];
-  }
-  T.lut1.insert(T.lut1.end(), T.lut.begin(), T.lut.begin() + T.mod.lut_off[kMaxModuli - 1]);
-  if (!build_crt(T.moduli1, T.crt1, T.P1)) return false;
   T.ok = true;
   return true;
 }

@@ -56,7 +56,7 @@ _SIGNATURES = {
     "ozfp4_plane_count": (_int, [_int, _p, _p]),
     "ozfp4_set_karatsuba": (_int, [_int]),
     "ozfp4_set_max_capacity": (_int, [_int]),
-    "ozfp4_set_one_limb_modulus": (_int, [_int]),
+    "ozfp4_set_one_limb_moduli": (_int, [_int]),
     "ozfp4_plane_layout": (_int, [_i64, _i64, _p, _p, _p]),
     "ozfp4_scales": (_int, [_i64, _i64, _i64, _p, _i64, _p, _i64, _int, _p, _p]),
     "ozfp4_limb_planes": (_int, [_i64, _i64, _i64, _p, _i64, _p, _i64, _int, _p, _p]),
@@ -171,8 +171,8 @@ def ozfp4_set_max_capacity(bits: int) -> int:
     return load().ozfp4_set_max_capacity(bits)
 
 
-def ozfp4_set_one_limb_modulus(enable: bool) -> int:
-    return load().ozfp4_set_one_limb_modulus(1 if enable else 0)
+def ozfp4_set_one_limb_moduli(heads: int) -> int:
+    return load().ozfp4_set_one_limb_moduli(int(heads))
 
 
 def ozfp4_plane_layout(lines: int, k: int) -> tuple[int, int, int]:

@@ -1,12 +1,15 @@
-"""GPU parity of the one-limb moduli list (ozfp4_set_one_limb_modulus:
-11 with one limb, then the greedy moduli) against the oracle
+"""GPU parity of the one-limb moduli lists (ozfp4_set_one_limb_moduli(h):
+the first h of 11, 9, 8, 7, 5 with one limb each, then the greedy rule
+seeded with them; mostly h = 1, 11 then the greedy moduli) against the oracle
 (oracle/one_limb_fp4.py): the scales, the limb planes byte for byte, every
 residue plane (11's from the single-product GEMM, the others from the
 default GEMM), and C bit for bit, on ragged shapes, shapes whose tile grid
 takes the XCD-share mapping of both GEMMs, edge values, the largest k, the
 wide capacity cap, the allocation-free entry point, the FP32 emulation over
 the list, and sampled outputs of m = n = k = 16384 with 18 moduli, whose
-normalized error must stay within 2^-50."""
+normalized error must stay within 2^-50. With 2..5 heads: C bit for bit
+(including lists of heads only), every residue plane, and C equal to the
+greedy 18 / 19 moduli's C where the capacities agree."""
 
 import numpy as np
 import pytest
@@ -22,9 +25,9 @@ SEED = 20261401
 
 @pytest.fixture(autouse=True)
 def one_limb(gpu_lib):
-    assert gpu_lib.ozfp4_set_one_limb_modulus(True) == gpu_lib.OZFP4_OK
+    assert gpu_lib.ozfp4_set_one_limb_moduli(1) == gpu_lib.OZFP4_OK
     yield
-    gpu_lib.ozfp4_set_one_limb_modulus(False)
+    gpu_lib.ozfp4_set_one_limb_moduli(0)
     gpu_lib.ozfp4_set_max_capacity(53)
 
 
@@ -173,7 +176,7 @@ def test_one_limb_too_few_moduli_refused(gpu_lib):
 
 def test_one_limb_off_restores_the_greedy_list(gpu_lib):
     A, B = dgemm_inputs(96, 80, 200, 0.5, SEED + 7)
-    gpu_lib.ozfp4_set_one_limb_modulus(False)
+    gpu_lib.ozfp4_set_one_limb_moduli(0)
     announce("dgemm after the one-limb setting is cleared")
     assert bits_equal(to_np(gpu_lib.dgemm(dev_cm(A), dev_cm(B), 14)), o.dgemm(A, B, 14)["C"])
 
@@ -223,3 +226,67 @@ def test_one_limb_16384_sampled_and_accurate(gpu_lib):
     assert bits_equal(C, want["C"])
     err = o.normalized_errors_block(C[:4, :4], A, B, rows[:4], cols[:4]).max()
     assert err <= 2.0 ** -50
+
+
+@pytest.fixture
+def heads_setting(gpu_lib):
+    yield
+    gpu_lib.ozfp4_set_one_limb_moduli(0)
+
+
+@pytest.mark.parametrize("h,m,n,k,L", [
+    (2, 131, 67, 129, 12), (3, 300, 300, 200, 19), (4, 200, 130, 333, 21),
+    (5, 1000, 200, 300, 21), (5, 33, 97, 64, 4), (5, 64, 64, 500, 5), (5, 256, 256, 1000, 27)])
+def test_heads_dgemm_bit_exact(gpu_lib, heads_setting, h, m, n, k, L):
+    A, B = dgemm_inputs(m, n, k, 0.5, SEED + 20 + h + m)
+    want = o.dgemm_one_limb(A, B, L, heads=h)["C"]
+    announce(f"dgemm with {h} one-limb heads m={m} n={n} k={k} L={L}")
+    assert gpu_lib.ozfp4_set_one_limb_moduli(h) == gpu_lib.OZFP4_OK
+    C = to_np(gpu_lib.dgemm(dev_cm(A), dev_cm(B), L))
+    assert bits_equal(C, want)
+
+
+def test_heads_residues_bit_exact(gpu_lib, heads_setting):
+    m, n, k, L, h = 300, 300, 200, 21, 5
+    A, B = dgemm_inputs(m, n, k, 0.5, SEED + 30)
+    res = o.dgemm_one_limb(A, B, L, heads=h)
+    announce(f"residues with {h} one-limb heads m={m} n={n} k={k} L={L}")
+    assert gpu_lib.ozfp4_set_one_limb_moduli(h) == gpu_lib.OZFP4_OK
+    R = to_np(gpu_lib.residues(dev_cm(A), dev_cm(B), L))
+    for l in range(L):
+        assert np.array_equal(R[l].T.astype(np.int64), res["r"][l]), f"modulus {res['moduli'][l]}"
+
+
+def test_heads_same_c_as_the_greedy_lists(gpu_lib, heads_setting):
+    """At k = 4096 the 21-moduli lists with 5 and 4 heads have the
+    capacities of the greedy 18 (52 / 52) and 19 (53 / 53): the library's C
+    is the same bit for bit, and the oracle's."""
+    m, n, k = 512, 512, 4096
+    A, B = dgemm_inputs(m, n, k, 0.5, SEED + 31)
+    Ad, Bd = dev_cm(A), dev_cm(B)
+    announce("dgemm with 5 / 4 heads and 21 moduli against the greedy 18 / 19")
+    gpu_lib.ozfp4_set_one_limb_moduli(0)     # the greedy lists for the reference
+    g18 = to_np(gpu_lib.dgemm(Ad, Bd, 18))
+    g19 = to_np(gpu_lib.dgemm(Ad, Bd, 19))
+    c18, c19 = gpu_lib.ozfp4_capacity(k, 18), gpu_lib.ozfp4_capacity(k, 19)
+    gpu_lib.ozfp4_set_one_limb_moduli(5)
+    assert gpu_lib.ozfp4_capacity(k, 21) == c18
+    h5 = to_np(gpu_lib.dgemm(Ad, Bd, 21))
+    gpu_lib.ozfp4_set_one_limb_moduli(4)
+    assert gpu_lib.ozfp4_capacity(k, 21) == c19
+    h4 = to_np(gpu_lib.dgemm(Ad, Bd, 21))
+    gpu_lib.ozfp4_set_one_limb_moduli(0)
+    assert bits_equal(h5, g18) and bits_equal(h4, g19)
+    assert not bits_equal(g18, g19)
+    rows, cols = np.arange(0, m, 97), np.arange(0, n, 131)
+    assert bits_equal(h5[np.ix_(rows, cols)], o.dgemm(A, B, 18, rows=rows, cols=cols)["C"])
+
+
+def test_heads_sgemm_bit_exact(gpu_lib, heads_setting):
+    A, B = dgemm_inputs(131, 67, 129, 2.0, SEED + 32)
+    A, B = A.astype(np.float32), B.astype(np.float32)
+    want = o.sgemm_one_limb(A, B, 13, heads=5)["C"]
+    announce("sgemm with 5 one-limb heads, 13 moduli")
+    assert gpu_lib.ozfp4_set_one_limb_moduli(5) == gpu_lib.OZFP4_OK
+    C = to_np(gpu_lib.sgemm(dev_cm(A), dev_cm(B), 13))
+    assert np.array_equal(C.view(np.uint32), want.view(np.uint32))

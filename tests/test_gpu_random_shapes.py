@@ -155,14 +155,15 @@ def test_random_split(gpu_lib, case):
 
 @pytest.mark.parametrize("case", range(N_ONE))
 def test_random_one_limb(gpu_lib, case):
-    """The one-limb moduli list (11 first) at caps 53 and 63."""
+    """The one-limb moduli lists (1..5 heads) at caps 53 and 63."""
     rng = np.random.default_rng([SEED + 5, case])
     m, n, k = _dim(rng), _dim(rng), _dim(rng)
     cmax = 63 if rng.random() < 0.3 else 53
+    h = int(rng.integers(1, 6))
 
     def cap_ok(k_, L_):
         try:
-            o.capacity_bits(k_, o.select_moduli_one_limb(L_), cmax=cmax)
+            o.capacity_bits(k_, o.select_moduli_one_limb(L_, heads=h), cmax=cmax)
             return True
         except ValueError:
             return False
@@ -170,13 +171,14 @@ def test_random_one_limb(gpu_lib, case):
     phi = float(rng.choice([0.0, 0.5, 2.0, 6.0]))
     seed = int(rng.integers(1 << 30))
     A, B = dgemm_inputs(m, n, k, phi, seed)
-    want = oracle_one_limb(A, B, L, cmax=cmax)["C"]
-    announce(f"random one-limb case {case}: m={m} n={n} k={k} L={L} phi={phi} cmax={cmax} seed={seed}")
+    want = oracle_one_limb(A, B, L, cmax=cmax, heads=h)["C"]
+    announce(f"random one-limb case {case}: m={m} n={n} k={k} L={L} heads={h} phi={phi} "
+             f"cmax={cmax} seed={seed}")
     try:
         gpu_lib.ozfp4_set_max_capacity(cmax)
-        gpu_lib.ozfp4_set_one_limb_modulus(True)
+        gpu_lib.ozfp4_set_one_limb_moduli(h)
         C = to_np(gpu_lib.dgemm(dev_cm(A), dev_cm(B), L))
     finally:
-        gpu_lib.ozfp4_set_one_limb_modulus(False)
+        gpu_lib.ozfp4_set_one_limb_moduli(0)
         gpu_lib.ozfp4_set_max_capacity(53)
     assert bits_equal(C, want)

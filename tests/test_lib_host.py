@@ -37,7 +37,7 @@ def test_header_declares_the_boundary():
                      "ozfp4_sum_limb_table", "ozfp4_plane_count", "ozfp4_set_karatsuba",
                      "ozfp4_set_max_capacity", "ozfp4_dgemm_ozi", "ozfp4_ozi_config",
                      "ozfp4_ozi_limb_planes", "ozfp4_ozi_partials", "ozfp4_sgemm",
-                     "ozfp4_sgemm_capacity", "ozfp4_set_one_limb_modulus"):
+                     "ozfp4_sgemm_capacity", "ozfp4_set_one_limb_moduli"):
         assert required in names
 
 
@@ -128,42 +128,48 @@ def test_plane_count_in_both_modes(lib):
     assert ozfp4.ozfp4_plane_count(18)[0] == 36
 
 
-def test_one_limb_list_matches_oracle(lib):
-    """With the one-limb setting the host queries follow the list 11, then
-    the greedy moduli: the list itself, the capacities at every L and cap,
-    the one-limb representatives of 11 (second limb 0) and the unchanged
-    two-limb tables of the others, two planes per modulus; the Karatsuba
-    mode is refused with it."""
+def test_one_limb_lists_match_oracle(lib):
+    """With h = 1..5 one-limb heads the host queries follow the list (the
+    heads, then the greedy rule seeded with them): the list itself, the
+    capacities at every L and cap, the heads' one-limb representatives
+    (second limb 0) and the two-limb tables of the others, two planes per
+    modulus; the Karatsuba mode is refused with heads, and so are 6 heads."""
     try:
-        assert ozfp4.ozfp4_set_one_limb_modulus(True) == ozfp4.OZFP4_OK
-        for L in (2, 18, 19, 27):
-            assert ozfp4.ozfp4_moduli(L) == o.select_moduli_one_limb(L)
-        for cmax in (53, 63):
-            assert ozfp4.ozfp4_set_max_capacity(cmax) == ozfp4.OZFP4_OK
+        for h in range(1, 6):
+            assert ozfp4.ozfp4_set_one_limb_moduli(h) == ozfp4.OZFP4_OK
             for L in range(2, 28):
-                ms = o.select_moduli_one_limb(L)
-                for k in (1, 3, 256, 4096, 16384, 32768, 131072):
-                    try:
-                        want = o.capacity_bits(k, ms, cmax)
-                    except ValueError:
-                        with pytest.raises(ozfp4.OzFP4Error) as ei:
-                            ozfp4.ozfp4_capacity(k, L)
-                        assert ei.value.code == ozfp4.OZFP4_EMODULI
-                        continue
-                    assert ozfp4.ozfp4_capacity(k, L) == want, (k, L, cmax)
-        ozfp4.ozfp4_set_max_capacity(53)
+                assert ozfp4.ozfp4_moduli(L) == o.select_moduli_one_limb(L, heads=h), (h, L)
+            for cmax in (53, 63):
+                assert ozfp4.ozfp4_set_max_capacity(cmax) == ozfp4.OZFP4_OK
+                for L in range(2, 28):
+                    ms = o.select_moduli_one_limb(L, heads=h)
+                    for k in (1, 3, 256, 4096, 16384, 131072):
+                        try:
+                            want = o.capacity_bits(k, ms, cmax)
+                        except ValueError:
+                            with pytest.raises(ozfp4.OzFP4Error) as ei:
+                                ozfp4.ozfp4_capacity(k, L)
+                            assert ei.value.code == ozfp4.OZFP4_EMODULI
+                            continue
+                        assert ozfp4.ozfp4_capacity(k, L) == want, (h, k, L, cmax)
+            ozfp4.ozfp4_set_max_capacity(53)
+            for idx, m in enumerate(o.select_moduli_one_limb(27, heads=h)):
+                got_m, table = ozfp4.ozfp4_two_limb_table(idx)
+                assert got_m == m
+                for r in range(m):
+                    if idx < h:
+                        want = o.e2m1_code(o.one_limb_split(r, m))
+                    else:
+                        c0, c1 = o.two_limb_split(r, m)
+                        want = o.e2m1_code(c0) | (o.e2m1_code(c1) << 4)
+                    assert table[r] == want, (h, m, r)
+            assert ozfp4.ozfp4_plane_count(18) == (36, [-1] * 18)
+        ozfp4.ozfp4_set_one_limb_moduli(1)
         assert ozfp4.ozfp4_capacity(16384, 18) == (50, 50)
-        for idx, m in enumerate(o.select_moduli_one_limb(27)):
-            got_m, table = ozfp4.ozfp4_two_limb_table(idx)
-            assert got_m == m
-            for r in range(m):
-                if idx == 0:
-                    want = o.e2m1_code(o.one_limb_split(r, m))
-                else:
-                    c0, c1 = o.two_limb_split(r, m)
-                    want = o.e2m1_code(c0) | (o.e2m1_code(c1) << 4)
-                assert table[r] == want, (m, r)
-        assert ozfp4.ozfp4_plane_count(18) == (36, [-1] * 18)
+        ozfp4.ozfp4_set_one_limb_moduli(5)
+        assert ozfp4.ozfp4_capacity(16384, 21) == (51, 51)
+        ozfp4.ozfp4_set_one_limb_moduli(4)
+        assert ozfp4.ozfp4_capacity(16384, 21) == (53, 53)
         ozfp4.ozfp4_set_karatsuba(True)
         with pytest.raises(ozfp4.OzFP4Error) as ei:
             ozfp4.ozfp4_plane_count(18)
@@ -171,10 +177,12 @@ def test_one_limb_list_matches_oracle(lib):
         A = (ctypes.c_double * 4)()
         C = (ctypes.c_double * 4)()
         assert lib.ozfp4_dgemm(2, 2, 2, A, 2, A, 2, C, 2, 18) == ozfp4.OZFP4_EINVAL
+        assert ozfp4.ozfp4_set_one_limb_moduli(6) == ozfp4.OZFP4_EINVAL
+        assert ozfp4.ozfp4_set_one_limb_moduli(-1) == ozfp4.OZFP4_EINVAL
     finally:
         ozfp4.ozfp4_set_karatsuba(False)
         ozfp4.ozfp4_set_max_capacity(53)
-        ozfp4.ozfp4_set_one_limb_modulus(False)
+        ozfp4.ozfp4_set_one_limb_moduli(0)
     assert ozfp4.ozfp4_moduli(18) == o.select_moduli(18)
     assert ozfp4.ozfp4_capacity(16384, 18) == (51, 51)
 
@@ -261,13 +269,13 @@ def test_sgemm_capacity_matches_oracle(lib):
         assert ozfp4.ozfp4_sgemm_capacity(16384, 19) == (24, 24)
     finally:
         ozfp4.ozfp4_set_max_capacity(53)
-    # with the one-limb list the FP32 capacities follow its P
+    # with one-limb heads the FP32 capacities follow the list's P
     try:
-        assert ozfp4.ozfp4_set_one_limb_modulus(True) == ozfp4.OZFP4_OK
+        assert ozfp4.ozfp4_set_one_limb_moduli(1) == ozfp4.OZFP4_OK
         for L in range(2, 28):
             for k in (1, 100, 16384, 131072):
                 try:
-                    want = o.capacity_bits_fp32(k, o.select_moduli_one_limb(L))
+                    want = o.capacity_bits_fp32(k, o.select_moduli_one_limb(L, heads=1))
                 except ValueError:
                     with pytest.raises(ozfp4.OzFP4Error):
                         ozfp4.ozfp4_sgemm_capacity(k, L)
@@ -276,7 +284,7 @@ def test_sgemm_capacity_matches_oracle(lib):
         assert ozfp4.sgemm_moduli(16384) == 10
         assert ozfp4.ozfp4_sgemm_capacity(16384, 9) == (22, 21)
     finally:
-        ozfp4.ozfp4_set_one_limb_modulus(False)
+        ozfp4.ozfp4_set_one_limb_moduli(0)
 
 
 @pytest.mark.parametrize("args,code", [
