@@ -508,14 +508,21 @@ def main() -> int:
     Ad, Bd = dev_cm(A, torch), dev_cm(B, torch)
     C = torch.empty_strided((N, N), (1, N), dtype=torch.float64, device="cuda")
 
-    def one_limb(call):
-        """call() with the one-limb moduli list (11 first), then the
-        greedy list again."""
-        ozfp4.ozfp4_set_one_limb_moduli(1)
+    def with_heads(h, call):
+        """call() with the moduli list of h one-limb heads (11, 9, 8, 7, 5
+        first), then the greedy list again."""
+        ozfp4.ozfp4_set_one_limb_moduli(h)
         try:
             return call()
         finally:
             ozfp4.ozfp4_set_one_limb_moduli(0)
+
+    def one_limb(call):
+        return with_heads(1, call)
+
+    # one-limb lists reported beside the headline: (heads, moduli, the greedy
+    # list whose capacities, and hence C, they reproduce at 16384^3)
+    HEAD_LISTS = [(1, 18, None), (5, 21, 18), (4, 21, 19)]
 
     if args.sweep:
         # accuracy on a 128 x 128 output block at full k (all 16384 elements)
@@ -662,7 +669,9 @@ def main() -> int:
                  "native_fp64": lambda: torch.matmul(Ar, Br, out=Cn),
                  "emulation_L19": lambda: ozfp4.dgemm(Ad, Bd, 19, out=C)}
         if not args.no_one_limb:
-            calls["emulation_one_limb_L18"] = lambda: one_limb(lambda: ozfp4.dgemm(Ad, Bd, 18, out=C))
+            for h_, L_, _ in HEAD_LISTS:
+                calls[f"emulation_heads{h_}_L{L_}"] = (
+                    lambda h_=h_, L_=L_: with_heads(h_, lambda: ozfp4.dgemm(Ad, Bd, L_, out=C)))
         rounds = max(5, args.steps)
         times = paired_times(torch, calls, rounds, max(2, args.warmup))
         st = {name: stats(v) for name, v in times.items()}
@@ -699,31 +708,47 @@ def main() -> int:
         torch.cuda.empty_cache()
 
     if not args.no_one_limb:
-        # the one-limb moduli list: 11 (one limb, one FP4 product) and the
-        # first L - 1 greedy moduli, in place of the greedy list's L-th
-        # modulus (four products); reported beside the headline
-        log(f"one-limb moduli list, {L} moduli")
-        oms, ost = time_call(ozfp4, torch, lambda: one_limb(lambda: ozfp4.dgemm(Ad, Bd, L, out=C)),
-                             args.steps, args.warmup)
-        q1 = 4 * (L - 1) - 1 + 1      # the greedy L - 1 (169 without a1 b1), then 11's one product
-        rec = {"moduli": one_limb(lambda: ozfp4.ozfp4_moduli(L)),
-               "capacity_bits": list(one_limb(lambda: ozfp4.ozfp4_capacity(N, L))),
-               "ms": oms, "tflops": 2.0 * N ** 3 / oms / 1e9,
-               "stages_ms": dict(zip(stage_names, ost)),
-               "products_per_element": q1, "headline_products_per_element": Q,
-               "gemm_fp4_tflops": q1 * 2.0 * N ** 3 / ost[3] / 1e9,
-               "speedup_vs_headline": ms / oms}
-        if ref_block is not None:
-            Cb1 = block_of(C, rows, cols, torch)
-            b1, w1 = accuracy_bits(Cb1, ref_block)
-            rec.update({"error_bits": b1, "max_normalized_error": w1, "fp64_accurate": w1 <= 2.0 ** -50,
-                        "vs_rounded_product": elementwise_vs_rounded(Cb1, ref_block)})
-        if "native_fp64" in result:
-            rec["vs_native_fp64"] = result["native_fp64"]["vs_emulation"]["one_limb_L18"] \
-                if L == 18 else None
-        result["one_limb"] = rec
-        log(json.dumps(rec))
-        ozfp4.dgemm(Ad, Bd, L, out=C)
+        # the one-limb moduli lists: h one-limb heads (one FP4 product each)
+        # and the two-limb moduli by the greedy rule seeded with them;
+        # reported beside the headline. Where a list's capacities equal a
+        # greedy list's, its C must equal that list's bit for bit.
+        Cg = {L: C.clone()}
+        lists = {}
+        for h_, L_, same_as in HEAD_LISTS:
+            if same_as is not None and same_as not in Cg:
+                Cg[same_as] = torch.empty_like(C)
+                ozfp4.dgemm(Ad, Bd, same_as, out=Cg[same_as])
+            log(f"one-limb moduli list: {h_} heads, {L_} moduli")
+            oms, ost = with_heads(h_, lambda: time_call(
+                ozfp4, torch, lambda: ozfp4.dgemm(Ad, Bd, L_, out=C), args.steps, args.warmup))
+            mods = with_heads(h_, lambda: ozfp4.ozfp4_moduli(L_))
+            nh = min(h_, L_)
+            # two-limb moduli: four products each, 169 three; heads: one
+            q = sum(3 if x == 169 else 4 for x in mods[nh:]) + nh
+            rec = {"heads": h_, "n_moduli": L_, "moduli": mods,
+                   "capacity_bits": list(with_heads(h_, lambda: ozfp4.ozfp4_capacity(N, L_))),
+                   "ms": oms, "tflops": 2.0 * N ** 3 / oms / 1e9,
+                   "stages_ms": dict(zip(stage_names, ost)),
+                   "limb_products_per_element": q, "headline_products_per_element": Q,
+                   "gemm_fp4_tflops": q * 2.0 * N ** 3 / ost[3] / 1e9,
+                   "speedup_vs_headline": ms / oms}
+            if same_as is not None:
+                rec["c_bitwise_equal_to_greedy"] = {
+                    "n_moduli": same_as,
+                    "equal": bool(torch.equal(C.view(torch.int64), Cg[same_as].view(torch.int64)))}
+            if ref_block is not None:
+                Cb1 = block_of(C, rows, cols, torch)
+                b1, w1 = accuracy_bits(Cb1, ref_block)
+                rec.update({"error_bits": b1, "max_normalized_error": w1,
+                            "fp64_accurate": w1 <= 2.0 ** -50})
+            if "native_fp64" in result:
+                rec["vs_native_fp64"] = result["native_fp64"]["vs_emulation"].get(f"heads{h_}_L{L_}")
+            lists[f"heads{h_}_L{L_}"] = rec
+            log(json.dumps(rec))
+        result["one_limb"] = lists
+        C.copy_(Cg[L])
+        del Cg
+        torch.cuda.empty_cache()
 
     if not args.no_sweep4096:
         # the moduli count of the headline: the smallest count whose output
@@ -754,12 +779,12 @@ def main() -> int:
                                "headline_moduli_is_smallest": (ok == [18])}
         if not args.no_one_limb:
             sw1 = []
-            for L2 in (17, 18):
-                ms2, _ = one_limb(lambda: time_dgemm(ozfp4, torch, A2d, B2d, C2, L2, 10, 2))
+            for h2, L2 in ((1, 17), (1, 18), (5, 20), (5, 21)):
+                ms2, _ = with_heads(h2, lambda: time_dgemm(ozfp4, torch, A2d, B2d, C2, L2, 10, 2))
                 Cb2 = block_of(C2, rows2, rows2, torch)
                 bits2, worst2 = accuracy_bits(Cb2, ref2)
-                sw1.append({"n_moduli": L2,
-                            "capacity_bits": list(one_limb(lambda: ozfp4.ozfp4_capacity(N2, L2))),
+                sw1.append({"heads": h2, "n_moduli": L2,
+                            "capacity_bits": list(with_heads(h2, lambda: ozfp4.ozfp4_capacity(N2, L2))),
                             "ms": ms2, "tflops": 2.0 * N2 ** 3 / ms2 / 1e9,
                             "error_bits": bits2, "max_normalized_error": worst2,
                             "fp64_accurate": worst2 <= 2.0 ** -50})

@@ -391,6 +391,10 @@ int run_dgemm(const DgemmPlan& p, DeviceState* d, const void* Av, int64_t lda, c
   const int64_t nblocks = tiles_m * tiles_n * Lg;
   const int64_t rplane = p.m_pad * p.n_pad;
   if (p.heads) {
+    // the heads first: their short burst of residue writes then lands well
+    // before the CRT reads
+    HIP_TRY(launch_gemm_one_limb(g_stream, pa, pb, R, p.m_pad, rplane, p.plane_a, p.plane_b,
+                                 p.m_pad, p.n_pad, p.kblocks, p.nh, d->lists[p.heads].head));
     if (Lg > 0) {
       hipLaunchKernelGGL(k_gemm_res, dim3((unsigned)nblocks), dim3(kWaves * 64), 0, g_stream,
                          pa + 2 * p.nh * p.plane_a, pb + 2 * p.nh * p.plane_b, R + p.nh * rplane,
@@ -398,8 +402,6 @@ int run_dgemm(const DgemmPlan& p, DeviceState* d, const void* Av, int64_t lda, c
                          rplane, d->lists[p.heads].tail);
       HIP_TRY(hipGetLastError());
     }
-    HIP_TRY(launch_gemm_one_limb(g_stream, pa, pb, R, p.m_pad, rplane, p.plane_a, p.plane_b,
-                                 p.m_pad, p.n_pad, p.kblocks, p.nh, d->lists[p.heads].head));
   } else if (p.kar) {
     HIP_TRY(launch_gemm_res_kar((unsigned)nblocks, g_stream, pa, pb, R, p.plane_a, p.plane_b,
                                 p.kblocks, tiles_m, tiles_n, nblocks, p.m_pad, p.m_pad * p.n_pad,
