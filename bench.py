@@ -874,6 +874,19 @@ def main() -> int:
             rows1.append({"n": N1, "ms": t1, "tflops_total": f1 / t1 / 1e9,
                           "tflops_compute": f1 / (st1[3] + st1[4]) / 1e9,
                           "paper_tflops_compute": comp, "paper_tflops_total": total})
+            if not args.no_one_limb:
+                # the same C from 21 moduli with the one-limb heads 11, 9, 8, 7
+                # (their capacities equal the 19 greedy moduli's at these k)
+                C19 = C1.clone()
+                t4, st4 = with_heads(4, lambda: time_call(
+                    ozfp4, torch, lambda: ozfp4.dgemm(A1d, B1d, 21, out=C1), reps, 2))
+                rows1[-1]["four_heads_21_moduli"] = {
+                    "ms": t4, "tflops_total": f1 / t4 / 1e9,
+                    "tflops_compute": f1 / (st4[3] + st4[4]) / 1e9,
+                    "c_bitwise_equal_to_19_moduli": bool(torch.equal(C1.view(torch.int64),
+                                                                     C19.view(torch.int64)))}
+                C1.copy_(C19)
+                del C19
             log(json.dumps(rows1[-1]))
             if N1 != N:
                 del A1d, B1d, C1
