@@ -1,8 +1,10 @@
 /* A plain C99 client of libozfp4.so, for tests/test_c_abi_client.py: it
  * includes only include/ozfp4.h and the HIP runtime's C API, allocates with
- * hipMalloc, calls ozfp4_dgemm and ozfp4_igemm_s8 on the null stream, and
- * compares C with a CPU triple loop. The inputs are small integers, so both
- * products are exact integers and must agree exactly.
+ * hipMalloc, calls ozfp4_dgemm and ozfp4_igemm_s8 on the null stream, then
+ * ozfp4_dgemm_noalloc (after ozfp4_init) and ozfp4_dgemm with five one-limb
+ * heads and 21 moduli, and compares every C with a CPU triple loop. The
+ * inputs are small integers, so the products are exact integers and must
+ * agree exactly.
  * Prints "OK" and exits 0 on success; prints the first mismatch and exits 1
  * otherwise, 2 on a setup error. */
 #include <hip/hip_runtime_api.h>
@@ -78,6 +80,38 @@ int main(void) {
       fprintf(stderr, "igemm_s8 element %d: %d != %d\n", i, (int)C8[i], (int)W8[i]);
       return 1;
     }
+  }
+  /* the allocation-free entry, then the list with five one-limb heads */
+  if (ozfp4_init() != OZFP4_OK) return setup_failed("ozfp4_init");
+  for (int pass = 0; pass < 2; ++pass) {
+    if (hipMemset(dC, 0, sizeof C) != hipSuccess || hipDeviceSynchronize() != hipSuccess)
+      return setup_failed("hipMemset");
+    if (pass == 0) {
+      rc = ozfp4_dgemm_noalloc(M, N, K, (const double*)dA, M, (const double*)dB, K, (double*)dC, M,
+                               18);
+    } else {
+      if (ozfp4_set_one_limb_moduli(5) != OZFP4_OK) return setup_failed("one-limb setting");
+      rc = ozfp4_dgemm(M, N, K, (const double*)dA, M, (const double*)dB, K, (double*)dC, M, 21);
+      ozfp4_set_one_limb_moduli(0);
+    }
+    if (rc != OZFP4_OK) {
+      fprintf(stderr, "%s: %s\n", pass ? "ozfp4_dgemm, 5 heads" : "ozfp4_dgemm_noalloc",
+              ozfp4_strerror(rc));
+      return 1;
+    }
+    if (hipDeviceSynchronize() != hipSuccess ||
+        hipMemcpy(C, dC, sizeof C, hipMemcpyDeviceToHost) != hipSuccess)
+      return setup_failed("copy back");
+    for (int i = 0; i < M * N; ++i)
+      if (C[i] != W[i]) {
+        fprintf(stderr, "%s element %d: %.17g != %.17g\n",
+                pass ? "dgemm with 5 heads" : "dgemm_noalloc", i, C[i], W[i]);
+        return 1;
+      }
+  }
+  if (ozfp4_set_one_limb_moduli(6) != OZFP4_EINVAL) {
+    fprintf(stderr, "6 one-limb heads were not rejected\n");
+    return 1;
   }
   /* an argument error comes back as a code, with no GPU work */
   if (ozfp4_dgemm(M, N, K, (const double*)dA, M - 1, (const double*)dB, K, (double*)dC, M, 19) !=

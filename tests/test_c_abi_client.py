@@ -44,7 +44,8 @@ def test_c_client_compiles_and_links(tmp_path):
 @pytest.mark.gpu
 def test_c_client_runs(tmp_path):
     exe = _build(tmp_path)
-    print("c_abi_client: dgemm 77x45x300 L=19 and igemm_s8, exact integers", flush=True)
+    print("c_abi_client: dgemm 77x45x300 L=19, igemm_s8, dgemm_noalloc L=18, dgemm with 5 "
+          "one-limb heads L=21, exact integers", flush=True)
     res = subprocess.run([exe], capture_output=True, text=True, timeout=120)
     assert res.returncode == 0, res.stdout + res.stderr
     assert res.stdout.strip() == "OK"
