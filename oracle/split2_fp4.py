@@ -36,7 +36,9 @@ give the correctly rounded product fl(AB).
 Readings (the paper describes only the one-term conversion): d =
 min(c_A, c_B), so both cross terms share one scale and one residue product;
 the three products use the same moduli and capacities as the one-term
-method; the conversion of each term rounds half to even.
+method; the conversion of each term rounds half to even. With one-limb
+heads (``heads`` > 0, see one_limb_fp4) the moduli are that list's and the
+heads take the single limb product.
 """
 
 from __future__ import annotations
@@ -45,6 +47,7 @@ from fractions import Fraction
 
 import numpy as np
 
+from .one_limb_fp4 import residue_products_one_limb, select_moduli_one_limb
 from .ozaki2_fp4 import (capacity_bits, crt_reconstruct, residue_products, round_scaled,
                          select_moduli, shift_exponents)
 
@@ -88,15 +91,22 @@ def split_terms(X: np.ndarray, shifts: np.ndarray, axis: int, d: int):
     return X1.astype(np.int64), X2.astype(np.int64)
 
 
-def _residue_route(Xi: np.ndarray, Yi: np.ndarray, moduli) -> tuple[list, np.ndarray]:
+def _moduli(n_moduli: int, heads: int) -> list[int]:
+    return select_moduli_one_limb(n_moduli, heads) if heads else select_moduli(n_moduli)
+
+
+def _residue_route(Xi: np.ndarray, Yi: np.ndarray, moduli, heads: int = 0) -> tuple[list, np.ndarray]:
     """Residues of Xi Yi for every modulus (the scheme-II residue products of
-    Sec. V-A) and the symmetric CRT reconstruction (Sec. V-B)."""
-    res = [residue_products(Xi, Yi, m)["r"] for m in moduli]
+    Sec. V-A; the single limb product for one-limb heads) and the symmetric
+    CRT reconstruction (Sec. V-B)."""
+    one = set(moduli[:min(heads, len(moduli))])
+    res = [(residue_products_one_limb if m in one else residue_products)(Xi, Yi, m)["r"]
+           for m in moduli]
     return res, crt_reconstruct(res, moduli)
 
 
 def dgemm_split2(A: np.ndarray, B: np.ndarray, n_moduli: int, rows=None, cols=None,
-                 cmax: int = 53) -> dict:
+                 cmax: int = 53, heads: int = 0) -> dict:
     """C = A B by scheme II with the two-term split (see the module text).
 
     Optional `rows` / `cols` restrict the output to a block (shifts still
@@ -109,7 +119,7 @@ def dgemm_split2(A: np.ndarray, B: np.ndarray, n_moduli: int, rows=None, cols=No
     assert B.shape[0] == k
     rows = np.arange(m) if rows is None else np.asarray(rows)
     cols = np.arange(B.shape[1]) if cols is None else np.asarray(cols)
-    moduli = select_moduli(n_moduli)
+    moduli = _moduli(n_moduli, heads)
     cA, cB = capacity_bits(k, moduli, cmax)
     d = split_scale(cA, cB)
     As, Bs = A[rows, :], B[:, cols]
@@ -117,9 +127,9 @@ def dgemm_split2(A: np.ndarray, B: np.ndarray, n_moduli: int, rows=None, cols=No
     t = shift_exponents(Bs, axis=0, c=cB)
     A1, A2 = split_terms(As, s, axis=1, d=d)
     B1, B2 = split_terms(Bs, t, axis=0, d=d)
-    r11, X11 = _residue_route(A1, B1, moduli)
-    r12, X12 = _residue_route(np.hstack([A1, A2]), np.vstack([B2, B1]), moduli)
-    r22, X22 = _residue_route(A2, B2, moduli)
+    r11, X11 = _residue_route(A1, B1, moduli, heads)
+    r12, X12 = _residue_route(np.hstack([A1, A2]), np.vstack([B2, B1]), moduli, heads)
+    r22, X22 = _residue_route(A2, B2, moduli, heads)
     X = np.empty(X11.shape, dtype=object)
     C = np.empty(X11.shape, dtype=np.float64)
     for i in range(X.shape[0]):
@@ -133,7 +143,7 @@ def dgemm_split2(A: np.ndarray, B: np.ndarray, n_moduli: int, rows=None, cols=No
 
 
 def dgemm_split2_definition(A: np.ndarray, B: np.ndarray, n_moduli: int,
-                            cmax: int = 53) -> np.ndarray:
+                            cmax: int = 53, heads: int = 0) -> np.ndarray:
     """The defined result without residues: C_ij = RN(sum_k (A1 + 2^-d A2)_ik
     (B1 + 2^-d B2)_kj 2^-(s_i + t_j)), terms from exact rationals, sums of
     Python ints (tiny inputs)."""
@@ -141,7 +151,7 @@ def dgemm_split2_definition(A: np.ndarray, B: np.ndarray, n_moduli: int,
     B = np.asarray(B, dtype=np.float64)
     m, k = A.shape
     n = B.shape[1]
-    moduli = select_moduli(n_moduli)
+    moduli = _moduli(n_moduli, heads)
     cA, cB = capacity_bits(k, moduli, cmax)
     d = split_scale(cA, cB)
     s = shift_exponents(A, axis=1, c=cA)

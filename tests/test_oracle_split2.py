@@ -18,7 +18,10 @@ wide-range route: each check ties it to something other than itself.
   method's 2^-31..2^-36 to within the final rounding (<= 2^-52).
 * Planted mistakes (a cross term at the wrong scale, the concatenation in
   the wrong order, the second term at the wrong scale, X22 dropped) are each
-  caught by the residue-route pin."""
+  caught by the residue-route pin.
+* With one-limb heads: the same route against its definition over the
+  list, and at k = 32768 the four-head 21-moduli list's C equal bit for bit
+  to the 19 greedy moduli's."""
 
 import math
 from fractions import Fraction
@@ -91,6 +94,41 @@ def test_residue_route_equals_the_expanded_definition(L, cmax, spread, seed):
         assert np.array_equal(res["X11"], A1.dot(B1))
         assert np.array_equal(res["X12"], A1.dot(B2) + A2.dot(B1))
         assert np.array_equal(res["X22"], A2.dot(B2))
+
+
+@pytest.mark.parametrize("h,L,spread,seed", [(1, 12, 60, 11), (5, 21, 200, 12), (4, 21, 40, 13),
+                                          (3, 8, 100, 14)])
+def test_residue_route_with_one_limb_heads(h, L, spread, seed):
+    """With one-limb heads (11, 9, 8, 7, 5 first) the split route equals its
+    expanded definition over that list, and the three reconstructions are
+    the exact integer products."""
+    rng = np.random.default_rng(seed)
+    for _ in range(4):
+        m, n, k = (int(x) for x in rng.integers(1, 6, 3))
+        A, B = _wide(m, k, spread, rng.integers(1 << 30)), _wide(k, n, spread, rng.integers(1 << 30))
+        res = o.dgemm_split2(A, B, L, heads=h)
+        assert res["moduli"] == o.select_moduli_one_limb(L, heads=h)
+        want = o.dgemm_split2_definition(A, B, L, heads=h)
+        assert np.array_equal(res["C"].view(np.int64), want.view(np.int64))
+        A1, A2 = res["A1"].astype(object), res["A2"].astype(object)
+        B1, B2 = res["B1"].astype(object), res["B2"].astype(object)
+        assert np.array_equal(res["X11"], A1.dot(B1))
+        assert np.array_equal(res["X12"], A1.dot(B2) + A2.dot(B1))
+        assert np.array_equal(res["X22"], A2.dot(B2))
+
+
+def test_four_heads_give_the_greedy_19_result_at_k_32768():
+    """At k = 32768 the 21-moduli list with four heads has the capacities of
+    the 19 greedy moduli (53 / 53), so the split route's C is the same bit
+    for bit."""
+    rng = np.random.default_rng(15)
+    k = 32768
+    A = (rng.random((3, k)) - 0.5) * np.exp(4.0 * rng.standard_normal((3, k)))
+    B = (rng.random((k, 2)) - 0.5) * np.exp(4.0 * rng.standard_normal((k, 2)))
+    g = o.dgemm_split2(A, B, 19)
+    h = o.dgemm_split2(A, B, 21, heads=4)
+    assert (g["cA"], g["cB"]) == (h["cA"], h["cB"]) == (53, 53)
+    assert np.array_equal(g["C"].view(np.int64), h["C"].view(np.int64))
 
 
 def test_products_stay_inside_the_crt_range_at_the_capacity_bound():
