@@ -1053,6 +1053,20 @@ def main() -> int:
                      "fp64_accurate": worst4 <= 2.0 ** -50,
                      "vs_rounded_product": elementwise_vs_rounded(C4b, ref4)})
         log(json.dumps(runs[-1]))
+        if not args.no_one_limb:
+            # the same C from 21 moduli with the one-limb heads 11, 9, 8, 7
+            # (the 19 greedy moduli's capacities at k = 32768)
+            C4g = C4.clone()
+            ms5, st5 = with_heads(4, lambda: time_call(
+                ozfp4, torch, lambda: ozfp4.dgemm_split(A4d, B4d, 21, out=C4), 3, 1))
+            runs.append({"route": "two-term split, 4 one-limb heads", "n_moduli": 21,
+                         "max_capacity": 53, "ms": ms5,
+                         "tflops": 2.0 * M4 * M4 * K4 / ms5 / 1e9, "gemm_ms": st5[3],
+                         "products_per_element": 4 * (4 * 17 - 1 + 4),
+                         "c_bitwise_equal_to_19_greedy_moduli": bool(
+                             torch.equal(C4.view(torch.int64), C4g.view(torch.int64)))})
+            log(json.dumps(runs[-1]))
+            del C4g
         result["phi4"] = {"workload": "dgemm m=n=8192, k=32768, phi=4",
                           "block": "64x64 (every 128th row and column)", "runs": runs}
         del A4d, B4d, C4

@@ -113,7 +113,8 @@ int ozfp4_dgemm(int64_t m, int64_t n, int64_t k,
  * exactly, so lines that span fewer than about c_A + d - 53 binades give
  * the correctly rounded product. Four times the residue-GEMM work of
  * ozfp4_dgemm. Same arguments, errors and synchronization as ozfp4_dgemm;
- * ignores the Karatsuba and capacity settings.
+ * ignores the Karatsuba and capacity settings and follows the moduli list
+ * of ozfp4_set_one_limb_moduli.
  */
 int ozfp4_dgemm_split(int64_t m, int64_t n, int64_t k,
                       const double* A, int64_t lda,
@@ -205,9 +206,9 @@ int ozfp4_set_max_capacity(int bits);
 
 /*
  * ozfp4_set_one_limb_moduli -- the moduli list of subsequent scheme-II calls
- * (ozfp4_dgemm, ozfp4_dgemm_noalloc, ozfp4_sgemm and the hooks
- * ozfp4_scales, ozfp4_limb_planes, ozfp4_residues): heads = 0..5 one-limb
- * heads, default 0. An extension of the moduli choice of Sec. V-A: a
+ * (ozfp4_dgemm, ozfp4_dgemm_noalloc, ozfp4_dgemm_split, ozfp4_sgemm and the
+ * hooks ozfp4_scales, ozfp4_limb_planes, ozfp4_residues): heads = 0..5
+ * one-limb heads, default 0. An extension of the moduli choice of Sec. V-A: a
  * one-limb modulus has an element of S in every residue class (11: 0, +-1,
  * +-2, +-3, +-4, and 5 = -6, 6 = 6 mod 11; 9, 8, 7 and 5 likewise), so its
  * residues need one limb (c1 = 0) and its residue product is the single
@@ -224,7 +225,8 @@ int ozfp4_set_max_capacity(int bits);
  * give 24 / 24. Modulus indices 0..min(h, L) - 1 of the planes and residues
  * are the heads (second limb plane all zero). The Karatsuba mode cannot be
  * combined with heads: those FP64 calls return OZFP4_EINVAL.
- * ozfp4_dgemm_split and ozfp4_dgemm_ozi keep their own moduli. The host
+ * ozfp4_dgemm_ozi has no moduli. For ozfp4_dgemm_split at k = 32768,
+ * h = 4 and 21 moduli give the 19 greedy moduli's 53 / 53 and C. The host
  * queries (ozfp4_moduli, ozfp4_capacity, ozfp4_sgemm_capacity,
  * ozfp4_two_limb_table, ozfp4_plane_count) follow the setting. Returns
  * OZFP4_EINVAL for heads outside 0..5. A process-wide setting, like the

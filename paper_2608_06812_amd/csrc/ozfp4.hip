@@ -567,6 +567,7 @@ int finish_with_flag(DeviceState* d, const int* dflag, int nstages) {
 struct SplitPlan {
   int64_t m, n, k;
   int L, cA, cB, d;
+  int heads, nh;             // one-limb heads of the list, and of them among the L moduli
   int64_t m_pad, n_pad, k_pad, kblocks, plane_a, plane_b, rset;
   size_t off_amax_a, off_amax_b, off_flag, off_pa1, off_pa2, off_pb1, off_pb2, off_r, total;
 };
@@ -575,7 +576,10 @@ int make_split_plan(int64_t m, int64_t n, int64_t k, int L, SplitPlan* p) {
   const HostTables* T = tables();
   if (!T) return OZFP4_EHIP;
   p->m = m; p->n = n; p->k = k; p->L = L;
-  if (!capacity_split(T->P[L], k, 53, &p->cA, &p->cB)) return OZFP4_EMODULI;
+  p->heads = g_heads;
+  p->nh = std::min(g_heads, L);
+  if (!capacity_split(p->heads ? T->lists[p->heads].P[L] : T->P[L], k, 53, &p->cA, &p->cB))
+    return OZFP4_EMODULI;
   p->d = std::min(p->cA, p->cB);
   p->m_pad = round_up(m, kTile);
   p->n_pad = round_up(n, kTile);
@@ -614,7 +618,11 @@ int run_split(const SplitPlan& p, DeviceState* d, const double* A, int64_t lda, 
   launch_amax_f64(A, lda, B, ldb, p.m, p.n, p.k, amax_a, amax_b, flag);
   HIP_TRY(hipGetLastError());
   record(d, 1);
-  const int lut_entries = T->mod.lut_off[L - 1] + 3 * T->mod.m[L - 1];
+  // the moduli list: the greedy one, or one with one-limb heads
+  const ModConst& mod = p.heads ? T->lists[p.heads].mod : T->mod;
+  const ModConst* d_mod = p.heads ? d->lists[p.heads].mod : d->d_mod;
+  const uint16_t* d_lut = p.heads ? d->lists[p.heads].lut : d->d_lut;
+  const int lut_entries = mod.lut_off[L - 1] + 3 * mod.m[L - 1];
   const size_t lut_bytes = sizeof(uint16_t) * (size_t)lut_entries;
   const int64_t nfa = (p.m_pad / kFragLines) * p.kblocks;
   const int64_t nfb = (p.n_pad / kFragLines) * p.kblocks;
@@ -622,30 +630,43 @@ int run_split(const SplitPlan& p, DeviceState* d, const double* A, int64_t lda, 
     HIP_TRY(launch_encode_split(term == 1, false, (unsigned)encode_grid(nfa), lut_bytes, g_stream, A,
                                 (int64_t)1, lda, p.m, p.k, amax_a, p.cA,
                                 ws + (term ? p.off_pa2 : p.off_pa1), p.plane_a, nfa, p.kblocks, L,
-                                d->d_mod, d->d_lut, lut_entries, p.d));
+                                d_mod, d_lut, lut_entries, p.d));
   record(d, 2);
   for (int term = 0; term < 2; ++term)
     HIP_TRY(launch_encode_split(term == 1, false, (unsigned)encode_grid(nfb), lut_bytes, g_stream, B,
                                 ldb, (int64_t)1, p.n, p.k, amax_b, p.cB,
                                 ws + (term ? p.off_pb2 : p.off_pb1), p.plane_b, nfb, p.kblocks, L,
-                                d->d_mod, d->d_lut, lut_entries, p.d));
+                                d_mod, d_lut, lut_entries, p.d));
   record(d, 3);
-  // residue sets: A1 B1, A1 B2, A2 B1, A2 B2
+  // residue sets: A1 B1, A1 B2, A2 B1, A2 B2; with heads, the heads by the
+  // single-product GEMM, then the two-limb moduli from their planes on
   const int64_t tiles_m = p.m_pad / kTileM, tiles_n = p.n_pad / kTileN;
-  const int64_t nblocks = tiles_m * tiles_n * L;
+  const int Lg = L - p.nh;
+  const int64_t nblocks = tiles_m * tiles_n * Lg;
+  const int64_t rplane = p.m_pad * p.n_pad;
   const size_t pa[4] = {p.off_pa1, p.off_pa1, p.off_pa2, p.off_pa2};
   const size_t pb[4] = {p.off_pb1, p.off_pb2, p.off_pb1, p.off_pb2};
-  for (int q = 0; q < 4; ++q)
-    hipLaunchKernelGGL(k_gemm_res, dim3((unsigned)nblocks), dim3(kWaves * 64), 0, g_stream,
-                       ws + pa[q], ws + pb[q], ws + p.off_r + (size_t)q * p.rset, p.plane_a,
-                       p.plane_b, p.kblocks, tiles_m, tiles_n, nblocks, p.m_pad,
-                       p.m_pad * p.n_pad, d->d_mod);
+  const ModConst* d_tail = p.heads ? d->lists[p.heads].tail : d->d_mod;
+  for (int q = 0; q < 4; ++q) {
+    uint8_t* Rq = ws + p.off_r + (size_t)q * p.rset;
+    if (p.heads)
+      HIP_TRY(launch_gemm_one_limb(g_stream, ws + pa[q], ws + pb[q], Rq, p.m_pad, rplane,
+                                   p.plane_a, p.plane_b, p.m_pad, p.n_pad, p.kblocks, p.nh,
+                                   d->lists[p.heads].head));
+    if (Lg > 0)
+      hipLaunchKernelGGL(k_gemm_res, dim3((unsigned)nblocks), dim3(kWaves * 64), 0, g_stream,
+                         ws + pa[q] + 2 * p.nh * p.plane_a, ws + pb[q] + 2 * p.nh * p.plane_b,
+                         Rq + p.nh * rplane, p.plane_a, p.plane_b, p.kblocks, tiles_m, tiles_n,
+                         nblocks, p.m_pad, rplane, d_tail);
+  }
   HIP_TRY(hipGetLastError());
   record(d, 4);
   const uint8_t* R = ws + p.off_r;
-  HIP_TRY(launch_crt_split(g_stream, T->crt[L].nc, R, R + p.rset, R + 2 * p.rset, R + 3 * p.rset,
-                           p.m_pad, p.m_pad * p.n_pad, p.m, p.n, amax_a, amax_b, p.cA, p.cB, p.d,
-                           d->d_mod, d->d_crt + L, C, ldc));
+  const int nc = (p.heads ? T->lists[p.heads].crt : T->crt)[L].nc;
+  const CrtConst* crt = (p.heads ? d->lists[p.heads].crt : d->d_crt) + L;
+  HIP_TRY(launch_crt_split(g_stream, nc, R, R + p.rset, R + 2 * p.rset, R + 3 * p.rset,
+                           p.m_pad, rplane, p.m, p.n, amax_a, amax_b, p.cA, p.cB, p.d,
+                           d_mod, crt, C, ldc));
   record(d, 5);
   return OZFP4_OK;
 }

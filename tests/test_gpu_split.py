@@ -149,3 +149,36 @@ def test_split_wide_workload_sampled(gpu_lib):
     err = o.normalized_errors_block(Cb, A, B, rows, cols).max()
     announce(f"split phi=4 sample: {-math.log2(err) if err else float('inf'):.1f} bits")
     assert err <= 2.0 ** -52
+
+
+@pytest.fixture
+def heads_setting(gpu_lib):
+    yield
+    gpu_lib.ozfp4_set_one_limb_moduli(0)
+
+
+@pytest.mark.parametrize("h,m,n,k,L,spread", [
+    (1, 131, 67, 129, 19, 40), (5, 300, 300, 200, 21, 60), (5, 64, 80, 300, 6, 30),
+    (4, 97, 31, 1000, 21, 10), (2, 33, 97, 64, 12, 200)])
+def test_split_with_one_limb_heads_bit_exact(gpu_lib, heads_setting, h, m, n, k, L, spread):
+    A, B = _wide(m, k, spread, SEED + 40 + m), _wide(k, n, spread, SEED + 41 + n)
+    want = o.dgemm_split2(A, B, L, heads=h)["C"]
+    announce(f"dgemm_split with {h} one-limb heads m={m} n={n} k={k} L={L}")
+    assert gpu_lib.ozfp4_set_one_limb_moduli(h) == gpu_lib.OZFP4_OK
+    C = to_np(gpu_lib.dgemm_split(dev_cm(A), dev_cm(B), L))
+    assert bits_equal(C, want)
+
+
+def test_split_four_heads_give_the_greedy_19_result(gpu_lib, heads_setting):
+    """At k = 4096 the 21-moduli list with four heads has the 19 greedy
+    moduli's capacities (53 / 53): the split route's C is the same bit for
+    bit."""
+    A, B = dgemm_inputs(256, 256, 4096, 4.0, SEED + 42)
+    Ad, Bd = dev_cm(A), dev_cm(B)
+    announce("dgemm_split, 19 greedy moduli against 4 heads and 21 moduli")
+    gpu_lib.ozfp4_set_one_limb_moduli(0)
+    g = to_np(gpu_lib.dgemm_split(Ad, Bd, 19))
+    gpu_lib.ozfp4_set_one_limb_moduli(4)
+    h = to_np(gpu_lib.dgemm_split(Ad, Bd, 21))
+    assert bits_equal(g, h)
+    assert bits_equal(g[:4, :4], o.dgemm_split2(A, B, 19, rows=np.arange(4), cols=np.arange(4))["C"])
