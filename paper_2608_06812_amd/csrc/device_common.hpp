@@ -395,98 +395,113 @@ __device__ __forceinline__ void gemm_res_tile(
 #pragma unroll
         for (int v = 0; v < 16; ++v) acc[a][i][j][v] = 0.0f;
 
-  // Per stage s: k fragment 0 (read, 16 MFMAs), k fragment 1 (read, 12
-  // MFMAs), then the stage handover: wait until stage s + 1 has landed and
-  // this wave's reads are done, barrier, and only then the last 4 MFMAs of
-  // stage s, so the matrix pipe still has queued work while the waves
-  // synchronise. Stage s + 2 is copied during stage s into the slot of
-  // stage s - 1, which every wave finished reading before the previous
-  // barrier; its six copies per wave go out in pairs between the MFMAs
-  // rather than in one burst after the barrier, so the data path from L2
-  // into LDS never holds up the matrix pipe of every wave at once. At the
-  // handover only those six copies may still be in flight.
+  // Schedule. The operand registers of a k fragment (a_p, b_p: two
+  // fragments each for planes p = 0, 1) are refilled from LDS for the next
+  // k fragment as soon as their last product group has been issued, so
+  // every LDS read has at least one product group (four MFMAs of this wave,
+  // eight of its SIMD) to land in, and the two waves of a SIMD never wait
+  // for their reads at the same time. With product group g_pq = the four
+  // MFMAs a_p b_q, k fragment 0 of a stage issues g00 g01 g11 g10 and
+  // k fragment 1 issues g01 g00 g10 g11: each fragment's last groups free
+  // the registers that the next fragment's first groups need last.
+  // Modulus 169 has no g11 and issues g10 g00 g01 in both fragments.
+  //
+  // Stage s + 2 is copied during stage s into the slot of stage s - 1,
+  // which every wave finished reading before the previous barrier, one
+  // copy per wave after each product group before the handover. The
+  // handover (this wave's copies of stage s + 1 landed and its reads of
+  // stage s done, then a barrier) comes after the first two groups of
+  // k fragment 1 (first one for 169), so the matrix pipe still has eight
+  // MFMAs of the wave queued while the waves synchronise; the reads of
+  // stage s + 1 start right after it.
+  v4i a[2][2], b[2][2];   // [plane][i] of A, [plane][j] of B
+  auto readA = [&](const uint8_t* sb, int kbl, int p) {
+#pragma unroll
+    for (int i = 0; i < 2; ++i) a[p][i] = *reinterpret_cast<const v4i*>(sb + fragA(p, rbw + i, kbl) + lane16);
+  };
+  auto readB = [&](const uint8_t* sb, int kbl, int p) {
+#pragma unroll
+    for (int j = 0; j < 2; ++j) b[p][j] = *reinterpret_cast<const v4i*>(sb + fragB(p, cbw + j, kbl) + lane16);
+  };
+  // g_pq into acc[p + q]: a0 b0 -> acc0, a0 b1 and a1 b0 -> acc1, a1 b1 -> acc2
+  auto group = [&](int p, int q) {
+#pragma unroll
+    for (int i = 0; i < 2; ++i)
+#pragma unroll
+      for (int j = 0; j < 2; ++j) acc[p + q][i][j] = mfma_fp4(a[p][i], b[q][j], acc[p + q][i][j]);
+  };
+  auto fence = [] { __builtin_amdgcn_sched_barrier(0); };
+  auto handover = [&](bool copy) {
+    if (copy)
+      wait_vm_lgkm0<kDmaPerWave>();   // stage s + 1 landed; reads of stage s done
+    else
+      wait_vm_lgkm0<0>();
+    block_sync();
+  };
+
+  // copy: issue the copies of stage s + 2; next: stage s + 1 exists
+  auto stage = [&](int s, bool copy, bool next) {
+    const uint8_t* sb = lds + (s % kRing) * kStageBytes;
+    const uint8_t* nb = lds + ((s + 1) % kRing) * kStageBytes;
+    auto cp = [&](int j) {
+      if (copy) dma(s + 2, j);
+    };
+    if constexpr (!kSkipA1B1) {
+      group(0, 0); cp(0); fence();
+      group(0, 1); readA(sb, 1, 0); cp(1); fence();
+      group(1, 1); readB(sb, 1, 1); cp(2); fence();
+      group(1, 0); readA(sb, 1, 1); readB(sb, 1, 0); cp(3); fence();
+      group(0, 1); cp(4); fence();
+      group(0, 0); cp(5); fence();
+      if (next) {
+        handover(copy);
+        readA(nb, 0, 0); fence();
+        group(1, 0); readB(nb, 0, 0); fence();
+        group(1, 1); readA(nb, 0, 1); readB(nb, 0, 1); fence();
+      } else {
+        group(1, 0); group(1, 1); fence();
+      }
+    } else {
+      group(1, 0); readA(sb, 1, 1); cp(0); cp(1); fence();
+      group(0, 0); readB(sb, 1, 0); cp(2); cp(3); fence();
+      group(0, 1); readA(sb, 1, 0); readB(sb, 1, 1); cp(4); fence();
+      group(1, 0); cp(5); fence();
+      if (next) {
+        handover(copy);
+        readA(nb, 0, 1); fence();
+        group(0, 0); readB(nb, 0, 0); fence();
+        group(0, 1); readA(nb, 0, 0); readB(nb, 0, 1); fence();
+      } else {
+        group(0, 0); group(0, 1); fence();
+      }
+    }
+  };
+
 #pragma unroll
   for (int j = 0; j < kDmaPerWave; ++j) dma(0, j);
 #pragma unroll
   for (int j = 0; j < kDmaPerWave; ++j) dma(1, j);   // nst >= 2 by padding
   wait_vm_lgkm0<kDmaPerWave>();   // stage 0 landed
   block_sync();
-
-  v4i a[2][2], b[2][2];   // [plane][i] of A, [plane][j] of B
-  auto read_frags = [&](const uint8_t* sb, int kbl) {
-#pragma unroll
-    for (int p = 0; p < 2; ++p)
-#pragma unroll
-      for (int i = 0; i < 2; ++i) {
-        a[p][i] = *reinterpret_cast<const v4i*>(sb + fragA(p, rbw + i, kbl) + lane16);
-        b[p][i] = *reinterpret_cast<const v4i*>(sb + fragB(p, cbw + i, kbl) + lane16);
-      }
-  };
-  // every product except a1 b1 (acc2), which is issued after the handover
-  // of the stage's second k fragment
-  auto mfma_head = [&]() {
-#pragma unroll
-    for (int i = 0; i < 2; ++i)
-#pragma unroll
-      for (int j = 0; j < 2; ++j) {
-        acc[0][i][j] = mfma_fp4(a[0][i], b[0][j], acc[0][i][j]);
-        acc[1][i][j] = mfma_fp4(a[0][i], b[1][j], acc[1][i][j]);
-      }
-#pragma unroll
-    for (int i = 0; i < 2; ++i)
-#pragma unroll
-      for (int j = 0; j < 2; ++j) acc[1][i][j] = mfma_fp4(a[1][i], b[0][j], acc[1][i][j]);
-  };
-  auto mfma_tail = [&]() {
-    if constexpr (!kSkipA1B1) {
-#pragma unroll
-      for (int i = 0; i < 2; ++i)
-#pragma unroll
-        for (int j = 0; j < 2; ++j) acc[2][i][j] = mfma_fp4(a[1][i], b[1][j], acc[2][i][j]);
-    }
-  };
-  // everything of stage s before the handover; with `copy`, the copies of
-  // stage s + 2 interleaved
-  auto stage_body = [&](int s, bool copy) {
-    const uint8_t* sb = lds + (s % kRing) * kStageBytes;
-    read_frags(sb, 0);
-    mfma_head();
-    if (copy) {
-      dma(s + 2, 0);
-      dma(s + 2, 1);
-    }
-    __builtin_amdgcn_sched_barrier(0);
-    mfma_tail();
-    __builtin_amdgcn_sched_barrier(0);
-    read_frags(sb, 1);
-    if (copy) {
-      dma(s + 2, 2);
-      dma(s + 2, 3);
-    }
-    mfma_head();
-    if (copy) {
-      dma(s + 2, 4);
-      dma(s + 2, 5);
-    }
-    __builtin_amdgcn_sched_barrier(0);
-  };
+  // k fragment 0 of stage 0, in the order in which a stage reads the next
+  // stage's (so the waits at the top of the loop are the same on entry)
+  if constexpr (!kSkipA1B1) {
+    readA(lds, 0, 0);
+    readB(lds, 0, 0);
+    readA(lds, 0, 1);
+    readB(lds, 0, 1);
+  } else {
+    readA(lds, 0, 1);
+    readB(lds, 0, 0);
+    readA(lds, 0, 0);
+    readB(lds, 0, 1);
+  }
+  fence();
 
   int s = 0;
-  for (; s + 2 < nst; ++s) {       // steady state: stage s + 2 exists
-    stage_body(s, true);
-    wait_vm_lgkm0<kDmaPerWave>();  // stage s + 1 landed; reads of stage s done
-    block_sync();
-    mfma_tail();
-    __builtin_amdgcn_sched_barrier(0);
-  }
-  // the last two stages
-  stage_body(s, false);
-  wait_vm_lgkm0<0>();
-  block_sync();
-  mfma_tail();
-  __builtin_amdgcn_sched_barrier(0);
-  stage_body(s + 1, false);
-  mfma_tail();
+  for (; s + 2 < nst; ++s) stage(s, true, true);   // steady state: stage s + 2 exists
+  stage(s, false, true);
+  stage(s + 1, false, false);
 
   store_residues<4, 52, 676>(acc, l, tm, tn, wm, wn, lane, R, ldr, rplane, mc);
 }

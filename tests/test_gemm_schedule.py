@@ -94,6 +94,26 @@ def _largest_read_batch(loop):
     return max(best, n)
 
 
+def _min_read_cover(loop):
+    """Fewest MFMAs the wave issues between an LDS read and the first wait
+    that needs it done, going round the loop twice (the first pass only
+    fills the queue of outstanding reads, which complete in order)."""
+    pending, n_mfma, best = [], 0, None
+    for lap in range(2):
+        for x in loop:
+            if x.startswith("ds_read"):
+                pending.append(n_mfma)
+            elif x.startswith("v_mfma"):
+                n_mfma += 1
+            elif x.startswith("s_waitcnt"):
+                m = re.search(r"lgkmcnt\((\d+)\)", x)
+                while m and len(pending) > int(m.group(1)):
+                    cover = n_mfma - pending.pop(0)
+                    if lap == 1:
+                        best = cover if best is None else min(best, cover)
+    return best
+
+
 def test_no_kernel_spills(asm):
     for tu, text in asm.items():
         sizes = re.findall(r"\.set\s+(\S+)\.private_seg_size,\s*(\d+)", text)
@@ -135,3 +155,16 @@ def test_no_scaled_mfma_anywhere(asm):
         assert _count(body, r"^v_mfma_scale|^v_mfma_ld_scale") == 0, tu
         if tu not in ("sgemm.hip", "split.hip"):   # these reuse the default GEMM
             assert _count(body, r"^v_mfma_f32_32x32x64_f8f6f4 ") > 0, tu
+
+
+@pytest.mark.parametrize("mfma", [32, 24])   # two-limb moduli; 169 without a1 b1
+def test_residue_gemm_reads_land_under_mfmas(asm, mfma):
+    """The residue GEMM refills each operand register from LDS as soon as its
+    last product group has been issued: every LDS read of the steady loop
+    has at least four MFMAs of the wave between its issue and the wait for
+    it, so the two waves of a SIMD do not stall on their reads together."""
+    body = _function(asm["ozfp4.hip"], "_ZN5ozfp410k_gemm_res")
+    loops = [l for l in _loops(body) if _count(l, r"v_mfma") == mfma]
+    assert loops, f"no loop with {mfma} MFMAs"
+    cover = _min_read_cover(loops[0])
+    assert cover is not None and cover >= 4, cover
