@@ -23,7 +23,7 @@ SOURCES = [os.path.join(HERE, "csrc", n)
 HEADERS = [os.path.join(HERE, "csrc", n) for n in
            ("device_common.hpp", "kernels.hpp", "karatsuba.hpp", "crt_round.hpp", "tables.hpp",
             "ozaki1.hpp", "ozi_round.hpp", "sgemm.hpp", "crt_round_f32.hpp",
-            "calibrate.hpp", "split.hpp", "crt_split.hpp", "onelimb.hpp", "plain_gemm.hpp")] + \
+            "calibrate.hpp", "split.hpp", "crt_split.hpp", "onelimb.hpp", "plain_gemm.hpp", "limb3_sched.hpp")] + \
           [os.path.join(ROOT, "include", "ozfp4.h")]
 
 # -packed-fp32-ops: keep the compiler from emitting packed FP32 arithmetic.

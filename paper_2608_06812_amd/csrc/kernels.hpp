@@ -6,6 +6,7 @@
 #pragma once
 
 #include "device_common.hpp"
+#include "limb3_sched.hpp"
 
 namespace ozfp4 {
 
@@ -210,57 +211,39 @@ __global__ __launch_bounds__(512, 1) void k_gemm_s8(
 #pragma unroll
     for (int v = 0; v < 16; ++v) out[i][v] = 0u;
   v4i a[3][2], b[3];
-  auto read_frags = [&](const uint8_t* sb, int kbl) {
+  // the operands of one k fragment; schedule of a stage in limb3_sched.hpp
+  auto group = [&](int p, int q) {
 #pragma unroll
-    for (int p = 0; p < 3; ++p) {
-#pragma unroll
-      for (int i = 0; i < 2; ++i) a[p][i] = *reinterpret_cast<const v4i*>(sb + fragA8(p, rbw + i, kbl) + lane16);
-      b[p] = *reinterpret_cast<const v4i*>(sb + fragB8(p, wn, kbl) + lane16);
-    }
+    for (int i = 0; i < 2; ++i) acc[p + q][i] = mfma_fp4(a[p][i], b[q], acc[p + q][i]);
   };
-  // the products with i + j <= 2 (12 MFMAs); those with i + j >= 3 (6 MFMAs)
-  // form the tail, which follows the stage handover
-  auto mfma_head = [&]() {
-#pragma unroll
-    for (int i = 0; i < 2; ++i) {
-      acc[0][i] = mfma_fp4(a[0][i], b[0], acc[0][i]);
-      acc[1][i] = mfma_fp4(a[0][i], b[1], acc[1][i]);
-      acc[1][i] = mfma_fp4(a[1][i], b[0], acc[1][i]);
-      acc[2][i] = mfma_fp4(a[0][i], b[2], acc[2][i]);
-      acc[2][i] = mfma_fp4(a[1][i], b[1], acc[2][i]);
-      acc[2][i] = mfma_fp4(a[2][i], b[0], acc[2][i]);
-    }
+  auto handover = [&](bool copy) {
+    if (copy)
+      wait_vm_lgkm0<kDmaPerWave>();   // stage s + 1 landed; reads of stage s done
+    else
+      wait_vm_lgkm0<0>();
+    block_sync();
   };
-  auto mfma_tail = [&]() {
-#pragma unroll
-    for (int i = 0; i < 2; ++i) {
-      acc[3][i] = mfma_fp4(a[1][i], b[2], acc[3][i]);
-      acc[3][i] = mfma_fp4(a[2][i], b[1], acc[3][i]);
-      acc[4][i] = mfma_fp4(a[2][i], b[2], acc[4][i]);
-    }
-  };
-  auto stage_body = [&](int s, bool copy) {   // with the copies of stage s + 2
+  // stage s; copy: with the copies of stage s + 2; next: stage s + 1 exists
+  auto stage = [&](int s, bool copy, bool next) {
     const uint8_t* sb = lds + (s % kRing) * kStageBytes;
-    read_frags(sb, 0);
-    mfma_head();
-    if (copy) {
-      dma(s + 2, 0);
-      dma(s + 2, 1);
-    }
-    __builtin_amdgcn_sched_barrier(0);
-    mfma_tail();
-    __builtin_amdgcn_sched_barrier(0);
-    read_frags(sb, 1);
-    if (copy) {
-      dma(s + 2, 2);
-      dma(s + 2, 3);
-    }
-    mfma_head();
-    if (copy) {
-      dma(s + 2, 4);
-      dma(s + 2, 5);
-    }
-    __builtin_amdgcn_sched_barrier(0);
+    const uint8_t* nb = lds + ((s + 1) % kRing) * kStageBytes;
+    limb3_stage(
+        next, group,
+        [&](int half, bool is_b, int p) {
+          const uint8_t* base = half ? sb : nb;
+          const int kbl = half;
+          if (is_b) {
+            b[p] = *reinterpret_cast<const v4i*>(base + fragB8(p, wn, kbl) + lane16);
+          } else {
+#pragma unroll
+            for (int i = 0; i < 2; ++i)
+              a[p][i] = *reinterpret_cast<const v4i*>(base + fragA8(p, rbw + i, kbl) + lane16);
+          }
+        },
+        [&](int j) {
+          if (copy) dma(s + 2, j);
+        },
+        [&] { handover(copy); });
   };
 
   const int nch = (nst + kChunkS8Stages - 1) / kChunkS8Stages;
@@ -284,21 +267,19 @@ __global__ __launch_bounds__(512, 1) void k_gemm_s8(
     wait_vm_lgkm0<kDmaPerWave>();   // stage 0 landed
     block_sync();
 
+    limb3_first_reads([&](int, bool is_b, int p) {
+      if (is_b) {
+        b[p] = *reinterpret_cast<const v4i*>(lds + fragB8(p, wn, 0) + lane16);
+      } else {
+#pragma unroll
+        for (int i = 0; i < 2; ++i)
+          a[p][i] = *reinterpret_cast<const v4i*>(lds + fragA8(p, rbw + i, 0) + lane16);
+      }
+    });
     int s = 0;
-    for (; s + 2 < len; ++s) {
-      stage_body(s, true);
-      wait_vm_lgkm0<kDmaPerWave>();  // stage s + 1 landed; reads of stage s done
-      block_sync();
-      mfma_tail();
-      __builtin_amdgcn_sched_barrier(0);
-    }
-    stage_body(s, false);
-    wait_vm_lgkm0<0>();
-    block_sync();
-    mfma_tail();
-    __builtin_amdgcn_sched_barrier(0);
-    stage_body(s + 1, false);
-    mfma_tail();
+    for (; s + 2 < len; ++s) stage(s, true, true);   // stage s + 2 exists
+    stage(s, false, true);
+    stage(s + 1, false, false);
 
     // add this chunk's sum_g 13^g 4 G_g into the wrapping outputs (each
     // 4 G_g exact below 2^24)

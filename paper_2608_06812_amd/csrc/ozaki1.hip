@@ -16,6 +16,7 @@
 #include <hip/hip_runtime.h>
 
 #include "device_common.hpp"
+#include "limb3_sched.hpp"
 #include "ozaki1.hpp"
 #include "ozi_round.hpp"
 
@@ -188,58 +189,39 @@ __global__ __launch_bounds__(512, 1) void k_gemm_ozi(
 
   v16f acc[5][2];
   v4i a[3][2], b[3];
-  auto read_frags = [&](const uint8_t* sb, int kbl) {
+  // the operands of one k fragment; schedule of a stage in limb3_sched.hpp
+  auto group = [&](int p, int q) {
 #pragma unroll
-    for (int p = 0; p < 3; ++p) {
+    for (int i = 0; i < 2; ++i) acc[p + q][i] = mfma_fp4(a[p][i], b[q], acc[p + q][i]);
+  };
+  auto read = [&](const uint8_t* base, int kbl, bool is_b, int p) {
+    if (is_b) {
+      b[p] = *reinterpret_cast<const v4i*>(base + fragBo(p, wn, kbl) + lane16);
+    } else {
 #pragma unroll
-      for (int i = 0; i < 2; ++i) a[p][i] = *reinterpret_cast<const v4i*>(sb + fragAo(p, rbw + i, kbl) + lane16);
-      b[p] = *reinterpret_cast<const v4i*>(sb + fragBo(p, wn, kbl) + lane16);
+      for (int i = 0; i < 2; ++i)
+        a[p][i] = *reinterpret_cast<const v4i*>(base + fragAo(p, rbw + i, kbl) + lane16);
     }
   };
-  auto mfma_head = [&]() {
-#pragma unroll
-    for (int i = 0; i < 2; ++i) {
-      acc[0][i] = mfma_fp4(a[0][i], b[0], acc[0][i]);
-      acc[1][i] = mfma_fp4(a[0][i], b[1], acc[1][i]);
-      acc[1][i] = mfma_fp4(a[1][i], b[0], acc[1][i]);
-      acc[2][i] = mfma_fp4(a[0][i], b[2], acc[2][i]);
-      acc[2][i] = mfma_fp4(a[1][i], b[1], acc[2][i]);
-      acc[2][i] = mfma_fp4(a[2][i], b[0], acc[2][i]);
-    }
-  };
-  auto mfma_tail = [&]() {
-#pragma unroll
-    for (int i = 0; i < 2; ++i) {
-      acc[3][i] = mfma_fp4(a[1][i], b[2], acc[3][i]);
-      acc[3][i] = mfma_fp4(a[2][i], b[1], acc[3][i]);
-      acc[4][i] = mfma_fp4(a[2][i], b[2], acc[4][i]);
-    }
-  };
-  // stage s; with `copy`, the copies of stage s + 2 (at offset off) are
-  // interleaved
-  auto stage_body = [&](int s, bool copy, int64_t off) {
+  // stage s; copy: with the copies of stage s + 2 (at offset off); next:
+  // stage s + 1 exists
+  auto stage = [&](int s, bool copy, bool next, int64_t off) {
     const uint8_t* sb = lds + (s % kRing) * kStageBytes;
+    const uint8_t* nb = lds + ((s + 1) % kRing) * kStageBytes;
     const int slot2 = (s + 2) % kRing;
-    read_frags(sb, 0);
-    mfma_head();
-    if (copy) {
-      dma(slot2, off, 0);
-      dma(slot2, off, 1);
-    }
-    __builtin_amdgcn_sched_barrier(0);
-    mfma_tail();
-    __builtin_amdgcn_sched_barrier(0);
-    read_frags(sb, 1);
-    if (copy) {
-      dma(slot2, off, 2);
-      dma(slot2, off, 3);
-    }
-    mfma_head();
-    if (copy) {
-      dma(slot2, off, 4);
-      dma(slot2, off, 5);
-    }
-    __builtin_amdgcn_sched_barrier(0);
+    limb3_stage(
+        next, group,
+        [&](int half, bool is_b, int p) { read(half ? sb : nb, half, is_b, p); },
+        [&](int j) {
+          if (copy) dma(slot2, off, j);
+        },
+        [&] {
+          if (copy)
+            wait_vm_lgkm0<kDmaPerWave>();   // stage s + 1 landed; reads of stage s done
+          else
+            wait_vm_lgkm0<0>();
+          block_sync();
+        });
   };
 
   int64_t* Hh = H + (int64_t)h * hplane;
@@ -282,21 +264,12 @@ __global__ __launch_bounds__(512, 1) void k_gemm_ozi(
     wait_vm_lgkm0<kDmaPerWave>();   // stage 0 landed
     block_sync();
 
+    limb3_first_reads([&](int, bool is_b, int p) { read(lds, 0, is_b, p); });
     int s = 0;
-    for (; s + 2 < total; ++s) {
-      stage_body(s, true, next_off());   // copies stage s + 2 into the slot of stage s - 1
-      wait_vm_lgkm0<kDmaPerWave>();  // stage s + 1 landed; reads of stage s done
-      block_sync();
-      mfma_tail();
-      __builtin_amdgcn_sched_barrier(0);
-    }
-    stage_body(s, false, 0);
-    wait_vm_lgkm0<0>();
-    block_sync();
-    mfma_tail();
-    __builtin_amdgcn_sched_barrier(0);
-    stage_body(s + 1, false, 0);
-    mfma_tail();
+    for (; s + 2 < total; ++s)
+      stage(s, true, true, next_off());   // copies stage s + 2 into the slot of stage s - 1
+    stage(s, false, true, 0);
+    stage(s + 1, false, false, 0);
     // keeps every MFMA ahead of the flush instead of sunk into its branches
 #pragma unroll
     for (int e = 0; e < 5; ++e)

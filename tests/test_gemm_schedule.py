@@ -157,13 +157,18 @@ def test_no_scaled_mfma_anywhere(asm):
             assert _count(body, r"^v_mfma_f32_32x32x64_f8f6f4 ") > 0, tu
 
 
-@pytest.mark.parametrize("mfma", [32, 24])   # two-limb moduli; 169 without a1 b1
-def test_residue_gemm_reads_land_under_mfmas(asm, mfma):
-    """The residue GEMM refills each operand register from LDS as soon as its
-    last product group has been issued: every LDS read of the steady loop
-    has at least four MFMAs of the wave between its issue and the wait for
-    it, so the two waves of a SIMD do not stall on their reads together."""
-    body = _function(asm["ozfp4.hip"], "_ZN5ozfp410k_gemm_res")
+@pytest.mark.parametrize("tu,prefix,mfma", [
+    ("ozfp4.hip", "_ZN5ozfp410k_gemm_res", 32),   # two-limb moduli
+    ("ozfp4.hip", "_ZN5ozfp410k_gemm_res", 24),   # 169, without a1 b1
+    ("ozfp4.hip", "_ZN5ozfp49k_gemm_s8", 36),     # three limbs (limb3_sched.hpp)
+    ("ozaki1.hip", "_ZN5ozfp410k_gemm_ozi", 36),  # three limbs (limb3_sched.hpp)
+])
+def test_gemm_reads_land_under_mfmas(asm, tu, prefix, mfma):
+    """The GEMMs refill each operand register from LDS as soon as its last
+    product group has been issued: every LDS read of the steady loop has at
+    least four MFMAs of the wave between its issue and the wait for it, so
+    the two waves of a SIMD do not stall on their reads together."""
+    body = _function(asm[tu], prefix)
     loops = [l for l in _loops(body) if _count(l, r"v_mfma") == mfma]
     assert loops, f"no loop with {mfma} MFMAs"
     cover = _min_read_cover(loops[0])
