@@ -934,15 +934,27 @@ def main() -> int:
         one32 = None
         if not args.no_one_limb:
             # the one-limb list (11 first): the same 24-bit capacities with
-            # 4 (L - 1) - 1 + 1 products; then the emulation with both lists
-            # and native FP32 timed alike, alternating
+            # 4 (L - 1) - 1 + 1 products; then the emulation with the three
+            # lists and native FP32 timed alike, alternating
             L1 = one_limb(lambda: ozfp4.sgemm_moduli(N))
             oms32, ost32 = one_limb(lambda: time_call(
                 ozfp4, torch, lambda: ozfp4.sgemm(A32d, B32d, L1, out=C32), max(3, args.steps // 2), 1))
             obits32, oworst32 = accuracy_bits(block_of(C32, rows32, rows32, torch).astype(np.float64),
                                               ref32)
+            # three heads: the fewest limb products that reach the 24-bit
+            # capacities at this k (11 moduli, 34 products)
+            L3 = with_heads(3, lambda: ozfp4.sgemm_moduli(N))
+            cap3 = list(with_heads(3, lambda: ozfp4.ozfp4_sgemm_capacity(N, L3)))
+            C32g = torch.empty_like(C32)
+            ozfp4.sgemm(A32d, B32d, L32, out=C32g)
+            with_heads(3, lambda: ozfp4.sgemm(A32d, B32d, L3, out=C32))
+            torch.cuda.synchronize()
+            same3 = bool(torch.equal(C32.view(torch.int32), C32g.view(torch.int32)))
+            del C32g
             calls32 = {"emulation": lambda: ozfp4.sgemm(A32d, B32d, L32, out=C32),
                        "emulation_one_limb": lambda: one_limb(lambda: ozfp4.sgemm(A32d, B32d, L1, out=C32)),
+                       "emulation_three_heads": lambda: with_heads(
+                           3, lambda: ozfp4.sgemm(A32d, B32d, L3, out=C32)),
                        "native_fp32": lambda: torch.matmul(Ar32, Br32, out=Cn32)}
             t32 = {k: stats(v) for k, v in paired_times(torch, calls32, max(5, args.steps // 2), 1).items()}
             one32 = {"n_moduli": L1, "capacity_bits": list(one_limb(lambda: ozfp4.ozfp4_sgemm_capacity(N, L1))),
@@ -950,10 +962,15 @@ def main() -> int:
                      "stages_ms": dict(zip(stage_names, ost32)),
                      "products_per_element": 4 * (L1 - 1), "error_bits": obits32,
                      "max_normalized_error": oworst32,
+                     "three_heads": {"n_moduli": L3, "capacity_bits": cap3,
+                                     "products_per_element": 4 * L3 - 3 * 3 - 1,
+                                     "c_bitwise_equal_to_greedy": same3},
                      "paired": {"protocol": "each call alone between synchronisations, HIP events, "
-                                            "the three alternating", "ms": t32,
+                                            "the four alternating", "ms": t32,
                                 "one_limb_vs_native_fp32": t32["native_fp32"]["median"] /
                                 t32["emulation_one_limb"]["median"],
+                                "three_heads_vs_native_fp32": t32["native_fp32"]["median"] /
+                                t32["emulation_three_heads"]["median"],
                                 "greedy_vs_native_fp32": t32["native_fp32"]["median"] /
                                 t32["emulation"]["median"]}}
         result["sgemm"] = {

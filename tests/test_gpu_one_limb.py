@@ -290,3 +290,25 @@ def test_heads_sgemm_bit_exact(gpu_lib, heads_setting):
     assert gpu_lib.ozfp4_set_one_limb_moduli(5) == gpu_lib.OZFP4_OK
     C = to_np(gpu_lib.sgemm(dev_cm(A), dev_cm(B), 13))
     assert np.array_equal(C.view(np.uint32), want.view(np.uint32))
+
+
+def test_three_heads_sgemm_same_c_as_greedy(gpu_lib, heads_setting):
+    """Three heads with 11 moduli reach the FP32 emulation's 24-bit
+    capacities like the 10 greedy moduli, so C is the greedy list's bit for
+    bit (34 limb products instead of 39), over several tiles with ragged
+    tails; both equal the oracle's."""
+    m, n, k = 300, 260, 700
+    A, B = dgemm_inputs(m, n, k, 2.0, SEED + 33)
+    A, B = A.astype(np.float32), B.astype(np.float32)
+    Ad, Bd = dev_cm(A), dev_cm(B)
+    gpu_lib.ozfp4_set_one_limb_moduli(0)
+    assert gpu_lib.ozfp4_sgemm_capacity(k, 10) == (24, 24)
+    announce("sgemm, 10 greedy moduli, then 3 one-limb heads with 11 moduli")
+    greedy = to_np(gpu_lib.sgemm(Ad, Bd, 10))
+    assert gpu_lib.ozfp4_set_one_limb_moduli(3) == gpu_lib.OZFP4_OK
+    assert gpu_lib.ozfp4_sgemm_capacity(k, 11) == (24, 24)
+    heads = to_np(gpu_lib.sgemm(Ad, Bd, 11))
+    want = o.sgemm_one_limb(A, B, 11, heads=3)["C"]
+    assert np.array_equal(heads.view(np.uint32), want.view(np.uint32))
+    assert np.array_equal(greedy.view(np.uint32), heads.view(np.uint32))
+

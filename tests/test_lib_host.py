@@ -287,6 +287,28 @@ def test_sgemm_capacity_matches_oracle(lib):
         ozfp4.ozfp4_set_one_limb_moduli(0)
 
 
+def test_sgemm_fewest_products_with_three_heads(lib):
+    """At k = 16384 the FP32 emulation reaches its 24-bit capacities with
+    10 greedy moduli (39 limb products), 10 moduli with one one-limb head
+    (36), and 11 with three heads (34): the fewest over 0..5 heads, as the
+    oracle's lists give."""
+    def products(L, h):
+        ms = o.select_moduli_one_limb(L, heads=h) if h else o.select_moduli(L)
+        return sum(1 if i < h else (3 if q == 169 else 4) for i, q in enumerate(ms))
+    best = {}
+    try:
+        for h in range(6):
+            assert ozfp4.ozfp4_set_one_limb_moduli(h) == ozfp4.OZFP4_OK
+            L = ozfp4.sgemm_moduli(16384)
+            assert ozfp4.ozfp4_sgemm_capacity(16384, L) == (24, 24)
+            want = o.select_moduli_one_limb(L, heads=h) if h else o.select_moduli(L)
+            assert o.capacity_bits_fp32(16384, want) == (24, 24)
+            best[h] = (L, products(L, h))
+    finally:
+        ozfp4.ozfp4_set_one_limb_moduli(0)
+    assert best == {0: (10, 39), 1: (10, 36), 2: (11, 37), 3: (11, 34), 4: (12, 35), 5: (13, 36)}
+
+
 @pytest.mark.parametrize("args,code", [
     ((4, 4, 4, 1, 3, 1, 4, 1, 4, 10), ozfp4.OZFP4_EINVAL),           # lda < m
     ((4, 4, 4, 1, 4, 1, 4, 1, 3, 10), ozfp4.OZFP4_EINVAL),           # ldc < m
