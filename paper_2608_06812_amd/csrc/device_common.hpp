@@ -399,16 +399,17 @@ __device__ __forceinline__ void gemm_res_tile(
   // fragments each for planes p = 0, 1) are refilled from LDS for the next
   // k fragment as soon as their last product group has been issued, so
   // every LDS read has at least one product group (four MFMAs of this wave,
-  // eight of its SIMD) to land in, and the two waves of a SIMD never wait
-  // for their reads at the same time. With product group g_pq = the four
+  // eight of its SIMD) to land in, and the two waves of a SIMD no longer
+  // wait for their reads together at the start of each k fragment. With product group g_pq = the four
   // MFMAs a_p b_q, k fragment 0 of a stage issues g00 g01 g11 g10 and
   // k fragment 1 issues g01 g00 g10 g11: each fragment's last groups free
   // the registers that the next fragment's first groups need last.
   // Modulus 169 has no g11 and issues g10 g00 g01 in both fragments.
   //
   // Stage s + 2 is copied during stage s into the slot of stage s - 1,
-  // which every wave finished reading before the previous barrier, one
-  // copy per wave after each product group before the handover. The
+  // which every wave finished reading before the previous barrier; the six
+  // copies per wave are spread over the product groups before the
+  // handover. The
   // handover (this wave's copies of stage s + 1 landed and its reads of
   // stage s done, then a barrier) comes after the first two groups of
   // k fragment 1 (first one for 169), so the matrix pipe still has eight
