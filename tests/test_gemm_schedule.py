@@ -3,9 +3,10 @@ this repository's own sources (hipcc -S, no GPU needed).
 
 The streaming design relies on the compiler keeping a schedule: per stage a
 fixed number of MFMAs, LDS reads and LDS-DMA copies (global or buffer
-form), one barrier, no
-register spills, and LDS reads issued in batches rather than each one waited
-for before its MFMA. The compiler's schedule can change without any change
+form), one barrier, no register spills, LDS reads issued several at a time
+rather than each one waited for before its MFMA, and (residue, INT8 and
+scheme-I GEMMs) every LDS read issued at least four MFMAs before the wait
+for it. The compiler's schedule can change without any change
 to a kernel's source (a change elsewhere in the translation unit is
 enough); these checks catch a change of these properties before it
 reaches the GPU."""
