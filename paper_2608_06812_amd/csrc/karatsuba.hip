@@ -93,12 +93,14 @@ __device__ __forceinline__ void gemm_res_tile_k(
         for (int v = 0; v < 16; ++v) acc[a][i][j][v] = 0.0f;
 
   // Per stage: P0 (4 MFMAs), read the sum fragments, P2 (4), the handover
-  // (wait for stage s + 1 and this wave's reads, barrier), Ps (4), read c0 /
-  // c1 fragments of stage s + 1. The slot of stage s is free after the
-  // handover barrier and takes stage s + 4: two copies right after the
-  // barrier, two after Ps, the last two between P0 and P2 of stage s + 1,
-  // so no burst of copies holds up the matrix pipes. At a handover at most
-  // the copies of stages s + 2 and s + 3 are in flight.
+  // (wait for stage s + 1 and this wave's reads, barrier), read the c0
+  // fragments of stage s + 1, Ps (4), read its c1 fragments: every read
+  // lands under four MFMAs of the wave before its first use. The slot of
+  // stage s is free after the handover barrier and takes stage s + 4: two
+  // copies right after the barrier, two after Ps, the last two between P0
+  // and P2 of stage s + 1, so no burst of copies holds up the matrix pipes.
+  // At a handover at most the copies of stages s + 2 and s + 3 are in
+  // flight.
 #pragma unroll
   for (int st = 0; st < kRingK - 1; ++st)   // nst >= 6 > kRingK by padding
 #pragma unroll
@@ -110,11 +112,16 @@ __device__ __forceinline__ void gemm_res_tile_k(
 
   v4i a0[2], a1[2], b0[2], b1[2], as[2], bs[2];
   auto slot = [&](int s) { return lds + (s & (kRingK - 1)) * kStageBytesK; };
-  auto read_lo = [&](const uint8_t* sb) {
+  auto read_c0 = [&](const uint8_t* sb) {
 #pragma unroll
     for (int i = 0; i < 2; ++i) {
       a0[i] = *reinterpret_cast<const v4i*>(sb + fragAK(0, rbw + i) + lane16);
       b0[i] = *reinterpret_cast<const v4i*>(sb + fragBK(0, cbw + i) + lane16);
+    }
+  };
+  auto read_c1 = [&](const uint8_t* sb) {
+#pragma unroll
+    for (int i = 0; i < 2; ++i) {
       a1[i] = *reinterpret_cast<const v4i*>(sb + fragAK(1, rbw + i) + lane16);
       b1[i] = *reinterpret_cast<const v4i*>(sb + fragBK(1, cbw + i) + lane16);
     }
@@ -153,11 +160,26 @@ __device__ __forceinline__ void gemm_res_tile_k(
       dma(s + 3, 5);
     }
     read_sum(slot(s));
+    __builtin_amdgcn_sched_barrier(0);   // the sum reads go out before P2
     mfma_p2();
     __builtin_amdgcn_sched_barrier(0);
   };
 
-  read_lo(slot(0));
+  // after the handover of stage s: the c0 reads of stage s + 1, Ps, its c1
+  // reads
+  auto tail = [&](int s) {
+    read_c0(slot(s + 1));
+    __builtin_amdgcn_sched_barrier(0);
+    mfma_ps();
+    __builtin_amdgcn_sched_barrier(0);
+    read_c1(slot(s + 1));
+    __builtin_amdgcn_sched_barrier(0);
+  };
+
+  read_c0(slot(0));
+  __builtin_amdgcn_sched_barrier(0);
+  read_c1(slot(0));
+  __builtin_amdgcn_sched_barrier(0);
   int s = 0;
 #pragma unroll 1
   for (; s + kRingK < nst; ++s) {   // steady state: stage s + 4 exists
@@ -166,33 +188,28 @@ __device__ __forceinline__ void gemm_res_tile_k(
     block_sync();
     dma(s + kRingK, 0);
     dma(s + kRingK, 1);
+    read_c0(slot(s + 1));
     __builtin_amdgcn_sched_barrier(0);
     mfma_ps();
     __builtin_amdgcn_sched_barrier(0);
     dma(s + kRingK, 2);
     dma(s + kRingK, 3);
-    read_lo(slot(s + 1));
+    read_c1(slot(s + 1));
     __builtin_amdgcn_sched_barrier(0);
   }
   // the last four stages
   head(s, true);
   wait_vm_lgkm0<2 * kDmaPerWave>();
   block_sync();
-  mfma_ps();
-  read_lo(slot(s + 1));
-  __builtin_amdgcn_sched_barrier(0);
+  tail(s);
   head(s + 1, false);
   wait_vm_lgkm0<kDmaPerWave>();
   block_sync();
-  mfma_ps();
-  read_lo(slot(s + 2));
-  __builtin_amdgcn_sched_barrier(0);
+  tail(s + 1);
   head(s + 2, false);
   wait_vm_lgkm0<0>();
   block_sync();
-  mfma_ps();
-  read_lo(slot(s + 3));
-  __builtin_amdgcn_sched_barrier(0);
+  tail(s + 2);
   head(s + 3, false);
   mfma_ps();
 

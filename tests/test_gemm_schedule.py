@@ -4,9 +4,9 @@ this repository's own sources (hipcc -S, no GPU needed).
 The streaming design relies on the compiler keeping a schedule: per stage a
 fixed number of MFMAs, LDS reads and LDS-DMA copies (global or buffer
 form), one barrier, no register spills, LDS reads issued several at a time
-rather than each one waited for before its MFMA, and (residue, INT8 and
-scheme-I GEMMs) every LDS read issued at least four MFMAs before the wait
-for it. The compiler's schedule can change without any change
+rather than each one waited for before its MFMA, and (residue, INT8,
+scheme-I and Karatsuba GEMMs) every LDS read issued at least four MFMAs
+before the wait for it. The compiler's schedule can change without any change
 to a kernel's source (a change elsewhere in the translation unit is
 enough); these checks catch a change of these properties before it
 reaches the GPU."""
@@ -163,6 +163,7 @@ def test_no_scaled_mfma_anywhere(asm):
     ("ozfp4.hip", "_ZN5ozfp410k_gemm_res", 24),   # 169, without a1 b1
     ("ozfp4.hip", "_ZN5ozfp49k_gemm_s8", 36),     # three limbs (limb3_sched.hpp)
     ("ozaki1.hip", "_ZN5ozfp410k_gemm_ozi", 36),  # three limbs (limb3_sched.hpp)
+    ("karatsuba.hip", "_ZN5ozfp414k_gemm_res_kar", 12),   # three-product tile
 ])
 def test_gemm_reads_land_under_mfmas(asm, tu, prefix, mfma):
     """The GEMMs refill each operand register from LDS as soon as its last
