@@ -451,6 +451,19 @@ int ozfp4_ozi_partials(int64_t m, int64_t n, int64_t k,
  * blocks in 1..2^22, iterations >= 1. */
 int ozfp4_calib_mfma(int64_t blocks, int64_t iterations, uint32_t seed, float* sink);
 
+/* The same register-only loop on given E2M1 codes, since the power the
+ * matrix cores draw (and so the clock they hold) depends on the data: lane
+ * g of the blocks * 512 threads starts from the 16 words at g * 16 (modulo
+ * nwords) of the DEVICE arrays codes_a and codes_b, in the order a[p][i][w]
+ * (limb plane p, 32-line block i, word w; eight E2M1 codes per word, low
+ * nibble first), and before every k fragment rotates each A word by one code
+ * and each B word by three, so the operands change with every k fragment
+ * while the mix of codes stays that of the arrays. Writes one checksum per
+ * thread to sink[blocks * 512]. Executed flops as for ozfp4_calib_mfma.
+ * blocks in 1..2^22, iterations >= 1, nwords a positive multiple of 16. */
+int ozfp4_calib_mfma_codes(int64_t blocks, int64_t iterations, const uint32_t* codes_a,
+                           const uint32_t* codes_b, int64_t nwords, float* sink);
+
 /* A plain single-product FP4 GEMM, the effective FP4 rate R of the runtime
  * model (Sec. VII-C, Eq. (model)): C = A B in FP32, where A (m x k) and B
  * (k x n) are single planes of E2M1 codes in the limb-plane fragment layout

@@ -4,6 +4,8 @@
 //   * k_calib_mfma: the FP4 matrix-core rate with no memory traffic, on
 //     operands that change with every k fragment (the attainable rate of
 //     the residue GEMM's own register tile and MFMA order);
+//   * k_calib_mfma_codes: the same loop on given codes (the workload's limb
+//     planes), since the power the matrix cores draw depends on the data;
 //   * k_calib_gemm_fp4: a plain single-product FP4 GEMM, C = A B in FP32,
 //     streamed through the same LDS-DMA ring as the residue GEMM: the
 //     effective FP4 rate R of the runtime model (Sec. VII-C, Eq. (model));
@@ -73,6 +75,81 @@ __global__ __launch_bounds__(512, 1) void k_calib_mfma(int64_t iters, uint32_t s
           for (int w = 0; w < 4; ++w) {
             a[p][i][w] ^= (int)r;
             b[p][i][w] ^= (int)(r >> 3 | r << 29);
+          }
+#pragma unroll
+      for (int i = 0; i < 2; ++i)
+#pragma unroll
+        for (int j = 0; j < 2; ++j) {
+          acc[0][i][j] = mfma_fp4(a[0][i], b[0][j], acc[0][i][j]);
+          acc[1][i][j] = mfma_fp4(a[0][i], b[1][j], acc[1][i][j]);
+        }
+#pragma unroll
+      for (int i = 0; i < 2; ++i)
+#pragma unroll
+        for (int j = 0; j < 2; ++j) acc[1][i][j] = mfma_fp4(a[1][i], b[0][j], acc[1][i][j]);
+#pragma unroll
+      for (int i = 0; i < 2; ++i)
+#pragma unroll
+        for (int j = 0; j < 2; ++j) acc[2][i][j] = mfma_fp4(a[1][i], b[1][j], acc[2][i][j]);
+    }
+  }
+  float sum = 0.0f;
+#pragma unroll
+  for (int s = 0; s < 3; ++s)
+#pragma unroll
+    for (int i = 0; i < 2; ++i)
+#pragma unroll
+      for (int j = 0; j < 2; ++j)
+#pragma unroll
+        for (int v = 0; v < 16; ++v) sum += acc[s][i][j][v];
+  sink[gid] = sum;
+}
+
+// The same loop on given E2M1 codes: lane g starts from the 16 A words and
+// 16 B words at g * 16 (modulo nwords) of codes_a / codes_b, in the order of
+// a[p][i][w] (plane, 32-line block, word), and before every k fragment
+// rotates each A word by one code (4 bits) and each B word by three
+// (12 bits). The matrix cores see codes that change with every k fragment,
+// like streamed data, while the mix of codes stays that of the arrays (for
+// instance the workload's own limb planes).
+__global__ __launch_bounds__(512, 1) void k_calib_mfma_codes(int64_t iters,
+                                                             const uint32_t* __restrict__ codes_a,
+                                                             const uint32_t* __restrict__ codes_b,
+                                                             int64_t nwords, float* __restrict__ sink) {
+  const int64_t gid = (int64_t)blockIdx.x * 512 + threadIdx.x;
+  const int64_t base = (gid * 16) % nwords;   // nwords: a multiple of 16
+  v4i a[2][2], b[2][2];
+#pragma unroll
+  for (int p = 0; p < 2; ++p)
+#pragma unroll
+    for (int i = 0; i < 2; ++i)
+#pragma unroll
+      for (int w = 0; w < 4; ++w) {
+        const int idx = (p * 2 + i) * 4 + w;
+        a[p][i][w] = (int)codes_a[base + idx];
+        b[p][i][w] = (int)codes_b[base + idx];
+      }
+  v16f acc[3][2][2];
+#pragma unroll
+  for (int s = 0; s < 3; ++s)
+#pragma unroll
+    for (int i = 0; i < 2; ++i)
+#pragma unroll
+      for (int j = 0; j < 2; ++j)
+#pragma unroll
+        for (int v = 0; v < 16; ++v) acc[s][i][j][v] = 0.0f;
+  for (int64_t it = 0; it < iters; ++it) {
+#pragma unroll
+    for (int kf = 0; kf < 2; ++kf) {
+#pragma unroll
+      for (int p = 0; p < 2; ++p)
+#pragma unroll
+        for (int i = 0; i < 2; ++i)
+#pragma unroll
+          for (int w = 0; w < 4; ++w) {
+            const uint32_t x = (uint32_t)a[p][i][w], y = (uint32_t)b[p][i][w];
+            a[p][i][w] = (int)((x >> 4) | (x << 28));
+            b[p][i][w] = (int)((y >> 12) | (y << 20));
           }
 #pragma unroll
       for (int i = 0; i < 2; ++i)
@@ -186,6 +263,14 @@ __global__ __launch_bounds__(256) void k_calib_dma_read(const uint8_t* __restric
 hipError_t launch_calib_mfma(hipStream_t stream, int64_t blocks, int64_t iters, uint32_t seed,
                              float* sink) {
   hipLaunchKernelGGL(k_calib_mfma, dim3((unsigned)blocks), dim3(512), 0, stream, iters, seed, sink);
+  return hipGetLastError();
+}
+
+hipError_t launch_calib_mfma_codes(hipStream_t stream, int64_t blocks, int64_t iters,
+                                   const uint32_t* codes_a, const uint32_t* codes_b,
+                                   int64_t nwords, float* sink) {
+  hipLaunchKernelGGL(k_calib_mfma_codes, dim3((unsigned)blocks), dim3(512), 0, stream, iters,
+                     codes_a, codes_b, nwords, sink);
   return hipGetLastError();
 }
 

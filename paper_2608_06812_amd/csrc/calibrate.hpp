@@ -13,6 +13,12 @@ namespace ozfp4 {
 hipError_t launch_calib_mfma(hipStream_t stream, int64_t blocks, int64_t iters, uint32_t seed,
                              float* sink);
 
+// the same on given codes: lane g starts from words g * 16 .. g * 16 + 15
+// (modulo nwords, a multiple of 16) of codes_a and codes_b
+hipError_t launch_calib_mfma_codes(hipStream_t stream, int64_t blocks, int64_t iters,
+                                   const uint32_t* codes_a, const uint32_t* codes_b,
+                                   int64_t nwords, float* sink);
+
 // C (FP32, ldc) = A B from one plane each; m, n multiples of 256, k a
 // multiple of 128, at least 384
 hipError_t launch_calib_gemm_fp4(hipStream_t stream, int64_t m, int64_t n, int64_t k,

@@ -1129,6 +1129,14 @@ int ozfp4_calib_mfma(int64_t blocks, int64_t iterations, uint32_t seed, float* s
   return OZFP4_OK;
 }
 
+int ozfp4_calib_mfma_codes(int64_t blocks, int64_t iterations, const uint32_t* codes_a,
+                           const uint32_t* codes_b, int64_t nwords, float* sink) {
+  if (blocks < 1 || blocks > (int64_t(1) << 22) || iterations < 1 || !sink) return OZFP4_EINVAL;
+  if (!codes_a || !codes_b || nwords < 16 || nwords % 16) return OZFP4_EINVAL;
+  HIP_TRY(launch_calib_mfma_codes(g_stream, blocks, iterations, codes_a, codes_b, nwords, sink));
+  return OZFP4_OK;
+}
+
 int ozfp4_calib_gemm_fp4(int64_t m, int64_t n, int64_t k, const uint8_t* plane_a,
                          const uint8_t* plane_b, float* C, int64_t ldc) {
   if (m < kTile || n < kTile || m % kTile || n % kTile || !dims_ok(m, n, k)) return OZFP4_EINVAL;

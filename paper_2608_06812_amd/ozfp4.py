@@ -68,6 +68,7 @@ _SIGNATURES = {
     "ozfp4_ozi_limb_planes": (_int, [_i64, _i64, _i64, _p, _i64, _p, _i64, _int, _p, _p]),
     "ozfp4_ozi_partials": (_int, [_i64, _i64, _i64, _p, _i64, _p, _i64, _int, _p, _i64]),
     "ozfp4_calib_mfma": (_int, [_i64, _i64, ctypes.c_uint32, _p]),
+    "ozfp4_calib_mfma_codes": (_int, [_i64, _i64, _p, _p, _i64, _p]),
     "ozfp4_calib_gemm_fp4": (_int, [_i64, _i64, _i64, _p, _p, _p, _i64]),
     "ozfp4_calib_dma_read": (_int, [_p, _i64, _i64, _p]),
     "ozfp4_profile": (_int, [_int]),
@@ -226,6 +227,10 @@ def ozfp4_ozi_partials(m, n, k, A, lda, B, ldb, n_limbs, H, ldh) -> int:
 
 def ozfp4_calib_mfma(blocks, iterations, seed, sink) -> int:
     return load().ozfp4_calib_mfma(blocks, iterations, seed, sink)
+
+
+def ozfp4_calib_mfma_codes(blocks, iterations, codes_a, codes_b, nwords, sink) -> int:
+    return load().ozfp4_calib_mfma_codes(blocks, iterations, codes_a, codes_b, nwords, sink)
 
 
 def ozfp4_calib_gemm_fp4(m, n, k, plane_a, plane_b, C, ldc) -> int:
@@ -527,6 +532,23 @@ def calib_mfma(blocks: int, iterations: int, seed: int = 1, device=None):
     with _on(device, sink):
         _check(ozfp4_calib_mfma(blocks, iterations, seed & 0xFFFFFFFF, sink.data_ptr()),
                "ozfp4_calib_mfma")
+    return sink, blocks * 8 * iterations * 32 * 131072.0
+
+
+def calib_mfma_codes(blocks: int, iterations: int, codes_a, codes_b):
+    """Launches the register-only FP4 MFMA loop on given codes (int32 device
+    tensors of the same length, a multiple of 16 words, in the order of
+    ozfp4_calib_mfma_codes); returns the checksum tensor and the executed
+    flops."""
+    import torch
+    if codes_a.dtype != torch.int32 or codes_b.dtype != torch.int32:
+        raise ValueError("codes must be int32 tensors")
+    if codes_a.numel() != codes_b.numel() or not (codes_a.is_contiguous() and codes_b.is_contiguous()):
+        raise ValueError("codes_a and codes_b must be contiguous and of the same length")
+    sink = torch.empty(blocks * 512, dtype=torch.float32, device=codes_a.device)
+    with _on(codes_a.device, codes_b, sink):
+        _check(ozfp4_calib_mfma_codes(blocks, iterations, codes_a.data_ptr(), codes_b.data_ptr(),
+                                      codes_a.numel(), sink.data_ptr()), "ozfp4_calib_mfma_codes")
     return sink, blocks * 8 * iterations * 32 * 131072.0
 
 

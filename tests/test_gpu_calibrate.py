@@ -50,3 +50,28 @@ def test_mfma_loop_runs(gpu_lib):
     s = sink.cpu().numpy()
     assert flops == 256 * 8 * 16 * 32 * 131072
     assert np.all(np.isfinite(s)) and np.count_nonzero(s) > s.size // 2
+
+
+def test_mfma_loop_on_codes_exact(gpu_lib):
+    """With every code E2M1 1.0 (nibble 2) each MFMA adds 64 to each of its
+    outputs, and the rotations keep the codes, so every thread's checksum is
+    (2 + 4 + 2) x 4 tiles x 16 values x 64 x iterations = 32768 iterations
+    (exact in FP32). With random codes the loop runs and returns finite
+    sums."""
+    import torch
+    iters = 16
+    ones = torch.full((64,), 0x22222222, dtype=torch.int32, device="cuda")
+    announce("calib_mfma_codes on code 1.0")
+    sink, flops = gpu_lib.calib_mfma_codes(8, iters, ones, ones.clone())
+    torch.cuda.synchronize()
+    assert flops == 8 * 8 * iters * 32 * 131072
+    assert np.all(sink.cpu().numpy() == 32768.0 * iters)
+    g = torch.Generator(device="cpu").manual_seed(5)
+    ca = torch.randint(-2 ** 31, 2 ** 31, (4096,), dtype=torch.int64, generator=g).to(torch.int32).cuda()
+    cb = torch.randint(-2 ** 31, 2 ** 31, (4096,), dtype=torch.int64, generator=g).to(torch.int32).cuda()
+    announce("calib_mfma_codes on random codes")
+    sink, _ = gpu_lib.calib_mfma_codes(256, iters, ca, cb)
+    torch.cuda.synchronize()
+    s = sink.cpu().numpy()
+    assert np.all(np.isfinite(s)) and np.count_nonzero(s) > s.size // 2
+

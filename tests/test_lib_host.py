@@ -403,6 +403,12 @@ def test_binding_argument_checks_on_host():
     ("ozfp4_calib_mfma", (1 << 23, 10, 1, 1)),            # too many blocks
     ("ozfp4_calib_mfma", (8, 0, 1, 1)),                   # no iterations
     ("ozfp4_calib_mfma", (8, 10, 1, 0)),                  # null sink
+    ("ozfp4_calib_mfma_codes", (0, 10, 1, 1, 16, 1)),     # no blocks
+    ("ozfp4_calib_mfma_codes", (8, 0, 1, 1, 16, 1)),      # no iterations
+    ("ozfp4_calib_mfma_codes", (8, 10, 1, 1, 24, 1)),     # words not a multiple of 16
+    ("ozfp4_calib_mfma_codes", (8, 10, 1, 1, 0, 1)),      # no words
+    ("ozfp4_calib_mfma_codes", (8, 10, 0, 1, 16, 1)),     # null codes
+    ("ozfp4_calib_mfma_codes", (8, 10, 1, 1, 16, 0)),     # null sink
     ("ozfp4_calib_gemm_fp4", (300, 256, 384, 1, 1, 1, 300)),    # m not a multiple of 256
     ("ozfp4_calib_gemm_fp4", (256, 0, 384, 1, 1, 1, 256)),      # n = 0
     ("ozfp4_calib_gemm_fp4", (256, 256, 256, 1, 1, 1, 256)),    # k below three stages
